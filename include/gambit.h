@@ -1,0 +1,213 @@
+/*
+ * gambit.h - C ABI of the population-decode hot path of thought-level beam
+ * search on MI355X (gfx950).
+ *
+ * A population of reasoning traces decodes in lock step.  Their KV caches
+ * live in one pool of fixed-size blocks; a trace is a row of block ids.
+ * Branching spawns a child from its parent's prefix by sharing the parent's
+ * KV blocks (Alg. 1 notation, "Branch"; Sec. 4.1 Case 2: the child inherits
+ * the parent's KV-cache through prefix caching), and pruning frees the
+ * blocks nobody else references (Sec. 4.1 Case 2).  Every decode step
+ * appends one token per trace and attends over the whole context; blocks
+ * shared by several traces are read from HBM once per step for all of them.
+ * At thought boundaries a probe scores every trace, the population is
+ * ranked by score, the bottom is pruned and the top is branched (Alg. 1
+ * Tournament; Eqs. 2-3).
+ *
+ * Memory ownership
+ *   The caller owns ALL device memory: the K/V pools, the fp8 scales, the
+ *   block table, the lengths, the refcounts, the workspace, and every input
+ *   and output buffer.  The library owns only the host-side pool handle and
+ *   its host mirror of the bookkeeping (lengths, block table, refcounts,
+ *   free set, attention plan).  No entry point calls hipMalloc.
+ *
+ * Pointers
+ *   "host" pointers are ordinary CPU memory, read before the call returns.
+ *   "device" pointers are HIP device memory on the device that was current
+ *   when the pool was created.  `stream` is a hipStream_t (NULL = the null
+ *   stream).  A pool is used from one stream and one thread at a time.
+ *
+ * Errors
+ *   Arguments are validated on the host against the host mirror before any
+ *   work is enqueued; a call that returns an error has changed nothing.
+ *   Out-of-blocks is detected the same way (the mirror knows every length
+ *   and the free count).  Device-side invariant violations set an error word
+ *   that gambit_pool_check() reports.  gambit_last_error() returns the text
+ *   of the last error on a pool.
+ *
+ * Block allocation rule (all calls): a new block is the lowest free block
+ * id; requests are served in the call's list order and, inside one trace,
+ * in ascending logical block index.  The rule makes every block table a
+ * deterministic function of the call sequence.
+ */
+#ifndef GAMBIT_H
+#define GAMBIT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t gambit_status;
+
+enum {
+  GAMBIT_OK = 0,
+  GAMBIT_ERR_INVALID = -1,        /* bad argument, id, length or state      */
+  GAMBIT_ERR_OUT_OF_BLOCKS = -2,  /* the pool has too few free blocks       */
+  GAMBIT_ERR_SHARED_WRITE = -3,   /* write into a block another trace holds */
+  GAMBIT_ERR_UNSUPPORTED = -4,    /* shape the kernels do not implement     */
+  GAMBIT_ERR_DEVICE = -5,         /* HIP error or device invariant violated */
+  GAMBIT_ERR_WORKSPACE = -6       /* workspace smaller than required        */
+};
+
+enum { GAMBIT_KV_BF16 = 0, GAMBIT_KV_FP8_E4M3 = 1 };
+enum { GAMBIT_OUT_BF16 = 0, GAMBIT_OUT_F32 = 1 };
+
+typedef struct gambit_pool gambit_pool;
+
+/*
+ * Pool description.  Layouts (all device memory, caller-owned):
+ *   k_cache, v_cache  [num_blocks][num_kv_heads][block_size][head_dim]
+ *                     bf16, or OCP E4M3FN bytes for GAMBIT_KV_FP8_E4M3
+ *   kv_scale          [num_blocks][2] fp32 (K scale, V scale); fp8 only,
+ *                     NULL for bf16.  A stored fp8 value means code * scale.
+ *   block_table       [max_traces][max_blocks_per_trace] int32, -1 = none
+ *   seq_len           [max_traces] int32
+ *   refcount          [num_blocks] int32
+ *   workspace         >= gambit_workspace_size(desc) bytes, 256-B aligned
+ * The pool initialises tables, lengths and refcounts itself.
+ */
+typedef struct {
+  int32_t num_blocks;
+  int32_t block_size;            /* must be 16                              */
+  int32_t num_q_heads;           /* Hq                                      */
+  int32_t num_kv_heads;          /* Hkv; Hq / Hkv in {1, 2, 4, 8, 16}       */
+  int32_t head_dim;              /* must be 128                             */
+  int32_t kv_dtype;              /* GAMBIT_KV_*                             */
+  int32_t max_traces;            /* trace ids are 0 .. max_traces-1         */
+  int32_t max_blocks_per_trace;
+  int32_t max_splits;            /* attention partials per (trace, head); 0 = 64 */
+  float fp8_append_scale;        /* scale of blocks a decode step allocates; 0 = 2^-6 */
+  void* k_cache;
+  void* v_cache;
+  float* kv_scale;
+  int32_t* block_table;
+  int32_t* seq_len;
+  int32_t* refcount;
+  void* workspace;
+  size_t workspace_bytes;
+} gambit_pool_desc;
+
+/* Plan statistics of a trace list under the pool's current state (host only). */
+typedef struct {
+  int64_t total_tokens;          /* sum of lengths over the listed traces        */
+  int64_t unique_tokens;         /* valid tokens of the distinct blocks they use */
+  int64_t unique_blocks;         /* distinct blocks they use                     */
+  int32_t n_units;               /* attention work units of the current plan     */
+  int32_t max_splits_used;       /* largest number of partials of one trace      */
+} gambit_stats;
+
+/* Workspace bytes the description needs; 0 when the description is invalid. */
+size_t gambit_workspace_size(const gambit_pool_desc* desc);
+
+/* Create a pool over caller-owned memory; enqueues its initialisation on
+ * `stream`.  *out receives the handle. */
+gambit_status gambit_pool_create(const gambit_pool_desc* desc, void* stream, gambit_pool** out);
+gambit_status gambit_pool_destroy(gambit_pool* pool);
+
+/* Extend each listed trace by n_tokens[i] positions (allocation rule above).
+ * trace_ids, n_tokens: host [n].  The new positions hold no data until
+ * written.  fp8: new blocks get scale (1, 1). */
+gambit_status gambit_kv_alloc(gambit_pool* pool, int32_t n, const int32_t* trace_ids,
+                              const int32_t* n_tokens, void* stream);
+
+/* Write n tokens of K and V at positions pos0 .. pos0+n-1 of a trace.
+ * k, v: device [n][num_kv_heads][head_dim] in the cache dtype.  Every touched
+ * block must be held by this trace alone (else GAMBIT_ERR_SHARED_WRITE).
+ * fp8: scales is host [m][2] for the m blocks whose first position lies in
+ * [pos0, pos0+n), ascending; the codes of tokens in other blocks must
+ * already be quantised with those blocks' scales.  bf16: scales is NULL. */
+gambit_status gambit_kv_write(gambit_pool* pool, int32_t trace_id, int32_t pos0, int32_t n,
+                              const void* k, const void* v, const float* scales, void* stream);
+
+/* Branch (Alg. 1 notation; Sec. 4.1 Case 2): child_ids[i] starts from the
+ * prefix of parent_ids[i].  The child row lists the parent's full blocks
+ * (refcount + 1 each); a partial last block is copied into one new block
+ * (with its fp8 scales); the child's length equals the parent's.  Children
+ * must be empty, distinct, and not parents in the same call.
+ * parent_ids, child_ids: host [n]. */
+gambit_status gambit_kv_fork(gambit_pool* pool, int32_t n, const int32_t* parent_ids,
+                             const int32_t* child_ids, void* stream);
+
+/* Prune (Sec. 4.1 Case 2): every block of each listed trace loses one
+ * reference and becomes free at zero; the row empties and the length
+ * becomes 0.  trace_ids: host [n]; freeing an empty trace is an error. */
+gambit_status gambit_kv_free(gambit_pool* pool, int32_t n, const int32_t* trace_ids, void* stream);
+
+/* One decode step for the listed traces (Alg. 1 Generate, attention part):
+ * append k_new/v_new at position seq_len (taking a new block when seq_len is
+ * a multiple of 16; fp8 blocks taken here get fp8_append_scale), then for
+ * every trace t and query head h, with G = h / (Hq / Hkv),
+ *     out[t][h] = softmax(q[t][h] . K_t[:, G]^T * sm_scale) V_t[:, G]
+ * over all seq_len + 1 positions.  Blocks shared by several listed traces
+ * are read once for all of them.
+ *   trace_ids  host [n], distinct, each with seq_len > 0
+ *   q          device [n][Hq][head_dim] bf16
+ *   k_new,v_new device [n][Hkv][head_dim] cache dtype (fp8: codes for the
+ *              scale of the block the token lands in)
+ *   out        device [n][Hq][head_dim], bf16 or fp32 (out_dtype) */
+gambit_status gambit_decode_attn(gambit_pool* pool, int32_t n, const int32_t* trace_ids,
+                                 const void* q, const void* k_new, const void* v_new,
+                                 void* out, int32_t out_dtype, float sm_scale, void* stream);
+
+/* A thought boundary (Alg. 1 Tournament; Eqs. 2-3; Sec. 4.1):
+ *   score[i] = 1 / (1 + exp(-(h[i] . w + b)))   (linear sigmoid probe, the
+ *              head form of Eq. 6 applied to the boundary hidden state)
+ *   rank the listed traces by (score descending, trace id ascending);
+ *   keep_out = the first `keep` ids in rank order;
+ *   prune the other n - keep traces (ascending id);
+ *   branch: with c = (n - keep) / n_parents, freed slot j (ascending) becomes
+ *   a child of keep_out[j / c]; the parent keeps running (App. A.5).
+ * The paper's Case 2 is keep = C - K, n_parents = K (c = 1).
+ *   trace_ids        host [n]
+ *   h                device [n][Dh] bf16, in list order
+ *   w                device [Dh] fp32;  b: bias
+ *   scores_out       device [n] fp32, list order
+ *   keep_out         device [keep] int32, rank order
+ *   child_parent_out device [n - keep][2] int32 (child id, parent id)
+ * Blocks until the ranking is known on the host (one device-to-host copy). */
+gambit_status gambit_score_prune_branch(gambit_pool* pool, int32_t n, const int32_t* trace_ids,
+                                        const void* h, int32_t Dh, const float* w, float b,
+                                        int32_t keep, int32_t n_parents, float* scores_out,
+                                        int32_t* keep_out, int32_t* child_parent_out,
+                                        void* stream);
+
+/* Stateless ranking (the selection step of Alg. 1 Tournament): keep_out[r]
+ * = the id of rank r under (score descending, id ascending), r < keep.
+ * trace_ids, scores: device [n]; keep_out: device [keep]; n <= 4096. */
+gambit_status gambit_rank_topk(int32_t n, const int32_t* trace_ids, const float* scores,
+                               int32_t keep, int32_t* keep_out, void* stream);
+
+/* Synchronise `stream`, then compare the device block table, lengths,
+ * refcounts and free set with the host mirror and read the device error
+ * word.  GAMBIT_OK when all agree. */
+gambit_status gambit_pool_check(gambit_pool* pool, void* stream);
+
+/* Statistics of the attention work for a trace list (host only, no sync). */
+gambit_status gambit_plan_stats(gambit_pool* pool, int32_t n, const int32_t* trace_ids,
+                                gambit_stats* out);
+
+/* Host mirror queries (no sync): length of a trace; free block count. */
+int32_t gambit_seq_len(const gambit_pool* pool, int32_t trace_id);
+int32_t gambit_free_blocks(const gambit_pool* pool);
+
+const char* gambit_status_str(gambit_status s);
+const char* gambit_last_error(const gambit_pool* pool);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GAMBIT_H */

@@ -1,0 +1,287 @@
+// Block-table kernels: pool initialisation, lowest-free-first allocation,
+// KV writes, prune (free) and branch (fork).
+//
+// Branch spawns a child from its parent's prefix by sharing the parent's KV
+// blocks (Alg. 1 notation; Sec. 4.1 Case 2), so a fork copies block ids and
+// bumps refcounts; only a partially filled last block is copied, because
+// both traces keep appending into their own copy of it.  Prune frees the
+// blocks nobody else references (Sec. 4.1 Case 2).
+#include "kernels.h"
+
+namespace gambit {
+namespace {
+
+constexpr int kAllocThreads = 1024;
+
+__device__ inline int cdiv16(int x) { return (x + kBlock - 1) / kBlock; }
+
+__global__ void pool_init_kernel(DevPool P) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  const size_t i0 = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t ntab = (size_t)P.max_traces * P.max_blocks;
+  for (size_t i = i0; i < ntab; i += stride) P.table[i] = -1;
+  for (size_t i = i0; i < (size_t)P.max_traces; i += stride) P.seq_len[i] = 0;
+  for (size_t i = i0; i < (size_t)P.num_blocks; i += stride) P.refcount[i] = 0;
+  for (size_t w = i0; w < (size_t)P.nwords; w += stride) {
+    const int lo = (int)w * 32;
+    const int valid = min(32, P.num_blocks - lo);
+    P.freebits[w] = valid >= 32 ? 0xFFFFFFFFu : ((1u << valid) - 1u);
+  }
+  if (i0 == 0) *P.err = 0;
+}
+
+// Exclusive scan of one int per thread across the workgroup (kAllocThreads).
+__device__ int wg_exclusive_scan(int v, int* total) {
+  __shared__ int s[kAllocThreads];
+  const int t = threadIdx.x;
+  s[t] = v;
+  __syncthreads();
+  for (int off = 1; off < kAllocThreads; off <<= 1) {
+    const int x = t >= off ? s[t - off] : 0;
+    __syncthreads();
+    s[t] += x;
+    __syncthreads();
+  }
+  const int incl = s[t];
+  *total = s[kAllocThreads - 1];
+  __syncthreads();
+  return incl - v;
+}
+
+// One workgroup.  Request i extends trace req_trace[i] by its token count;
+// the blocks it needs are the next lowest free ids, in request order and
+// ascending logical index.
+__global__ __launch_bounds__(kAllocThreads) void alloc_kernel(DevPool P, const int32_t* req_trace,
+                                                             const int32_t* req_ntok, int32_t uniform,
+                                                             int32_t m, float new_scale) {
+  const int t = threadIdx.x;
+  const int rpt = (m + kAllocThreads - 1) / kAllocThreads;
+  const int r0 = min(m, t * rpt), r1 = min(m, r0 + rpt);
+  int need = 0;
+  for (int i = r0; i < r1; ++i) {
+    const int L = P.seq_len[req_trace[i]];
+    const int nt = uniform >= 0 ? uniform : req_ntok[i];
+    need += cdiv16(L + nt) - cdiv16(L);
+  }
+  int total = 0;
+  const int base = wg_exclusive_scan(need, &total);
+  if (total > 0) {  // uniform across the workgroup
+    const int wpt = (P.nwords + kAllocThreads - 1) / kAllocThreads;
+    const int w0 = min(P.nwords, t * wpt), w1 = min(P.nwords, w0 + wpt);
+    int nfree = 0;
+    for (int w = w0; w < w1; ++w) nfree += __popc(P.freebits[w]);
+    int avail = 0;
+    int rank = wg_exclusive_scan(nfree, &avail);
+    if (avail < total) {  // the host mirror rules this out; leave the pool untouched
+      if (t == 0) atomicOr(P.err, kErrAllocShort);
+      return;
+    }
+    for (int w = w0; w < w1 && rank < total; ++w) {
+      uint32_t bits = P.freebits[w];
+      while (bits && rank < total) {
+        const int bit = __ffs(bits) - 1;
+        bits &= bits - 1;
+        P.alloc_list[rank++] = w * 32 + bit;
+        P.freebits[w] &= ~(1u << bit);
+      }
+    }
+    __syncthreads();
+  }
+  int off = base;
+  for (int i = r0; i < r1; ++i) {
+    const int tr = req_trace[i];
+    const int L = P.seq_len[tr];
+    const int nt = uniform >= 0 ? uniform : req_ntok[i];
+    const int j0 = cdiv16(L), j1 = cdiv16(L + nt);
+    int32_t* row = P.table + (size_t)tr * P.max_blocks;
+    for (int j = j0; j < j1; ++j) {
+      const int b = P.alloc_list[off++];
+      row[j] = b;
+      P.refcount[b] = 1;
+      if (P.kv_scale) {
+        P.kv_scale[2 * b] = new_scale;
+        P.kv_scale[2 * b + 1] = new_scale;
+      }
+    }
+    P.seq_len[tr] = L + nt;
+  }
+}
+
+// Copy one token's K and V (all KV heads) into the cache.  One workgroup per
+// token; chunks of 16 bytes.
+__device__ inline void copy_token(const DevPool& P, int blk, int row, const uint8_t* ksrc,
+                                  const uint8_t* vsrc) {
+  const int row_bytes = kHeadDim * P.esize;           // one head, one token
+  const int chunks = P.Hkv * row_bytes / 16;
+  for (int c = threadIdx.x; c < chunks; c += blockDim.x) {
+    const int head = c / (row_bytes / 16);
+    const int cc = c % (row_bytes / 16);
+    const size_t dst = (((size_t)blk * P.Hkv + head) * kBlock + row) * row_bytes + cc * 16;
+    const size_t src = (size_t)head * row_bytes + cc * 16;
+    *reinterpret_cast<uint4*>(P.k_cache + dst) = *reinterpret_cast<const uint4*>(ksrc + src);
+    *reinterpret_cast<uint4*>(P.v_cache + dst) = *reinterpret_cast<const uint4*>(vsrc + src);
+  }
+}
+
+__global__ void write_kernel(DevPool P, int32_t trace, int32_t pos0, const uint8_t* k,
+                             const uint8_t* v, const float* started_scales) {
+  const int i = blockIdx.x;
+  const int pos = pos0 + i;
+  const int blk = P.table[(size_t)trace * P.max_blocks + pos / kBlock];
+  if ((unsigned)blk >= (unsigned)P.num_blocks) {
+    if (threadIdx.x == 0) atomicOr(P.err, kErrBadBlock);
+    return;
+  }
+  const size_t tok_bytes = (size_t)P.Hkv * kHeadDim * P.esize;
+  copy_token(P, blk, pos % kBlock, k + i * tok_bytes, v + i * tok_bytes);
+  if (started_scales && threadIdx.x == 0 && pos % kBlock == 0) {
+    const int first = (pos0 + kBlock - 1) / kBlock * kBlock;
+    const int k2 = (pos - first) / kBlock;
+    P.kv_scale[2 * blk] = started_scales[2 * k2];
+    P.kv_scale[2 * blk + 1] = started_scales[2 * k2 + 1];
+  }
+}
+
+// The decode step's append: list position i writes its new token at
+// position seq_len - 1 (the allocator already advanced seq_len).
+__global__ void append_write_kernel(DevPool P, const int32_t* list, const uint8_t* k_new,
+                                    const uint8_t* v_new) {
+  const int i = blockIdx.x;
+  const int tr = list[i];
+  const int pos = P.seq_len[tr] - 1;
+  const int blk = pos >= 0 ? P.table[(size_t)tr * P.max_blocks + pos / kBlock] : -1;
+  if ((unsigned)blk >= (unsigned)P.num_blocks) {
+    if (threadIdx.x == 0) atomicOr(P.err, kErrBadBlock);
+    return;
+  }
+  const size_t tok_bytes = (size_t)P.Hkv * kHeadDim * P.esize;
+  copy_token(P, blk, pos % kBlock, k_new + i * tok_bytes, v_new + i * tok_bytes);
+}
+
+// Prune: one workgroup per trace.
+__global__ void free_kernel(DevPool P, const int32_t* ids) {
+  const int tr = ids[blockIdx.x];
+  const int nb = cdiv16(P.seq_len[tr]);
+  int32_t* row = P.table + (size_t)tr * P.max_blocks;
+  for (int j = threadIdx.x; j < nb; j += blockDim.x) {
+    const int b = row[j];
+    row[j] = -1;
+    if (b < 0 || b >= P.num_blocks) {
+      atomicOr(P.err, kErrBadBlock);
+      continue;
+    }
+    const int old = atomicSub(&P.refcount[b], 1);
+    if (old == 1) atomicOr(&P.freebits[b >> 5], 1u << (b & 31));
+    if (old < 1) atomicOr(P.err, kErrRefUnderflow);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) P.seq_len[tr] = 0;
+}
+
+// Branch, part 1: the child row takes the parent's full blocks (refcount + 1)
+// and the child length is set to the full-block prefix; the partial tail is
+// requested from the allocator (req_ntok = parent length mod 16).
+__global__ void fork_share_kernel(DevPool P, const int32_t* pairs, int32_t* req_trace,
+                                  int32_t* req_ntok) {
+  const int child = pairs[2 * blockIdx.x], parent = pairs[2 * blockIdx.x + 1];
+  const int L = P.seq_len[parent];
+  const int full = L / kBlock;
+  const int32_t* prow = P.table + (size_t)parent * P.max_blocks;
+  int32_t* crow = P.table + (size_t)child * P.max_blocks;
+  for (int j = threadIdx.x; j < full; j += blockDim.x) {
+    const int b = prow[j];
+    crow[j] = b;
+    if ((unsigned)b < (unsigned)P.num_blocks)
+      atomicAdd(&P.refcount[b], 1);
+    else
+      atomicOr(P.err, kErrBadBlock);
+  }
+  if (threadIdx.x == 0) {
+    P.seq_len[child] = full * kBlock;
+    req_trace[blockIdx.x] = child;
+    req_ntok[blockIdx.x] = L % kBlock;
+  }
+}
+
+// Branch, part 2: copy the partial tail (valid tokens, every KV head) and
+// its fp8 scales into the child's new block.
+__global__ void fork_tail_kernel(DevPool P, const int32_t* pairs) {
+  const int child = pairs[2 * blockIdx.x], parent = pairs[2 * blockIdx.x + 1];
+  const int L = P.seq_len[parent];
+  const int tail = L % kBlock;
+  if (tail == 0) return;
+  const int j = L / kBlock;
+  const int src = P.table[(size_t)parent * P.max_blocks + j];
+  const int dst = P.table[(size_t)child * P.max_blocks + j];
+  if ((unsigned)src >= (unsigned)P.num_blocks || (unsigned)dst >= (unsigned)P.num_blocks) {
+    if (threadIdx.x == 0) atomicOr(P.err, kErrBadBlock);
+    return;
+  }
+  const int row_bytes = kHeadDim * P.esize;
+  const int chunks_per_row = row_bytes / 16;
+  const int chunks = P.Hkv * tail * chunks_per_row;
+  for (int c = threadIdx.x; c < chunks; c += blockDim.x) {
+    const int head = c / (tail * chunks_per_row);
+    const int rem = c % (tail * chunks_per_row);
+    const int row = rem / chunks_per_row, cc = rem % chunks_per_row;
+    const size_t so = (((size_t)src * P.Hkv + head) * kBlock + row) * row_bytes + cc * 16;
+    const size_t d0 = (((size_t)dst * P.Hkv + head) * kBlock + row) * row_bytes + cc * 16;
+    *reinterpret_cast<uint4*>(P.k_cache + d0) = *reinterpret_cast<const uint4*>(P.k_cache + so);
+    *reinterpret_cast<uint4*>(P.v_cache + d0) = *reinterpret_cast<const uint4*>(P.v_cache + so);
+  }
+  if (P.kv_scale && threadIdx.x == 0) {
+    P.kv_scale[2 * dst] = P.kv_scale[2 * src];
+    P.kv_scale[2 * dst + 1] = P.kv_scale[2 * src + 1];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_pool_init(const DevPool& P, hipStream_t s) {
+  hipLaunchKernelGGL(pool_init_kernel, dim3(1024), dim3(256), 0, s, P);
+  return hipGetLastError();
+}
+
+hipError_t launch_alloc(const DevPool& P, const int32_t* req_trace, const int32_t* req_ntok,
+                        int32_t uniform_ntok, int32_t m, float new_scale, hipStream_t s) {
+  if (m <= 0) return hipSuccess;
+  hipLaunchKernelGGL(alloc_kernel, dim3(1), dim3(kAllocThreads), 0, s, P, req_trace, req_ntok,
+                     uniform_ntok, m, new_scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_write(const DevPool& P, int32_t trace, int32_t pos0, int32_t n, const void* k,
+                        const void* v, const float* started_scales, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(write_kernel, dim3(n), dim3(128), 0, s, P, trace, pos0,
+                     static_cast<const uint8_t*>(k), static_cast<const uint8_t*>(v), started_scales);
+  return hipGetLastError();
+}
+
+hipError_t launch_append_write(const DevPool& P, const int32_t* list, int32_t n, const void* k_new,
+                               const void* v_new, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(append_write_kernel, dim3(n), dim3(128), 0, s, P, list,
+                     static_cast<const uint8_t*>(k_new), static_cast<const uint8_t*>(v_new));
+  return hipGetLastError();
+}
+
+hipError_t launch_free(const DevPool& P, const int32_t* ids, int32_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(free_kernel, dim3(n), dim3(256), 0, s, P, ids);
+  return hipGetLastError();
+}
+
+hipError_t launch_fork(const DevPool& P, const int32_t* pairs, int32_t n, int32_t* req_trace,
+                       int32_t* req_ntok, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fork_share_kernel, dim3(n), dim3(256), 0, s, P, pairs, req_trace, req_ntok);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = launch_alloc(P, req_trace, req_ntok, -1, n, 1.0f, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(fork_tail_kernel, dim3(n), dim3(256), 0, s, P, pairs);
+  return hipGetLastError();
+}
+
+}  // namespace gambit

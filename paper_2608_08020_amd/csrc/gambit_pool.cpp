@@ -1,0 +1,821 @@
+// Host side of libgambit: the pool handle, its host mirror of the block
+// bookkeeping, argument validation, the shared-run attention planner and the
+// C ABI entry points declared in include/gambit.h.
+//
+// The mirror applies exactly the allocation rule the device kernels apply
+// (lowest free block id first, requests in list order, ascending logical
+// index), so it always knows every length, every table row and the free
+// count without reading the device.  That lets every call validate and
+// detect out-of-blocks before it enqueues anything, and lets the planner
+// find which traces share which blocks.  The one device-to-host read on the
+// hot path is the ranking at a thought boundary.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <numeric>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "../../include/gambit.h"
+#include "kernels.h"
+
+using gambit::AttnUnit;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kDefaultSplits = 64;
+constexpr int kDefaultChunkBlocks = 64;  // blocks per attention chunk before balancing
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+// Workspace carve-up.  All offsets are kAlign-aligned.
+struct Layout {
+  size_t list, ids, req_trace, req_ntok, pairs, free_list, nk, ticket, err, scales, freebits,
+      alloc_list, units, members, part_ml, part_acc, total;
+  int kmax, max_units, max_members, nwords;
+};
+
+bool layout_of(const gambit_pool_desc* d, Layout* L) {
+  if (!d) return false;
+  if (d->num_blocks <= 0 || d->block_size != gambit::kBlock || d->head_dim != gambit::kHeadDim)
+    return false;
+  if (d->num_q_heads <= 0 || d->num_kv_heads <= 0 || d->num_q_heads % d->num_kv_heads) return false;
+  const int g = d->num_q_heads / d->num_kv_heads;
+  if (g != 1 && g != 2 && g != 4 && g != 8 && g != 16) return false;
+  if (d->kv_dtype != GAMBIT_KV_BF16 && d->kv_dtype != GAMBIT_KV_FP8_E4M3) return false;
+  if (d->max_traces <= 0 || d->max_blocks_per_trace <= 0 || d->max_splits < 0) return false;
+  const int T = d->max_traces;
+  const int kmax = d->max_splits ? d->max_splits : kDefaultSplits;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  L->kmax = kmax;
+  L->nwords = cdiv(d->num_blocks, 32);
+  L->max_units = T * kmax * d->num_kv_heads;
+  L->max_members = T * kmax;
+  L->list = take(4 * (size_t)T);
+  L->ids = take(4 * (size_t)T);
+  L->req_trace = take(4 * (size_t)T);
+  L->req_ntok = take(4 * (size_t)T);
+  L->pairs = take(8 * (size_t)T);
+  L->free_list = take(4 * (size_t)T);
+  L->nk = take(4 * (size_t)T);
+  L->ticket = take(64);
+  L->err = take(64);
+  L->scales = take(8 * ((size_t)d->max_blocks_per_trace + 1));
+  L->freebits = take(4 * (size_t)L->nwords);
+  L->alloc_list = take(4 * (size_t)d->num_blocks);
+  L->units = take(sizeof(AttnUnit) * (size_t)L->max_units);
+  L->members = take(4 * (size_t)L->max_members);
+  L->part_ml = take(8 * (size_t)T * d->num_q_heads * kmax);
+  L->part_acc = take(4 * (size_t)T * d->num_q_heads * kmax * gambit::kHeadDim);
+  L->total = o;
+  return true;
+}
+
+}  // namespace
+
+struct gambit_pool {
+  gambit_pool_desc d{};
+  Layout L{};
+  gambit::DevPool dev{};
+  uint8_t* ws = nullptr;
+  int g = 1;
+  float append_scale = 1.f / 64.f;
+
+  // host mirror
+  std::vector<std::vector<int32_t>> table;
+  std::vector<int32_t> seq_len, refcount;
+  std::vector<uint64_t> freebits;  // bit set = free
+  int32_t nfree = 0;
+  size_t hint = 0;                 // no free bit below word `hint`
+
+  // pinned staging for host-to-device copies, reused after an event fence
+  int32_t* stage = nullptr;
+  size_t stage_ints = 0;
+  hipEvent_t stage_ev = nullptr;
+  uint8_t* plan_stage = nullptr;
+  size_t plan_stage_bytes = 0;
+  hipEvent_t plan_ev = nullptr;
+
+  // attention plan
+  bool plan_valid = false;
+  std::vector<int32_t> plan_list;
+  int xcd_off[9] = {0};
+  int grid = 0;
+  int n_units = 0;
+  int max_splits_used = 0;
+  std::vector<int32_t> cnt, first, csr_off, csr_fill, csr;  // per-block planner scratch
+
+  std::string last_error;
+};
+
+namespace {
+
+gambit_status fail(gambit_pool* p, gambit_status s, const char* fmt, ...) {
+  if (p) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    p->last_error = buf;
+  }
+  return s;
+}
+
+gambit_status hip_fail(gambit_pool* p, hipError_t e, const char* where) {
+  return fail(p, GAMBIT_ERR_DEVICE, "%s: %s", where, hipGetErrorString(e));
+}
+
+#define HIP_TRY(p, expr, where)                 \
+  do {                                          \
+    const hipError_t e_ = (expr);               \
+    if (e_ != hipSuccess) return hip_fail(p, e_, where); \
+  } while (0)
+
+inline hipStream_t S(void* s) { return static_cast<hipStream_t>(s); }
+
+template <class T>
+T* ws_ptr(gambit_pool* p, size_t off) {
+  return reinterpret_cast<T*>(p->ws + off);
+}
+
+// ---- host mirror -----------------------------------------------------------
+int take_lowest(gambit_pool* p) {
+  for (size_t w = p->hint; w < p->freebits.size(); ++w) {
+    if (p->freebits[w]) {
+      const int bit = __builtin_ctzll(p->freebits[w]);
+      p->freebits[w] &= p->freebits[w] - 1;
+      p->hint = w;
+      --p->nfree;
+      return (int)(w * 64 + bit);
+    }
+  }
+  return -1;
+}
+
+void release(gambit_pool* p, int b) {
+  p->freebits[b >> 6] |= 1ull << (b & 63);
+  p->hint = std::min(p->hint, (size_t)(b >> 6));
+  ++p->nfree;
+}
+
+void mirror_grow(gambit_pool* p, int t, int ntok) {
+  const int L = p->seq_len[t];
+  for (int j = cdiv(L, 16); j < cdiv(L + ntok, 16); ++j) {
+    const int b = take_lowest(p);
+    p->refcount[b] = 1;
+    p->table[t].push_back(b);
+  }
+  p->seq_len[t] = L + ntok;
+}
+
+void mirror_fork(gambit_pool* p, int parent, int child) {
+  const int L = p->seq_len[parent];
+  const int full = L / 16;
+  auto& c = p->table[child];
+  c.assign(p->table[parent].begin(), p->table[parent].begin() + full);
+  for (int b : c) ++p->refcount[b];
+  p->seq_len[child] = full * 16;
+  mirror_grow(p, child, L % 16);
+}
+
+void mirror_free(gambit_pool* p, int t) {
+  for (int b : p->table[t])
+    if (--p->refcount[b] == 0) release(p, b);
+  p->table[t].clear();
+  p->seq_len[t] = 0;
+}
+
+// ---- staging ---------------------------------------------------------------
+// Copies `n` ints from host memory into device memory `dst` on `stream`
+// through the pinned staging buffer.
+gambit_status upload_ints(gambit_pool* p, int32_t* dst, const int32_t* src, size_t n, hipStream_t s,
+                          size_t stage_off = 0) {
+  if (n == 0) return GAMBIT_OK;
+  HIP_TRY(p, hipEventSynchronize(p->stage_ev), "staging fence");
+  std::memcpy(p->stage + stage_off, src, n * 4);
+  HIP_TRY(p, hipMemcpyAsync(dst, p->stage + stage_off, n * 4, hipMemcpyHostToDevice, s), "upload");
+  HIP_TRY(p, hipEventRecord(p->stage_ev, s), "staging fence");
+  return GAMBIT_OK;
+}
+
+gambit_status check_ids(gambit_pool* p, int32_t n, const int32_t* ids, const char* what,
+                        std::vector<char>* seen_out = nullptr) {
+  if (n < 0 || n > p->d.max_traces) return fail(p, GAMBIT_ERR_INVALID, "%s count %d out of range", what, n);
+  if (n > 0 && !ids) return fail(p, GAMBIT_ERR_INVALID, "%s list is NULL", what);
+  std::vector<char> seen(p->d.max_traces, 0);
+  for (int i = 0; i < n; ++i) {
+    const int t = ids[i];
+    if (t < 0 || t >= p->d.max_traces) return fail(p, GAMBIT_ERR_INVALID, "%s id %d out of range", what, t);
+    if (seen[t]) return fail(p, GAMBIT_ERR_INVALID, "duplicate %s id %d", what, t);
+    seen[t] = 1;
+  }
+  if (seen_out) seen_out->swap(seen);
+  return GAMBIT_OK;
+}
+
+// ---- planner ---------------------------------------------------------------
+// Cuts every listed trace's context into runs of blocks referenced by the
+// same set of listed traces.  Sharing only ever comes from forks, which hand
+// the child the parent's whole full-block prefix, so along one trace the set
+// of sharers can only shrink; two consecutive blocks with equal sharer
+// counts therefore have equal sharer sets.  A shared run is emitted once, by
+// its lowest list position, for all its sharers; the trailing private run
+// ends at the trace's current last block (read by the kernel at run time),
+// so the plan stays valid while decode steps append.
+struct Group {
+  std::vector<AttnUnit> units;
+  double cost;
+};
+
+gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t s) {
+  const int Hkv = p->d.num_kv_heads;
+  const int kmax = p->L.kmax;
+  const int tile_members = gambit::kRowsPerWG / p->g;
+  const int nb_total = p->d.num_blocks;
+  if ((int)p->cnt.size() != nb_total) {
+    p->cnt.assign(nb_total, 0);
+    p->first.assign(nb_total, -1);
+    p->csr_off.assign(nb_total, 0);
+    p->csr_fill.assign(nb_total, 0);
+  }
+  std::vector<int> nb(n);
+  std::vector<int32_t> touched;
+  for (int pos = 0; pos < n; ++pos) {
+    const auto& row = p->table[ids[pos]];
+    nb[pos] = cdiv(p->seq_len[ids[pos]], 16);
+    for (int j = 0; j < nb[pos]; ++j) {
+      const int b = row[j];
+      if (p->cnt[b]++ == 0) {
+        p->first[b] = pos;
+        touched.push_back(b);
+      }
+    }
+  }
+  // member lists of shared blocks (positions ascending)
+  size_t total = 0;
+  for (int b : touched) {
+    p->csr_off[b] = (int)total;
+    p->csr_fill[b] = 0;
+    if (p->cnt[b] > 1) total += p->cnt[b];
+  }
+  p->csr.resize(total);
+  for (int pos = 0; pos < n; ++pos) {
+    const auto& row = p->table[ids[pos]];
+    for (int j = 0; j < nb[pos]; ++j) {
+      const int b = row[j];
+      if (p->cnt[b] > 1) p->csr[p->csr_off[b] + p->csr_fill[b]++] = pos;
+    }
+  }
+
+  std::vector<Group> groups;
+  std::vector<int32_t> members;
+  std::vector<int32_t> nk(n, 0);
+  gambit_status st = GAMBIT_OK;
+  for (int chunk_blocks = kDefaultChunkBlocks;; chunk_blocks *= 2) {
+    groups.clear();
+    members.clear();
+    int worst = 0;
+    // One group per (chunk, KV head) holds all its row tiles, so the tiles
+    // that re-read the chunk land on one XCD.
+    auto emit = [&](int owner_pos, int jb0, int nblk, int ntok_est, const int32_t* mem, int mcnt,
+                    int kidx) {
+      const size_t first_tile = members.size();
+      std::vector<std::pair<int, int>> tiles;
+      for (int m0 = 0; m0 < mcnt; m0 += tile_members) {
+        const int mc = std::min(tile_members, mcnt - m0);
+        tiles.emplace_back((int)(first_tile + m0), mc);
+      }
+      members.insert(members.end(), mem, mem + mcnt);
+      for (int h = 0; h < Hkv; ++h) {
+        Group gr;
+        gr.cost = 0;
+        for (const auto& tl : tiles) {
+          gr.cost += (double)std::max(ntok_est, 1) * (2.0 + cdiv(tl.second * p->g, 16));
+          gr.units.push_back(AttnUnit{ids[owner_pos], jb0, nblk, h, tl.first, tl.second, kidx, 0});
+        }
+        groups.push_back(std::move(gr));
+      }
+    };
+    for (int pos = 0; pos < n; ++pos) {
+      const int t = ids[pos];
+      const auto& row = p->table[t];
+      int kidx = 0, j = 0;
+      while (j < nb[pos]) {
+        const int c = p->cnt[row[j]];
+        if (c == 1) {  // private run: through the trace's last block
+          const int len = nb[pos] - j;
+          const int nch = std::max(1, cdiv(len, chunk_blocks));
+          for (int k = 0, jb = j; k < nch; ++k) {
+            const int sz = len / nch + (k < len % nch ? 1 : 0);
+            const bool last = k == nch - 1;
+            emit(pos, jb, last ? -1 : sz, sz * 16, &pos, 1, kidx++);
+            jb += sz;
+          }
+          j = nb[pos];
+          break;
+        }
+        int j1 = j + 1;
+        while (j1 < nb[pos] && p->cnt[row[j1]] == c) ++j1;
+        const int len = j1 - j;
+        const int nch = cdiv(len, chunk_blocks);
+        const int b0 = row[j];
+        for (int k = 0, jb = j; k < nch; ++k) {
+          const int sz = len / nch + (k < len % nch ? 1 : 0);
+          if (p->first[b0] == pos) emit(pos, jb, sz, sz * 16, &p->csr[p->csr_off[b0]], c, kidx);
+          ++kidx;
+          jb += sz;
+        }
+        j = j1;
+        if (j == nb[pos]) emit(pos, j, -1, 16, &pos, 1, kidx++);  // appends go past the shared prefix
+      }
+      nk[pos] = kidx;
+      worst = std::max(worst, kidx);
+    }
+    if (worst <= kmax) {
+      p->max_splits_used = worst;
+      break;
+    }
+    if (chunk_blocks > p->d.max_blocks_per_trace) {
+      st = fail(p, GAMBIT_ERR_UNSUPPORTED, "a trace needs %d attention partials, max_splits is %d",
+                worst, kmax);
+      break;
+    }
+  }
+  for (int b : touched) {
+    p->cnt[b] = 0;
+    p->first[b] = -1;
+  }
+  if (st != GAMBIT_OK) return st;
+
+  // Longest-processing-time assignment of groups to the 8 XCDs.
+  std::vector<int> order(groups.size());
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return groups[a].cost > groups[b].cost; });
+  double load[8] = {0};
+  std::vector<std::vector<int>> per(8);
+  for (int gi : order) {
+    const int x = (int)(std::min_element(load, load + 8) - load);
+    load[x] += groups[gi].cost;
+    per[x].push_back(gi);
+  }
+  std::vector<AttnUnit> units;
+  int maxc = 0;
+  for (int x = 0; x < 8; ++x) {
+    p->xcd_off[x] = (int)units.size();
+    for (int gi : per[x]) units.insert(units.end(), groups[gi].units.begin(), groups[gi].units.end());
+    maxc = std::max(maxc, (int)units.size() - p->xcd_off[x]);
+  }
+  p->xcd_off[8] = (int)units.size();
+  p->grid = 8 * maxc;
+  p->n_units = (int)units.size();
+  if ((int)units.size() > p->L.max_units || (int)members.size() > p->L.max_members)
+    return fail(p, GAMBIT_ERR_UNSUPPORTED, "plan exceeds workspace bounds");
+
+  // upload: list, nk, members, units through the pinned plan stage
+  HIP_TRY(p, hipEventSynchronize(p->plan_ev), "plan fence");
+  uint8_t* st8 = p->plan_stage;
+  size_t o = 0;
+  auto put = [&](const void* src, size_t bytes, void* dst) -> hipError_t {
+    std::memcpy(st8 + o, src, bytes);
+    const hipError_t e = hipMemcpyAsync(dst, st8 + o, bytes, hipMemcpyHostToDevice, s);
+    o = align_up(o + bytes);
+    return e;
+  };
+  HIP_TRY(p, put(ids, 4 * (size_t)n, ws_ptr<int32_t>(p, p->L.list)), "plan upload");
+  HIP_TRY(p, put(nk.data(), 4 * (size_t)n, ws_ptr<int32_t>(p, p->L.nk)), "plan upload");
+  if (!members.empty())
+    HIP_TRY(p, put(members.data(), 4 * members.size(), ws_ptr<int32_t>(p, p->L.members)), "plan upload");
+  if (!units.empty())
+    HIP_TRY(p, put(units.data(), sizeof(AttnUnit) * units.size(), ws_ptr<AttnUnit>(p, p->L.units)),
+            "plan upload");
+  HIP_TRY(p, hipEventRecord(p->plan_ev, s), "plan fence");
+  p->plan_list.assign(ids, ids + n);
+  p->plan_valid = true;
+  return GAMBIT_OK;
+}
+
+void invalidate_plan(gambit_pool* p) { p->plan_valid = false; }
+
+}  // namespace
+
+// =============================================================================
+extern "C" {
+
+const char* gambit_status_str(gambit_status s) {
+  switch (s) {
+    case GAMBIT_OK: return "ok";
+    case GAMBIT_ERR_INVALID: return "invalid argument";
+    case GAMBIT_ERR_OUT_OF_BLOCKS: return "out of KV blocks";
+    case GAMBIT_ERR_SHARED_WRITE: return "write into a shared block";
+    case GAMBIT_ERR_UNSUPPORTED: return "unsupported";
+    case GAMBIT_ERR_DEVICE: return "device error";
+    case GAMBIT_ERR_WORKSPACE: return "workspace too small";
+    default: return "unknown status";
+  }
+}
+
+const char* gambit_last_error(const gambit_pool* pool) { return pool ? pool->last_error.c_str() : ""; }
+
+size_t gambit_workspace_size(const gambit_pool_desc* desc) {
+  Layout L;
+  return layout_of(desc, &L) ? L.total : 0;
+}
+
+gambit_status gambit_pool_create(const gambit_pool_desc* desc, void* stream, gambit_pool** out) {
+  if (!out) return GAMBIT_ERR_INVALID;
+  *out = nullptr;
+  Layout L;
+  if (!layout_of(desc, &L)) return GAMBIT_ERR_INVALID;
+  if (!desc->k_cache || !desc->v_cache || !desc->block_table || !desc->seq_len || !desc->refcount ||
+      !desc->workspace)
+    return GAMBIT_ERR_INVALID;
+  if ((desc->kv_dtype == GAMBIT_KV_FP8_E4M3) != (desc->kv_scale != nullptr)) return GAMBIT_ERR_INVALID;
+  if (desc->workspace_bytes < L.total) return GAMBIT_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(desc->workspace) % kAlign) return GAMBIT_ERR_INVALID;
+
+  auto* p = new gambit_pool;
+  p->d = *desc;
+  p->L = L;
+  p->ws = static_cast<uint8_t*>(desc->workspace);
+  p->g = desc->num_q_heads / desc->num_kv_heads;
+  if (desc->fp8_append_scale > 0.f) p->append_scale = desc->fp8_append_scale;
+
+  gambit::DevPool& D = p->dev;
+  D.k_cache = static_cast<uint8_t*>(desc->k_cache);
+  D.v_cache = static_cast<uint8_t*>(desc->v_cache);
+  D.kv_scale = desc->kv_scale;
+  D.table = desc->block_table;
+  D.seq_len = desc->seq_len;
+  D.refcount = desc->refcount;
+  D.freebits = ws_ptr<uint32_t>(p, L.freebits);
+  D.alloc_list = ws_ptr<int32_t>(p, L.alloc_list);
+  D.err = ws_ptr<int32_t>(p, L.err);
+  D.num_blocks = desc->num_blocks;
+  D.nwords = L.nwords;
+  D.max_traces = desc->max_traces;
+  D.max_blocks = desc->max_blocks_per_trace;
+  D.Hq = desc->num_q_heads;
+  D.Hkv = desc->num_kv_heads;
+  D.g = p->g;
+  D.esize = desc->kv_dtype == GAMBIT_KV_FP8_E4M3 ? 1 : 2;
+
+  p->table.assign(desc->max_traces, {});
+  p->seq_len.assign(desc->max_traces, 0);
+  p->refcount.assign(desc->num_blocks, 0);
+  p->freebits.assign(cdiv(desc->num_blocks, 64), ~0ull);
+  if (desc->num_blocks % 64) p->freebits.back() = (1ull << (desc->num_blocks % 64)) - 1;
+  p->nfree = desc->num_blocks;
+
+  p->stage_ints = 8 * (size_t)desc->max_traces + 2 * ((size_t)desc->max_blocks_per_trace + 1);
+  p->plan_stage_bytes = 4 * align_up(4 * (size_t)desc->max_traces) + sizeof(AttnUnit) * (size_t)L.max_units +
+                        4 * (size_t)L.max_members + 4 * kAlign;
+  hipError_t e = hipHostMalloc(reinterpret_cast<void**>(&p->stage), p->stage_ints * 4, hipHostMallocDefault);
+  if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void**>(&p->plan_stage), p->plan_stage_bytes, hipHostMallocDefault);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&p->stage_ev, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&p->plan_ev, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventRecord(p->stage_ev, S(stream));
+  if (e == hipSuccess) e = hipEventRecord(p->plan_ev, S(stream));
+  if (e == hipSuccess) e = hipMemsetAsync(p->ws + L.ticket, 0, 64, S(stream));
+  if (e == hipSuccess) e = gambit::launch_pool_init(D, S(stream));
+  if (e != hipSuccess) {
+    gambit_pool_destroy(p);
+    return GAMBIT_ERR_DEVICE;
+  }
+  *out = p;
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_pool_destroy(gambit_pool* p) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  if (p->stage_ev) (void)hipEventSynchronize(p->stage_ev);
+  if (p->plan_ev) (void)hipEventSynchronize(p->plan_ev);
+  if (p->stage) (void)hipHostFree(p->stage);
+  if (p->plan_stage) (void)hipHostFree(p->plan_stage);
+  if (p->stage_ev) (void)hipEventDestroy(p->stage_ev);
+  if (p->plan_ev) (void)hipEventDestroy(p->plan_ev);
+  delete p;
+  return GAMBIT_OK;
+}
+
+int32_t gambit_seq_len(const gambit_pool* p, int32_t t) {
+  return (p && t >= 0 && t < p->d.max_traces) ? p->seq_len[t] : -1;
+}
+
+int32_t gambit_free_blocks(const gambit_pool* p) { return p ? p->nfree : -1; }
+
+gambit_status gambit_kv_alloc(gambit_pool* p, int32_t n, const int32_t* ids, const int32_t* ntok,
+                              void* stream) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  gambit_status st = check_ids(p, n, ids, "trace");
+  if (st) return st;
+  if (n > 0 && !ntok) return fail(p, GAMBIT_ERR_INVALID, "token counts are NULL");
+  long need = 0;
+  for (int i = 0; i < n; ++i) {
+    if (ntok[i] < 0) return fail(p, GAMBIT_ERR_INVALID, "negative token count");
+    const long L = p->seq_len[ids[i]];
+    if (cdiv((int)std::min<long>(L + ntok[i], 1L << 30), 16) > p->d.max_blocks_per_trace)
+      return fail(p, GAMBIT_ERR_INVALID, "trace %d would exceed max_blocks_per_trace", ids[i]);
+    need += cdiv((int)(L + ntok[i]), 16) - cdiv((int)L, 16);
+  }
+  if (need > p->nfree) return fail(p, GAMBIT_ERR_OUT_OF_BLOCKS, "need %ld blocks, %d free", need, p->nfree);
+  if (n == 0) return GAMBIT_OK;
+  int32_t* rt = ws_ptr<int32_t>(p, p->L.req_trace);
+  int32_t* rn = ws_ptr<int32_t>(p, p->L.req_ntok);
+  std::vector<int32_t> both(ids, ids + n);
+  both.insert(both.end(), ntok, ntok + n);
+  HIP_TRY(p, hipEventSynchronize(p->stage_ev), "staging fence");
+  std::memcpy(p->stage, both.data(), 8 * (size_t)n);
+  HIP_TRY(p, hipMemcpyAsync(rt, p->stage, 4 * (size_t)n, hipMemcpyHostToDevice, S(stream)), "upload");
+  HIP_TRY(p, hipMemcpyAsync(rn, p->stage + n, 4 * (size_t)n, hipMemcpyHostToDevice, S(stream)), "upload");
+  HIP_TRY(p, hipEventRecord(p->stage_ev, S(stream)), "staging fence");
+  HIP_TRY(p, gambit::launch_alloc(p->dev, rt, rn, -1, n, 1.0f, S(stream)), "alloc kernel");
+  for (int i = 0; i < n; ++i) mirror_grow(p, ids[i], ntok[i]);
+  invalidate_plan(p);
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_kv_write(gambit_pool* p, int32_t t, int32_t pos0, int32_t n, const void* k,
+                              const void* v, const float* scales, void* stream) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  if (t < 0 || t >= p->d.max_traces) return fail(p, GAMBIT_ERR_INVALID, "trace id %d out of range", t);
+  if (pos0 < 0 || n < 0 || (long)pos0 + n > p->seq_len[t])
+    return fail(p, GAMBIT_ERR_INVALID, "write [%d, %d) outside trace %d's %d positions", pos0, pos0 + n, t,
+                p->seq_len[t]);
+  if (n == 0) return GAMBIT_OK;
+  if (!k || !v) return fail(p, GAMBIT_ERR_INVALID, "K or V is NULL");
+  for (int j = pos0 / 16; j <= (pos0 + n - 1) / 16; ++j)
+    if (p->refcount[p->table[t][j]] != 1)
+      return fail(p, GAMBIT_ERR_SHARED_WRITE, "block %d of trace %d is shared", j, t);
+  const int first = cdiv(pos0, 16), last = (pos0 + n - 1) / 16;
+  const int started = std::max(0, last - first + 1);
+  const bool fp8 = p->d.kv_dtype == GAMBIT_KV_FP8_E4M3;
+  if (!fp8 && scales) return fail(p, GAMBIT_ERR_INVALID, "scales are only for fp8 pools");
+  if (fp8 && started > 0 && !scales) return fail(p, GAMBIT_ERR_INVALID, "fp8 write needs block scales");
+  float* dsc = nullptr;
+  if (fp8 && started > 0) {
+    dsc = ws_ptr<float>(p, p->L.scales);
+    gambit_status st = upload_ints(p, reinterpret_cast<int32_t*>(dsc),
+                                   reinterpret_cast<const int32_t*>(scales), 2 * (size_t)started, S(stream));
+    if (st) return st;
+  }
+  HIP_TRY(p, gambit::launch_write(p->dev, t, pos0, n, k, v, dsc, S(stream)), "write kernel");
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_kv_fork(gambit_pool* p, int32_t n, const int32_t* parents, const int32_t* children,
+                             void* stream) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  std::vector<char> is_child;
+  gambit_status st = check_ids(p, n, children, "child", &is_child);
+  if (st) return st;
+  if (n > 0 && !parents) return fail(p, GAMBIT_ERR_INVALID, "parent list is NULL");
+  int tails = 0;
+  for (int i = 0; i < n; ++i) {
+    const int par = parents[i], ch = children[i];
+    if (par < 0 || par >= p->d.max_traces) return fail(p, GAMBIT_ERR_INVALID, "parent id %d out of range", par);
+    if (is_child[par]) return fail(p, GAMBIT_ERR_INVALID, "trace %d is both parent and child", par);
+    if (p->seq_len[ch] != 0) return fail(p, GAMBIT_ERR_INVALID, "child slot %d is not empty", ch);
+    if (p->seq_len[par] == 0) return fail(p, GAMBIT_ERR_INVALID, "parent %d is empty", par);
+    tails += p->seq_len[par] % 16 ? 1 : 0;
+  }
+  if (tails > p->nfree) return fail(p, GAMBIT_ERR_OUT_OF_BLOCKS, "need %d blocks, %d free", tails, p->nfree);
+  if (n == 0) return GAMBIT_OK;
+  std::vector<int32_t> pairs(2 * (size_t)n);
+  for (int i = 0; i < n; ++i) {
+    pairs[2 * i] = children[i];
+    pairs[2 * i + 1] = parents[i];
+  }
+  int32_t* dp = ws_ptr<int32_t>(p, p->L.pairs);
+  st = upload_ints(p, dp, pairs.data(), pairs.size(), S(stream));
+  if (st) return st;
+  HIP_TRY(p, gambit::launch_fork(p->dev, dp, n, ws_ptr<int32_t>(p, p->L.req_trace),
+                                 ws_ptr<int32_t>(p, p->L.req_ntok), S(stream)),
+          "fork kernels");
+  for (int i = 0; i < n; ++i) mirror_fork(p, parents[i], children[i]);
+  invalidate_plan(p);
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_kv_free(gambit_pool* p, int32_t n, const int32_t* ids, void* stream) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  gambit_status st = check_ids(p, n, ids, "trace");
+  if (st) return st;
+  for (int i = 0; i < n; ++i)
+    if (p->seq_len[ids[i]] == 0 && p->table[ids[i]].empty())
+      return fail(p, GAMBIT_ERR_INVALID, "trace %d is already empty", ids[i]);
+  if (n == 0) return GAMBIT_OK;
+  int32_t* d = ws_ptr<int32_t>(p, p->L.ids);
+  st = upload_ints(p, d, ids, n, S(stream));
+  if (st) return st;
+  HIP_TRY(p, gambit::launch_free(p->dev, d, n, S(stream)), "free kernel");
+  for (int i = 0; i < n; ++i) mirror_free(p, ids[i]);
+  invalidate_plan(p);
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, const void* q,
+                                 const void* k_new, const void* v_new, void* out, int32_t out_dtype,
+                                 float sm_scale, void* stream) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  gambit_status st = check_ids(p, n, ids, "trace");
+  if (st) return st;
+  if (n == 0) return GAMBIT_OK;
+  if (!q || !k_new || !v_new || !out) return fail(p, GAMBIT_ERR_INVALID, "NULL buffer");
+  if (out_dtype != GAMBIT_OUT_BF16 && out_dtype != GAMBIT_OUT_F32)
+    return fail(p, GAMBIT_ERR_INVALID, "bad output dtype");
+  if (!std::isfinite(sm_scale)) return fail(p, GAMBIT_ERR_INVALID, "softmax scale is not finite");
+  int need = 0;
+  for (int i = 0; i < n; ++i) {
+    const int L = p->seq_len[ids[i]];
+    if (L == 0) return fail(p, GAMBIT_ERR_INVALID, "trace %d is empty", ids[i]);
+    if (cdiv(L + 1, 16) > p->d.max_blocks_per_trace)
+      return fail(p, GAMBIT_ERR_INVALID, "trace %d is full", ids[i]);
+    need += L % 16 == 0;
+  }
+  if (need > p->nfree) return fail(p, GAMBIT_ERR_OUT_OF_BLOCKS, "need %d blocks, %d free", need, p->nfree);
+  hipStream_t s = S(stream);
+  if (!p->plan_valid || (int)p->plan_list.size() != n ||
+      !std::equal(p->plan_list.begin(), p->plan_list.end(), ids)) {
+    st = build_plan(p, n, ids, s);
+    if (st) return st;
+  }
+  const int32_t* dlist = ws_ptr<int32_t>(p, p->L.list);
+  HIP_TRY(p, gambit::launch_alloc(p->dev, dlist, nullptr, 1, n, p->append_scale, s), "append alloc");
+  HIP_TRY(p, gambit::launch_append_write(p->dev, dlist, n, k_new, v_new, s), "append write");
+  gambit::AttnLaunch A{};
+  A.q = static_cast<const uint16_t*>(q);
+  A.units = ws_ptr<AttnUnit>(p, p->L.units);
+  std::memcpy(A.xcd_off, p->xcd_off, sizeof A.xcd_off);
+  A.grid = p->grid;
+  A.members = ws_ptr<int32_t>(p, p->L.members);
+  A.nk = ws_ptr<int32_t>(p, p->L.nk);
+  A.part_acc = ws_ptr<float>(p, p->L.part_acc);
+  A.part_ml = ws_ptr<float2>(p, p->L.part_ml);
+  A.kmax = p->L.kmax;
+  A.n = n;
+  A.scale_log2 = sm_scale * 1.4426950408889634f;
+  A.out = out;
+  A.out_f32 = out_dtype == GAMBIT_OUT_F32;
+  HIP_TRY(p, gambit::launch_attention(p->dev, A, s), "attention");
+  for (int i = 0; i < n; ++i) mirror_grow(p, ids[i], 1);
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_score_prune_branch(gambit_pool* p, int32_t n, const int32_t* ids, const void* h,
+                                        int32_t Dh, const float* w, float b, int32_t keep,
+                                        int32_t n_parents, float* scores_out, int32_t* keep_out,
+                                        int32_t* child_parent_out, void* stream) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  gambit_status st = check_ids(p, n, ids, "trace");
+  if (st) return st;
+  if (n == 0 || n > gambit::kMaxRank) return fail(p, GAMBIT_ERR_UNSUPPORTED, "population size %d", n);
+  if (!h || !w || !scores_out || !keep_out) return fail(p, GAMBIT_ERR_INVALID, "NULL buffer");
+  if (Dh <= 0 || Dh % 8) return fail(p, GAMBIT_ERR_INVALID, "probe dimension %d is not a multiple of 8", Dh);
+  if (keep < 1 || keep > n) return fail(p, GAMBIT_ERR_INVALID, "keep %d of %d", keep, n);
+  const int nfree_traces = n - keep;
+  if (nfree_traces > 0) {
+    if (n_parents < 1 || n_parents > keep || nfree_traces % n_parents)
+      return fail(p, GAMBIT_ERR_INVALID, "%d pruned traces do not split over %d parents", nfree_traces, n_parents);
+    if (!child_parent_out) return fail(p, GAMBIT_ERR_INVALID, "NULL child/parent buffer");
+  }
+  for (int i = 0; i < n; ++i)
+    if (p->seq_len[ids[i]] == 0) return fail(p, GAMBIT_ERR_INVALID, "trace %d is empty", ids[i]);
+  hipStream_t s = S(stream);
+  int32_t* dids = ws_ptr<int32_t>(p, p->L.ids);
+  st = upload_ints(p, dids, ids, n, s);
+  if (st) return st;
+  gambit::ProbeLaunch PL{};
+  PL.list = dids;
+  PL.n = n;
+  PL.h = static_cast<const uint16_t*>(h);
+  PL.Dh = Dh;
+  PL.w = w;
+  PL.b = b;
+  PL.keep = keep;
+  PL.n_parents = nfree_traces > 0 ? n_parents : 0;
+  PL.scores_out = scores_out;
+  PL.keep_out = keep_out;
+  PL.pairs_out = nfree_traces > 0 ? child_parent_out : ws_ptr<int32_t>(p, p->L.pairs);
+  PL.free_list = ws_ptr<int32_t>(p, p->L.free_list);
+  PL.ticket = ws_ptr<uint32_t>(p, p->L.ticket);
+  HIP_TRY(p, gambit::launch_probe_rank(PL, s), "probe/rank kernel");
+  // the one blocking readback: the ranking
+  std::vector<int32_t> kept(keep), pairs(2 * (size_t)nfree_traces);
+  HIP_TRY(p, hipMemcpyAsync(kept.data(), keep_out, 4 * (size_t)keep, hipMemcpyDeviceToHost, s), "readback");
+  if (nfree_traces > 0)
+    HIP_TRY(p, hipMemcpyAsync(pairs.data(), child_parent_out, 8 * (size_t)nfree_traces, hipMemcpyDeviceToHost, s),
+            "readback");
+  HIP_TRY(p, hipStreamSynchronize(s), "readback");
+  // host check of the device plan, then the exact out-of-blocks test
+  std::vector<char> in_list(p->d.max_traces, 0), is_kept(p->d.max_traces, 0);
+  for (int i = 0; i < n; ++i) in_list[ids[i]] = 1;
+  for (int t : kept) {
+    if (t < 0 || t >= p->d.max_traces || !in_list[t] || is_kept[t])
+      return fail(p, GAMBIT_ERR_DEVICE, "device ranking returned an invalid id %d", t);
+    is_kept[t] = 1;
+  }
+  std::vector<int32_t> freed;
+  for (int t = 0; t < p->d.max_traces; ++t)
+    if (in_list[t] && !is_kept[t]) freed.push_back(t);
+  const int c = nfree_traces > 0 ? nfree_traces / n_parents : 0;
+  for (int j = 0; j < nfree_traces; ++j)
+    if (pairs[2 * j] != freed[j] || pairs[2 * j + 1] != kept[j / c])
+      return fail(p, GAMBIT_ERR_DEVICE, "device prune/branch plan disagrees with the ranking");
+  if (nfree_traces == 0) return GAMBIT_OK;
+  std::unordered_map<int, int> drop;
+  int released = 0;
+  for (int t : freed)
+    for (int blk : p->table[t]) ++drop[blk];
+  for (auto& kv : drop) released += p->refcount[kv.first] == kv.second;
+  int tails = 0;
+  for (int j = 0; j < nfree_traces; ++j) tails += p->seq_len[kept[j / c]] % 16 ? 1 : 0;
+  if (tails > p->nfree + released)
+    return fail(p, GAMBIT_ERR_OUT_OF_BLOCKS, "branching needs %d blocks, %d free after pruning", tails,
+                p->nfree + released);
+  HIP_TRY(p, gambit::launch_free(p->dev, PL.free_list, nfree_traces, s), "free kernel");
+  HIP_TRY(p, gambit::launch_fork(p->dev, child_parent_out, nfree_traces, ws_ptr<int32_t>(p, p->L.req_trace),
+                                 ws_ptr<int32_t>(p, p->L.req_ntok), s),
+          "fork kernels");
+  for (int t : freed) mirror_free(p, t);
+  for (int j = 0; j < nfree_traces; ++j) mirror_fork(p, kept[j / c], freed[j]);
+  invalidate_plan(p);
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_rank_topk(int32_t n, const int32_t* ids, const float* scores, int32_t keep,
+                               int32_t* keep_out, void* stream) {
+  if (n <= 0 || n > gambit::kMaxRank || keep < 1 || keep > n || !ids || !scores || !keep_out)
+    return GAMBIT_ERR_INVALID;
+  return gambit::launch_rank_topk(n, ids, scores, keep, keep_out, S(stream)) == hipSuccess ? GAMBIT_OK
+                                                                                             : GAMBIT_ERR_DEVICE;
+}
+
+gambit_status gambit_pool_check(gambit_pool* p, void* stream) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  hipStream_t s = S(stream);
+  HIP_TRY(p, hipStreamSynchronize(s), "sync");
+  const int T = p->d.max_traces, MB = p->d.max_blocks_per_trace, NB = p->d.num_blocks;
+  std::vector<int32_t> tab((size_t)T * MB), len(T), ref(NB), err(1);
+  std::vector<uint32_t> bits(p->L.nwords);
+  HIP_TRY(p, hipMemcpy(tab.data(), p->d.block_table, 4 * tab.size(), hipMemcpyDeviceToHost), "check read");
+  HIP_TRY(p, hipMemcpy(len.data(), p->d.seq_len, 4 * (size_t)T, hipMemcpyDeviceToHost), "check read");
+  HIP_TRY(p, hipMemcpy(ref.data(), p->d.refcount, 4 * (size_t)NB, hipMemcpyDeviceToHost), "check read");
+  HIP_TRY(p, hipMemcpy(err.data(), p->ws + p->L.err, 4, hipMemcpyDeviceToHost), "check read");
+  HIP_TRY(p, hipMemcpy(bits.data(), p->ws + p->L.freebits, 4 * bits.size(), hipMemcpyDeviceToHost), "check read");
+  if (err[0]) return fail(p, GAMBIT_ERR_DEVICE, "device error word 0x%x", err[0]);
+  for (int t = 0; t < T; ++t) {
+    if (len[t] != p->seq_len[t]) return fail(p, GAMBIT_ERR_DEVICE, "seq_len[%d]: device %d, host %d", t, len[t], p->seq_len[t]);
+    const auto& row = p->table[t];
+    for (int j = 0; j < MB; ++j) {
+      const int want = j < (int)row.size() ? row[j] : -1;
+      if (tab[(size_t)t * MB + j] != want)
+        return fail(p, GAMBIT_ERR_DEVICE, "table[%d][%d]: device %d, host %d", t, j, tab[(size_t)t * MB + j], want);
+    }
+  }
+  for (int b = 0; b < NB; ++b) {
+    if (ref[b] != p->refcount[b]) return fail(p, GAMBIT_ERR_DEVICE, "refcount[%d]: device %d, host %d", b, ref[b], p->refcount[b]);
+    const bool dfree = (bits[b >> 5] >> (b & 31)) & 1;
+    const bool hfree = (p->freebits[b >> 6] >> (b & 63)) & 1;
+    if (dfree != hfree) return fail(p, GAMBIT_ERR_DEVICE, "free bit of block %d: device %d, host %d", b, dfree, hfree);
+  }
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_plan_stats(gambit_pool* p, int32_t n, const int32_t* ids, gambit_stats* out) {
+  if (!p || !out) return GAMBIT_ERR_INVALID;
+  gambit_status st = check_ids(p, n, ids, "trace");
+  if (st) return st;
+  std::vector<char> seen(p->d.num_blocks, 0);
+  gambit_stats r{};
+  for (int i = 0; i < n; ++i) {
+    const int t = ids[i], L = p->seq_len[t];
+    r.total_tokens += L;
+    const auto& row = p->table[t];
+    for (size_t j = 0; j < row.size(); ++j) {
+      if (seen[row[j]]) continue;
+      seen[row[j]] = 1;
+      ++r.unique_blocks;
+      r.unique_tokens += std::min(16, L - 16 * (int)j);
+    }
+  }
+  const bool same = p->plan_valid && (int)p->plan_list.size() == n && std::equal(p->plan_list.begin(), p->plan_list.end(), ids);
+  r.n_units = same ? p->n_units : -1;
+  r.max_splits_used = same ? p->max_splits_used : -1;
+  *out = r;
+  return GAMBIT_OK;
+}
+
+}  // extern "C"

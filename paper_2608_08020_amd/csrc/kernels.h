@@ -1,0 +1,103 @@
+// Internal interface between the host library and the gfx950 kernels.
+// Not part of the public ABI (include/gambit.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace gambit {
+
+constexpr int kBlock = 16;     // tokens per KV block
+constexpr int kHeadDim = 128;  // head dimension the kernels implement
+constexpr int kRowsPerWG = 128;  // attention rows (trace x q-head) one workgroup holds
+
+// One attention work unit: a run of blocks that the same member traces share,
+// for one KV head and one tile of member traces.
+struct AttnUnit {
+  int32_t owner;    // trace whose block-table row lists the run's blocks
+  int32_t jb0;      // first logical block of the run
+  int32_t nblk;     // blocks in the run; -1 = through the owner's last block (read at run time)
+  int32_t kvh;      // KV head
+  int32_t mem_off;  // first member (list position) in the member array
+  int32_t mem_cnt;  // members in this tile; 0 = padding unit (does nothing)
+  int32_t kidx;     // partial slot of this run for every member
+  int32_t pad;
+};
+
+// Device view of a pool.
+struct DevPool {
+  uint8_t* k_cache;
+  uint8_t* v_cache;
+  float* kv_scale;        // [num_blocks][2], fp8 only
+  int32_t* table;         // [max_traces][max_blocks]
+  int32_t* seq_len;       // [max_traces]
+  int32_t* refcount;      // [num_blocks]
+  uint32_t* freebits;     // [nwords], bit set = block free
+  int32_t* alloc_list;    // [num_blocks] scratch of the allocator
+  int32_t* err;           // device error word
+  int32_t num_blocks, nwords, max_traces, max_blocks;
+  int32_t Hq, Hkv, g;
+  int32_t esize;          // bytes per cache element (2 bf16, 1 fp8)
+};
+
+enum : int32_t {
+  kErrAllocShort = 1,       // allocator found fewer free blocks than requested
+  kErrRefUnderflow = 2,     // a refcount dropped below zero
+  kErrBadBlock = 4,         // a table entry outside [0, num_blocks)
+};
+
+struct AttnLaunch {
+  const uint16_t* q;        // [n][Hq][128] bf16
+  const AttnUnit* units;    // grouped by XCD: XCD x runs units [xcd_off[x], xcd_off[x+1])
+  int32_t xcd_off[9];
+  int32_t grid;             // 8 * (largest per-XCD count)
+  const int32_t* members;   // list positions
+  const int32_t* nk;        // [n] partials per list position
+  float* part_acc;          // [n][Hq][kmax][128]
+  float2* part_ml;          // [n][Hq][kmax] (running max in log2 units, sum)
+  int32_t kmax;
+  int32_t n;
+  float scale_log2;         // sm_scale * log2(e)
+  void* out;
+  int32_t out_f32;
+};
+
+hipError_t launch_pool_init(const DevPool& P, hipStream_t s);
+// m requests (trace ids, token counts) on the device; uniform_ntok >= 0
+// overrides the counts.  fp8 pools give new blocks the scale `new_scale`.
+hipError_t launch_alloc(const DevPool& P, const int32_t* req_trace, const int32_t* req_ntok,
+                        int32_t uniform_ntok, int32_t m, float new_scale, hipStream_t s);
+hipError_t launch_write(const DevPool& P, int32_t trace, int32_t pos0, int32_t n, const void* k,
+                        const void* v, const float* started_scales, hipStream_t s);
+hipError_t launch_append_write(const DevPool& P, const int32_t* list, int32_t n, const void* k_new,
+                               const void* v_new, hipStream_t s);
+hipError_t launch_free(const DevPool& P, const int32_t* ids, int32_t n, hipStream_t s);
+// pairs: device [n][2] (child, parent).  req_trace/req_ntok: scratch [n].
+hipError_t launch_fork(const DevPool& P, const int32_t* pairs, int32_t n, int32_t* req_trace,
+                       int32_t* req_ntok, hipStream_t s);
+
+hipError_t launch_attention(const DevPool& P, const AttnLaunch& A, hipStream_t s);
+
+// Probe + sigmoid + ranking + prune/branch plan in one launch.
+struct ProbeLaunch {
+  const int32_t* list;      // device [n] trace ids
+  int32_t n;
+  const uint16_t* h;        // [n][Dh] bf16
+  int32_t Dh;
+  const float* w;
+  float b;
+  int32_t keep, n_parents;
+  float* scores_out;        // [n]
+  int32_t* keep_out;        // [keep]
+  int32_t* pairs_out;       // [n-keep][2]
+  int32_t* free_list;       // [n-keep] scratch: pruned ids ascending
+  uint32_t* ticket;         // zero before launch; the kernel leaves it zero
+};
+hipError_t launch_probe_rank(const ProbeLaunch& L, hipStream_t s);
+hipError_t launch_rank_topk(int32_t n, const int32_t* ids, const float* scores, int32_t keep,
+                            int32_t* keep_out, hipStream_t s);
+
+constexpr int kMaxRank = 4096;  // largest population the in-LDS ranking handles
+
+}  // namespace gambit

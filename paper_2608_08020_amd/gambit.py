@@ -1,0 +1,259 @@
+"""Python binding of libgambit (ctypes).  Argument marshalling only.
+
+Every step of the hot path runs in the library's HIP kernels; this module
+allocates the caller-owned device buffers with torch and passes pointers
+and the current HIP stream.  Method names follow the C entry points in
+include/gambit.h without the ``gambit_`` prefix.  There is no fallback: a
+missing library raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch  # loads the HIP runtime that libgambit binds to
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgambit.so")
+
+OK, ERR_INVALID, ERR_OUT_OF_BLOCKS, ERR_SHARED_WRITE, ERR_UNSUPPORTED, ERR_DEVICE, ERR_WORKSPACE = (
+    0, -1, -2, -3, -4, -5, -6)
+KV_BF16, KV_FP8_E4M3 = 0, 1
+OUT_BF16, OUT_F32 = 0, 1
+CODE_NAMES = {ERR_INVALID: "INVALID", ERR_OUT_OF_BLOCKS: "OUT_OF_BLOCKS",
+              ERR_SHARED_WRITE: "SHARED_WRITE", ERR_UNSUPPORTED: "UNSUPPORTED",
+              ERR_DEVICE: "DEVICE", ERR_WORKSPACE: "WORKSPACE"}
+MAX_RANK = 4096
+
+
+class GambitError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{CODE_NAMES.get(status, status)}: {msg}")
+        self.status = status
+        self.code = CODE_NAMES.get(status, str(status))
+
+
+class PoolDesc(ctypes.Structure):
+    _fields_ = [("num_blocks", ctypes.c_int32), ("block_size", ctypes.c_int32),
+                ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("kv_dtype", ctypes.c_int32),
+                ("max_traces", ctypes.c_int32), ("max_blocks_per_trace", ctypes.c_int32),
+                ("max_splits", ctypes.c_int32), ("fp8_append_scale", ctypes.c_float),
+                ("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p),
+                ("kv_scale", ctypes.c_void_p), ("block_table", ctypes.c_void_p),
+                ("seq_len", ctypes.c_void_p), ("refcount", ctypes.c_void_p),
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [("total_tokens", ctypes.c_int64), ("unique_tokens", ctypes.c_int64),
+                ("unique_blocks", ctypes.c_int64), ("n_units", ctypes.c_int32),
+                ("max_splits_used", ctypes.c_int32)]
+
+
+_lib = None
+EXPORTS = ["gambit_workspace_size", "gambit_pool_create", "gambit_pool_destroy", "gambit_kv_alloc",
+           "gambit_kv_write", "gambit_kv_fork", "gambit_kv_free", "gambit_decode_attn",
+           "gambit_score_prune_branch", "gambit_rank_topk", "gambit_pool_check",
+           "gambit_plan_stats", "gambit_seq_len", "gambit_free_blocks", "gambit_status_str",
+           "gambit_last_error"]
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2608_08020_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
+    sig = {
+        "gambit_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(PoolDesc)]),
+        "gambit_pool_create": (i32, [ctypes.POINTER(PoolDesc), vp, ctypes.POINTER(vp)]),
+        "gambit_pool_destroy": (i32, [vp]),
+        "gambit_kv_alloc": (i32, [vp, i32, vp, vp, vp]),
+        "gambit_kv_write": (i32, [vp, i32, i32, i32, vp, vp, vp, vp]),
+        "gambit_kv_fork": (i32, [vp, i32, vp, vp, vp]),
+        "gambit_kv_free": (i32, [vp, i32, vp, vp]),
+        "gambit_decode_attn": (i32, [vp, i32, vp, vp, vp, vp, vp, i32, f32, vp]),
+        "gambit_score_prune_branch": (i32, [vp, i32, vp, vp, i32, vp, f32, i32, i32, vp, vp, vp, vp]),
+        "gambit_rank_topk": (i32, [i32, vp, vp, i32, vp, vp]),
+        "gambit_pool_check": (i32, [vp, vp]),
+        "gambit_plan_stats": (i32, [vp, i32, vp, ctypes.POINTER(Stats)]),
+        "gambit_seq_len": (i32, [vp, i32]),
+        "gambit_free_blocks": (i32, [vp]),
+        "gambit_status_str": (ctypes.c_char_p, [i32]),
+        "gambit_last_error": (ctypes.c_char_p, [vp]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype, fn.argtypes = res, args
+    _lib = L
+    return L
+
+
+def workspace_size(desc: PoolDesc) -> int:
+    return int(lib().gambit_workspace_size(ctypes.byref(desc)))
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _host_i32(x) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _dev(t: torch.Tensor, dtype=None, shape=None):
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("expected a contiguous device tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"expected {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"expected shape {tuple(shape)}, got {tuple(t.shape)}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def rank_topk(ids: torch.Tensor, scores: torch.Tensor, keep: int, stream=None) -> torch.Tensor:
+    """gambit_rank_topk: ids of the top `keep` by (score desc, id asc), on the device."""
+    n = ids.numel()
+    out = torch.empty(keep, dtype=torch.int32, device=ids.device)
+    st = lib().gambit_rank_topk(n, _dev(ids, torch.int32), _dev(scores, torch.float32), keep,
+                                _dev(out), _stream(stream))
+    if st != OK:
+        raise GambitError(st, "rank_topk")
+    return out
+
+
+class Pool:
+    """A refcounted paged KV pool on one GPU; all buffers are torch tensors."""
+
+    def __init__(self, *, num_blocks: int, num_q_heads: int, num_kv_heads: int,
+                 max_traces: int, max_blocks_per_trace: int, kv_dtype: str = "bf16",
+                 head_dim: int = 128, max_splits: int = 0, fp8_append_scale: float = 0.0,
+                 device: str = "cuda", stream=None):
+        fp8 = kv_dtype == "fp8_e4m3"
+        if kv_dtype not in ("bf16", "fp8_e4m3"):
+            raise ValueError(kv_dtype)
+        self.kv_dtype = kv_dtype
+        self.Hq, self.Hkv, self.D = num_q_heads, num_kv_heads, head_dim
+        self.max_traces, self.max_blocks = max_traces, max_blocks_per_trace
+        cache_dtype = torch.uint8 if fp8 else torch.bfloat16
+        shape = (num_blocks, num_kv_heads, 16, head_dim)
+        self.k_cache = torch.empty(shape, dtype=cache_dtype, device=device)
+        self.v_cache = torch.empty(shape, dtype=cache_dtype, device=device)
+        self.kv_scale = torch.ones((num_blocks, 2), dtype=torch.float32, device=device) if fp8 else None
+        self.block_table = torch.empty((max_traces, max_blocks_per_trace), dtype=torch.int32, device=device)
+        self.seq_len = torch.empty(max_traces, dtype=torch.int32, device=device)
+        self.refcount = torch.empty(num_blocks, dtype=torch.int32, device=device)
+        d = PoolDesc(num_blocks, 16, num_q_heads, num_kv_heads, head_dim,
+                     KV_FP8_E4M3 if fp8 else KV_BF16, max_traces, max_blocks_per_trace, max_splits,
+                     fp8_append_scale, self.k_cache.data_ptr(), self.v_cache.data_ptr(),
+                     self.kv_scale.data_ptr() if fp8 else None, self.block_table.data_ptr(),
+                     self.seq_len.data_ptr(), self.refcount.data_ptr(), None, 0)
+        ws = workspace_size(d)
+        if ws == 0:
+            raise GambitError(ERR_INVALID, "invalid pool description")
+        self.workspace = torch.empty(ws + 256, dtype=torch.uint8, device=device)
+        base = self.workspace.data_ptr()
+        d.workspace = base + (-base) % 256
+        d.workspace_bytes = ws
+        self.desc = d
+        h = ctypes.c_void_p()
+        st = lib().gambit_pool_create(ctypes.byref(d), _stream(stream), ctypes.byref(h))
+        if st != OK:
+            raise GambitError(st, "pool_create")
+        self._h = h
+
+    # -- plumbing
+    def _check(self, st: int, what: str):
+        if st != OK:
+            raise GambitError(st, f"{what}: {lib().gambit_last_error(self._h).decode()}")
+
+    def close(self):
+        if getattr(self, "_h", None):
+            torch.cuda.current_stream().synchronize()
+            lib().gambit_pool_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- entry points
+    def kv_alloc(self, ids, n_tokens, stream=None):
+        ids, nt = _host_i32(ids), _host_i32(n_tokens)
+        self._check(lib().gambit_kv_alloc(self._h, ids.size, _ptr(ids), _ptr(nt), _stream(stream)),
+                    "kv_alloc")
+
+    def kv_write(self, trace: int, pos0: int, k: torch.Tensor, v: torch.Tensor, scales=None, stream=None):
+        n = k.shape[0]
+        sc = None
+        if scales is not None:
+            sc = np.ascontiguousarray(np.asarray(scales, np.float32))
+        self._check(lib().gambit_kv_write(self._h, trace, pos0, n, _dev(k), _dev(v),
+                                          None if sc is None else _ptr(sc), _stream(stream)),
+                    "kv_write")
+
+    def kv_fork(self, parents, children, stream=None):
+        p, c = _host_i32(parents), _host_i32(children)
+        self._check(lib().gambit_kv_fork(self._h, c.size, _ptr(p), _ptr(c), _stream(stream)), "kv_fork")
+
+    def kv_free(self, ids, stream=None):
+        ids = _host_i32(ids)
+        self._check(lib().gambit_kv_free(self._h, ids.size, _ptr(ids), _stream(stream)), "kv_free")
+
+    def decode_attn(self, ids, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
+                    out: torch.Tensor | None = None, out_dtype=torch.bfloat16, sm_scale=None,
+                    stream=None) -> torch.Tensor:
+        ids = _host_i32(ids)
+        n = ids.size
+        if out is None:
+            out = torch.empty((n, self.Hq, self.D), dtype=out_dtype, device=q.device)
+        od = OUT_F32 if out.dtype == torch.float32 else OUT_BF16
+        if out.dtype not in (torch.float32, torch.bfloat16):
+            raise ValueError("out must be bf16 or fp32")
+        sm = float(self.D ** -0.5 if sm_scale is None else sm_scale)
+        _dev(q, torch.bfloat16, (n, self.Hq, self.D))
+        self._check(lib().gambit_decode_attn(self._h, n, _ptr(ids), _dev(q), _dev(k_new), _dev(v_new),
+                                             _dev(out), od, sm, _stream(stream)), "decode_attn")
+        return out
+
+    def score_prune_branch(self, ids, h: torch.Tensor, w: torch.Tensor, b: float, keep: int,
+                           n_parents: int, stream=None):
+        """Returns device tensors (scores [n], keep ids [keep], child/parent pairs [n-keep][2])."""
+        ids = _host_i32(ids)
+        n = ids.size
+        dev = h.device
+        scores = torch.empty(n, dtype=torch.float32, device=dev)
+        keep_out = torch.empty(keep, dtype=torch.int32, device=dev)
+        pairs = torch.empty((max(n - keep, 1), 2), dtype=torch.int32, device=dev)
+        _dev(h, torch.bfloat16)
+        self._check(lib().gambit_score_prune_branch(self._h, n, _ptr(ids), _dev(h), h.shape[1],
+                                                    _dev(w, torch.float32), float(b), keep, n_parents,
+                                                    _dev(scores), _dev(keep_out), _dev(pairs),
+                                                    _stream(stream)), "score_prune_branch")
+        return scores, keep_out, pairs[:n - keep]
+
+    def pool_check(self, stream=None):
+        self._check(lib().gambit_pool_check(self._h, _stream(stream)), "pool_check")
+
+    def plan_stats(self, ids) -> Stats:
+        ids = _host_i32(ids)
+        s = Stats()
+        self._check(lib().gambit_plan_stats(self._h, ids.size, _ptr(ids), ctypes.byref(s)), "plan_stats")
+        return s
+
+    def seq_len_of(self, t: int) -> int:
+        return int(lib().gambit_seq_len(self._h, t))
+
+    def free_blocks(self) -> int:
+        return int(lib().gambit_free_blocks(self._h))
