@@ -1,0 +1,199 @@
+#!/usr/bin/env python3
+"""Population-decode benchmark on one MI355X.
+
+One step = one decode step of the whole population (append + shared-prefix
+split-K attention + merge) with the thought-boundary round (probe, rank,
+prune, branch) every `interval` steps, exactly as the workload schedules it.
+The default workload is 512 Qwen3-8B-shaped traces (32 q heads, 8 KV heads,
+head dim 128, bf16 KV) in a 5-generation branch tree with contexts up to
+32768 tokens, rounds every 256 steps keeping 128 and forking 4x.  The
+warm-up covers the first round, so the timed steps measure the steady state.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 4]
+
+Prints one JSON line.  `value` is trace-steps/s over the timed steps with
+every input already resident in HBM.  `roofline` prices the dominant kernel
+(split-K attention) by its algorithmic bytes - every distinct KV block the
+population references read once, plus queries and block-table entries - over
+its event-timed average duration.  `cpu_baseline` times the CPU oracle on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0
+METRIC = "decode-attention trace-steps/sec + achieved HBM GB/s (% of MI355X peak)"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2608_08020_amd", "csrc", "decode_attn.hip")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_sha() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """Per-launch HBM bytes from the committed rocprofv3 counter runs, if they
+    were taken on the current kernel source and this workload."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_sha") != kernel_sha() or rec.get("workload") != workload:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, budget_s: float):
+    """Oracle attention for sampled traces at the workload's first decode step."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import run as orun
+
+    T = wl.T
+    model = orun.new_pool(wl, 1 + sum(n.length // 16 + 2 for n in wl.tree.nodes) + 4 * T)
+    orun.apply_setup(model, wl, lazy=True)
+    k, v = wl.step_kv(0)
+    model.append(list(range(T)), k, v)
+    q = wl.step_q(0)
+    order = [int(t) for t in np.random.default_rng(0).permutation(T)]
+    done, spent, tokens = 0, 0.0, 0
+    for t in order:
+        model.materialise(t)                     # generate the lazily keyed inputs, untimed
+        t0 = time.perf_counter()
+        orun.attend(model, wl, q, [t])
+        spent += time.perf_counter() - t0
+        done += 1
+        tokens += model.seq_len[t]
+        if spent >= budget_s:
+            break
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": done / spent, "unit": "trace-steps/s", "cores": threads, "kind": "oracle",
+            "sample": (f"{done} traces (mean context {tokens / done:.0f} tokens) of the first decode "
+                       f"step, fp64 dense attention on materialised per-trace KV, "
+                       f"{spent:.1f} s; {len(os.sched_getaffinity(0))} host cores visible")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path shards by "
+              f"KV head or by sharing subtree, and nothing here runs across GPUs)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2608_08020_amd.runner import PopulationRun
+    from workload import CONFIGS, Workload
+
+    cfg = CONFIGS[args.config]
+    W = cfg.interval if args.warmup is None else args.warmup
+    K = (cfg.steps - W) if args.steps is None else args.steps
+    if K <= 0:
+        raise SystemExit("need at least one timed step")
+    t_setup = time.time()
+    wl = Workload(cfg, total_steps=W + K)
+    run = PopulationRun(wl)
+    run.setup()
+    log(f"{cfg.name}: setup {time.time() - t_setup:.1f}s")
+    run.load_steps(range(W + K))
+    rounds = wl.rounds_after()
+    run.load_rounds(range(len(rounds)))
+    log(f"inputs resident ({time.time() - t_setup:.1f}s)")
+    T = wl.T
+    ids = run.ids
+    out = torch.empty((T, cfg.n_q_heads, cfg.head_dim), dtype=torch.bfloat16, device="cuda")
+    round_of = {s: i for i, s in enumerate(rounds)}
+
+    for s in range(W):
+        run.decode(s, out=out)
+        if s in round_of:
+            run.round(round_of[s])
+    torch.cuda.synchronize()
+    log(f"warm-up {W} steps done")
+
+    e = cfg.kv_elem_bytes
+    Hkv, D, Hq = cfg.n_kv_heads, cfg.head_dim, cfg.n_q_heads
+    pool = run.pool
+    pool.profile_begin(K)
+    alg_bytes, ctx_tokens = [], 0
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record()
+    for s in range(W, W + K):
+        run.decode(s, out=out)
+        st = pool.plan_stats(ids)
+        alg_bytes.append(st.unique_tokens * Hkv * D * 2 * e + (8 * st.unique_blocks if e == 1 else 0)
+                         + T * Hq * D * 2 + 4 * st.table_entries)
+        ctx_tokens += st.total_tokens
+        if s in round_of:
+            run.round(round_of[s])
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = start.elapsed_time(end)
+    attn_ms, launches = pool.profile_end()
+    pool.pool_check()
+    timed_rounds = sum(1 for s in range(W, W + K) if s in round_of)
+
+    value = T * K / wall
+    bytes_per_launch = sum(alg_bytes) / len(alg_bytes)
+    attn_avg_s = attn_ms / 1e3 / launches
+    achieved = bytes_per_launch / attn_avg_s / 1e9
+    traffic = measured_traffic(cfg.name)
+    res = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "trace-steps/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(wall * 1e3 / K, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if e == 2 else "fp8_e4m3 KV, bf16 q, fp32 accumulate",
+        "data": "synthetic (seeded; shapes from the paper's trace statistics)",
+        "config": {"workload": cfg.name, "traces": T, "q_heads": Hq, "kv_heads": Hkv, "head_dim": D,
+                   "kv_dtype": cfg.kv_dtype, "mean_context_tokens": round(ctx_tokens / K / T),
+                   "round_every_steps": cfg.interval, "keep": cfg.keep, "fanout": cfg.fanout,
+                   "rounds_in_timed_steps": timed_rounds, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBPS, 4),
+                     "traffic": traffic, "kernel": "attn_units_kernel (split-K shared-run attention)",
+                     "alg_bytes_per_launch": round(bytes_per_launch),
+                     "avg_launch_us": round(attn_avg_s * 1e6, 2), "launches_timed": launches},
+        "step_hbm_GBps": round(sum(alg_bytes) / wall / 1e9, 1),
+        "event_ms_per_step": round(ev_ms / K, 4),
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle")
+        res["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

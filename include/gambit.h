@@ -105,6 +105,7 @@ typedef struct {
   int64_t total_tokens;          /* sum of lengths over the listed traces        */
   int64_t unique_tokens;         /* valid tokens of the distinct blocks they use */
   int64_t unique_blocks;         /* distinct blocks they use                     */
+  int64_t table_entries;         /* block-table entries they read (sum of blocks)*/
   int32_t n_units;               /* attention work units of the current plan     */
   int32_t max_splits_used;       /* largest number of partials of one trace      */
 } gambit_stats;
@@ -198,6 +199,15 @@ gambit_status gambit_pool_check(gambit_pool* pool, void* stream);
 /* Statistics of the attention work for a trace list (host only, no sync). */
 gambit_status gambit_plan_stats(gambit_pool* pool, int32_t n, const int32_t* trace_ids,
                                 gambit_stats* out);
+
+/* Event timing of the split-K attention kernel, the dominant kernel of a
+ * decode step.  Between gambit_profile_begin and gambit_profile_end every
+ * gambit_decode_attn records a HIP event pair on its stream around that
+ * kernel (at most max_launches pairs; later launches are not timed).
+ * gambit_profile_end waits for the last event and returns the summed
+ * kernel time in milliseconds and the number of timed launches. */
+gambit_status gambit_profile_begin(gambit_pool* pool, int32_t max_launches);
+gambit_status gambit_profile_end(gambit_pool* pool, double* attn_ms, int32_t* launches);
 
 /* Host mirror queries (no sync): length of a trace; free block count. */
 int32_t gambit_seq_len(const gambit_pool* pool, int32_t trace_id);

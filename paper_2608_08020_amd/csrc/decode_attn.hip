@@ -376,16 +376,17 @@ __global__ __launch_bounds__(256) void merge_kernel(DevPool P, AttnLaunch A) {
 
 }  // namespace
 
-hipError_t launch_attention(const DevPool& P, const AttnLaunch& A, hipStream_t s) {
+hipError_t launch_attention_units(const DevPool& P, const AttnLaunch& A, hipStream_t s) {
+  if (A.n <= 0 || A.grid <= 0) return hipSuccess;
+  if (P.esize == 1)
+    hipLaunchKernelGGL(attn_units_kernel<true>, dim3(A.grid), dim3(kThreads), 0, s, P, A);
+  else
+    hipLaunchKernelGGL(attn_units_kernel<false>, dim3(A.grid), dim3(kThreads), 0, s, P, A);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_merge(const DevPool& P, const AttnLaunch& A, hipStream_t s) {
   if (A.n <= 0) return hipSuccess;
-  if (A.grid > 0) {
-    if (P.esize == 1)
-      hipLaunchKernelGGL(attn_units_kernel<true>, dim3(A.grid), dim3(kThreads), 0, s, P, A);
-    else
-      hipLaunchKernelGGL(attn_units_kernel<false>, dim3(A.grid), dim3(kThreads), 0, s, P, A);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
   const int rows = A.n * P.Hq;
   hipLaunchKernelGGL(merge_kernel, dim3((rows + 3) / 4), dim3(256), 0, s, P, A);
   return hipGetLastError();

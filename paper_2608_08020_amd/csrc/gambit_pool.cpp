@@ -116,6 +116,12 @@ struct gambit_pool {
   int n_units = 0;
   int max_splits_used = 0;
   std::vector<int32_t> cnt, first, csr_off, csr_fill, csr;  // per-block planner scratch
+  gambit_stats stats{};            // of plan_list, kept current by decode steps
+
+  // attention-kernel event timing
+  std::vector<hipEvent_t> prof_ev;
+  int prof_used = 0;
+  bool prof_on = false;
 
   std::string last_error;
 };
@@ -264,6 +270,19 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
       }
     }
   }
+  {
+    gambit_stats& st = p->stats;
+    st = gambit_stats{};
+    st.unique_blocks = (int64_t)touched.size();
+    for (int pos = 0; pos < n; ++pos) {
+      const int L = p->seq_len[ids[pos]];
+      st.total_tokens += L;
+      st.table_entries += nb[pos];
+      // every block is full except a trace's partial last block, which only that trace holds
+      st.unique_tokens += L % 16 ? L % 16 - 16 : 0;
+    }
+    st.unique_tokens += 16 * (int64_t)touched.size();
+  }
   // member lists of shared blocks (positions ascending)
   size_t total = 0;
   for (int b : touched) {
@@ -404,6 +423,8 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
   HIP_TRY(p, hipEventRecord(p->plan_ev, s), "plan fence");
   p->plan_list.assign(ids, ids + n);
   p->plan_valid = true;
+  p->stats.n_units = p->n_units;
+  p->stats.max_splits_used = p->max_splits_used;
   return GAMBIT_OK;
 }
 
@@ -504,6 +525,7 @@ gambit_status gambit_pool_destroy(gambit_pool* p) {
   if (p->plan_ev) (void)hipEventSynchronize(p->plan_ev);
   if (p->stage) (void)hipHostFree(p->stage);
   if (p->plan_stage) (void)hipHostFree(p->plan_stage);
+  for (hipEvent_t e : p->prof_ev) (void)hipEventDestroy(e);
   if (p->stage_ev) (void)hipEventDestroy(p->stage_ev);
   if (p->plan_ev) (void)hipEventDestroy(p->plan_ev);
   delete p;
@@ -669,8 +691,19 @@ gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, 
   A.scale_log2 = sm_scale * 1.4426950408889634f;
   A.out = out;
   A.out_f32 = out_dtype == GAMBIT_OUT_F32;
-  HIP_TRY(p, gambit::launch_attention(p->dev, A, s), "attention");
+  const bool timed = p->prof_on && p->prof_used + 2 <= (int)p->prof_ev.size();
+  if (timed) HIP_TRY(p, hipEventRecord(p->prof_ev[p->prof_used], s), "profile event");
+  HIP_TRY(p, gambit::launch_attention_units(p->dev, A, s), "attention");
+  if (timed) {
+    HIP_TRY(p, hipEventRecord(p->prof_ev[p->prof_used + 1], s), "profile event");
+    p->prof_used += 2;
+  }
+  HIP_TRY(p, gambit::launch_attention_merge(p->dev, A, s), "attention merge");
   for (int i = 0; i < n; ++i) mirror_grow(p, ids[i], 1);
+  p->stats.total_tokens += n;
+  p->stats.unique_tokens += n;
+  p->stats.unique_blocks += need;
+  p->stats.table_entries += need;
   return GAMBIT_OK;
 }
 
@@ -798,12 +831,17 @@ gambit_status gambit_plan_stats(gambit_pool* p, int32_t n, const int32_t* ids, g
   if (!p || !out) return GAMBIT_ERR_INVALID;
   gambit_status st = check_ids(p, n, ids, "trace");
   if (st) return st;
+  if (p->plan_valid && (int)p->plan_list.size() == n && std::equal(p->plan_list.begin(), p->plan_list.end(), ids)) {
+    *out = p->stats;
+    return GAMBIT_OK;
+  }
   std::vector<char> seen(p->d.num_blocks, 0);
   gambit_stats r{};
   for (int i = 0; i < n; ++i) {
     const int t = ids[i], L = p->seq_len[t];
     r.total_tokens += L;
     const auto& row = p->table[t];
+    r.table_entries += (int64_t)row.size();
     for (size_t j = 0; j < row.size(); ++j) {
       if (seen[row[j]]) continue;
       seen[row[j]] = 1;
@@ -811,10 +849,37 @@ gambit_status gambit_plan_stats(gambit_pool* p, int32_t n, const int32_t* ids, g
       r.unique_tokens += std::min(16, L - 16 * (int)j);
     }
   }
-  const bool same = p->plan_valid && (int)p->plan_list.size() == n && std::equal(p->plan_list.begin(), p->plan_list.end(), ids);
-  r.n_units = same ? p->n_units : -1;
-  r.max_splits_used = same ? p->max_splits_used : -1;
+  r.n_units = -1;
+  r.max_splits_used = -1;
   *out = r;
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_profile_begin(gambit_pool* p, int32_t max_launches) {
+  if (!p || max_launches < 0) return GAMBIT_ERR_INVALID;
+  for (hipEvent_t e : p->prof_ev) (void)hipEventDestroy(e);
+  p->prof_ev.assign(2 * (size_t)max_launches, nullptr);
+  for (auto& e : p->prof_ev) HIP_TRY(p, hipEventCreate(&e), "profile events");
+  p->prof_used = 0;
+  p->prof_on = true;
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_profile_end(gambit_pool* p, double* attn_ms, int32_t* launches) {
+  if (!p || !attn_ms || !launches) return GAMBIT_ERR_INVALID;
+  double total = 0;
+  if (p->prof_used > 0) HIP_TRY(p, hipEventSynchronize(p->prof_ev[p->prof_used - 1]), "profile sync");
+  for (int i = 0; i + 1 < p->prof_used; i += 2) {
+    float ms = 0;
+    HIP_TRY(p, hipEventElapsedTime(&ms, p->prof_ev[i], p->prof_ev[i + 1]), "profile read");
+    total += ms;
+  }
+  *attn_ms = total;
+  *launches = p->prof_used / 2;
+  for (hipEvent_t e : p->prof_ev) (void)hipEventDestroy(e);
+  p->prof_ev.clear();
+  p->prof_used = 0;
+  p->prof_on = false;
   return GAMBIT_OK;
 }
 

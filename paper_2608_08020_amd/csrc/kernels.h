@@ -77,7 +77,8 @@ hipError_t launch_free(const DevPool& P, const int32_t* ids, int32_t n, hipStrea
 hipError_t launch_fork(const DevPool& P, const int32_t* pairs, int32_t n, int32_t* req_trace,
                        int32_t* req_ntok, hipStream_t s);
 
-hipError_t launch_attention(const DevPool& P, const AttnLaunch& A, hipStream_t s);
+hipError_t launch_attention_units(const DevPool& P, const AttnLaunch& A, hipStream_t s);
+hipError_t launch_attention_merge(const DevPool& P, const AttnLaunch& A, hipStream_t s);
 
 // Probe + sigmoid + ranking + prune/branch plan in one launch.
 struct ProbeLaunch {

@@ -48,7 +48,8 @@ class PoolDesc(ctypes.Structure):
 
 class Stats(ctypes.Structure):
     _fields_ = [("total_tokens", ctypes.c_int64), ("unique_tokens", ctypes.c_int64),
-                ("unique_blocks", ctypes.c_int64), ("n_units", ctypes.c_int32),
+                ("unique_blocks", ctypes.c_int64), ("table_entries", ctypes.c_int64),
+                ("n_units", ctypes.c_int32),
                 ("max_splits_used", ctypes.c_int32)]
 
 
@@ -57,7 +58,7 @@ EXPORTS = ["gambit_workspace_size", "gambit_pool_create", "gambit_pool_destroy",
            "gambit_kv_write", "gambit_kv_fork", "gambit_kv_free", "gambit_decode_attn",
            "gambit_score_prune_branch", "gambit_rank_topk", "gambit_pool_check",
            "gambit_plan_stats", "gambit_seq_len", "gambit_free_blocks", "gambit_status_str",
-           "gambit_last_error"]
+           "gambit_last_error", "gambit_profile_begin", "gambit_profile_end"]
 
 
 def lib() -> ctypes.CDLL:
@@ -85,6 +86,8 @@ def lib() -> ctypes.CDLL:
         "gambit_free_blocks": (i32, [vp]),
         "gambit_status_str": (ctypes.c_char_p, [i32]),
         "gambit_last_error": (ctypes.c_char_p, [vp]),
+        "gambit_profile_begin": (i32, [vp, i32]),
+        "gambit_profile_end": (i32, [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -251,6 +254,16 @@ class Pool:
         s = Stats()
         self._check(lib().gambit_plan_stats(self._h, ids.size, _ptr(ids), ctypes.byref(s)), "plan_stats")
         return s
+
+    def profile_begin(self, max_launches: int):
+        """gambit_profile_begin: time the split-K attention kernel of each decode step."""
+        self._check(lib().gambit_profile_begin(self._h, max_launches), "profile_begin")
+
+    def profile_end(self):
+        """gambit_profile_end: (summed attention-kernel ms, timed launches)."""
+        ms, n = ctypes.c_double(), ctypes.c_int32()
+        self._check(lib().gambit_profile_end(self._h, ctypes.byref(ms), ctypes.byref(n)), "profile_end")
+        return ms.value, n.value
 
     def seq_len_of(self, t: int) -> int:
         return int(lib().gambit_seq_len(self._h, t))
