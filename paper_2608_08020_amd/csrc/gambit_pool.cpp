@@ -61,7 +61,7 @@ bool layout_of(const gambit_pool_desc* d, Layout* L) {
   };
   L->kmax = kmax;
   L->nwords = cdiv(d->num_blocks, 32);
-  L->max_units = T * kmax * d->num_kv_heads;
+  L->max_units = T * kmax * d->num_kv_heads + 64;
   L->max_members = T * kmax;
   L->list = take(4 * (size_t)T);
   L->ids = take(4 * (size_t)T);
@@ -111,8 +111,8 @@ struct gambit_pool {
   // attention plan
   bool plan_valid = false;
   std::vector<int32_t> plan_list;
-  int xcd_off[9] = {0};
-  int grid = 0;
+  int coop_off[9] = {0}, narrow_off[9] = {0};
+  int coop_grid = 0, narrow_grid = 0;
   int n_units = 0;
   int max_splits_used = 0;
   std::vector<int32_t> cnt, first, csr_off, csr_fill, csr;  // per-block planner scratch
@@ -242,14 +242,15 @@ gambit_status check_ids(gambit_pool* p, int32_t n, const int32_t* ids, const cha
 // ends at the trace's current last block (read by the kernel at run time),
 // so the plan stays valid while decode steps append.
 struct Group {
-  std::vector<AttnUnit> units;
+  std::vector<AttnUnit> coop;    // cooperative items (one workgroup each)
+  std::vector<AttnUnit> narrow;  // one-row-block units
   double cost;
 };
 
 gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t s) {
   const int Hkv = p->d.num_kv_heads;
   const int kmax = p->L.kmax;
-  const int tile_members = gambit::kRowsPerWG / p->g;
+  const int tile_members = gambit::kRowsPerUnit / p->g;
   const int nb_total = p->d.num_blocks;
   if ((int)p->cnt.size() != nb_total) {
     p->cnt.assign(nb_total, 0);
@@ -307,23 +308,30 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
     groups.clear();
     members.clear();
     int worst = 0;
-    // One group per (chunk, KV head) holds all its row tiles, so the tiles
-    // that re-read the chunk land on one XCD.
+    // One group per (chunk, KV head): a chunk with <= 16 rows is one narrow
+    // unit; a wider chunk becomes cooperative items of up to 128 rows.
     auto emit = [&](int owner_pos, int jb0, int nblk, int ntok_est, const int32_t* mem, int mcnt,
                     int kidx) {
-      const size_t first_tile = members.size();
-      std::vector<std::pair<int, int>> tiles;
-      for (int m0 = 0; m0 < mcnt; m0 += tile_members) {
-        const int mc = std::min(tile_members, mcnt - m0);
-        tiles.emplace_back((int)(first_tile + m0), mc);
-      }
+      const int moff = (int)members.size();
       members.insert(members.end(), mem, mem + mcnt);
+      const double tok = std::max(ntok_est, 1);
+      if (mcnt * p->g <= gambit::kRowsPerUnit) {
+        for (int h = 0; h < Hkv; ++h) {
+          Group gr;
+          gr.cost = tok;
+          gr.narrow.push_back(AttnUnit{ids[owner_pos], jb0, nblk, h, moff, mcnt, kidx, 0});
+          groups.push_back(std::move(gr));
+        }
+        return;
+      }
+      const int item_members = gambit::kRowsPerCoop / p->g;
       for (int h = 0; h < Hkv; ++h) {
         Group gr;
         gr.cost = 0;
-        for (const auto& tl : tiles) {
-          gr.cost += (double)std::max(ntok_est, 1) * (2.0 + cdiv(tl.second * p->g, 16));
-          gr.units.push_back(AttnUnit{ids[owner_pos], jb0, nblk, h, tl.first, tl.second, kidx, 0});
+        for (int m0 = 0; m0 < mcnt; m0 += item_members) {
+          const int mc = std::min(item_members, mcnt - m0);
+          gr.coop.push_back(AttnUnit{ids[owner_pos], jb0, nblk, h, moff + m0, mc, kidx, 0});
+          gr.cost += 6.0 * tok;
         }
         groups.push_back(std::move(gr));
       }
@@ -349,7 +357,10 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
         int j1 = j + 1;
         while (j1 < nb[pos] && p->cnt[row[j1]] == c) ++j1;
         const int len = j1 - j;
-        const int nch = cdiv(len, chunk_blocks);
+        // a chunk is read by each of its row blocks, so wide runs take longer
+        // chunks: fewer partials, the same bytes per row block
+        const int nrb = cdiv(c * p->g, gambit::kRowsPerUnit);
+        const int nch = cdiv(len, chunk_blocks * std::min(nrb, 2));
         const int b0 = row[j];
         for (int k = 0, jb = j; k < nch; ++k) {
           const int sz = len / nch + (k < len % nch ? 1 : 0);
@@ -390,15 +401,24 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
     load[x] += groups[gi].cost;
     per[x].push_back(gi);
   }
+  // cooperative items (one workgroup each), then narrow units (four per
+  // workgroup), each list grouped by XCD
   std::vector<AttnUnit> units;
-  int maxc = 0;
+  int maxc = 0, maxn = 0;
   for (int x = 0; x < 8; ++x) {
-    p->xcd_off[x] = (int)units.size();
-    for (int gi : per[x]) units.insert(units.end(), groups[gi].units.begin(), groups[gi].units.end());
-    maxc = std::max(maxc, (int)units.size() - p->xcd_off[x]);
+    p->coop_off[x] = (int)units.size();
+    for (int gi : per[x]) units.insert(units.end(), groups[gi].coop.begin(), groups[gi].coop.end());
+    maxc = std::max(maxc, (int)units.size() - p->coop_off[x]);
   }
-  p->xcd_off[8] = (int)units.size();
-  p->grid = 8 * maxc;
+  p->coop_off[8] = (int)units.size();
+  for (int x = 0; x < 8; ++x) {
+    p->narrow_off[x] = (int)units.size();
+    for (int gi : per[x]) units.insert(units.end(), groups[gi].narrow.begin(), groups[gi].narrow.end());
+    maxn = std::max(maxn, (int)units.size() - p->narrow_off[x]);
+  }
+  p->narrow_off[8] = (int)units.size();
+  p->coop_grid = 8 * maxc;
+  p->narrow_grid = 8 * cdiv(maxn, gambit::kUnitsPerWG);
   p->n_units = (int)units.size();
   if ((int)units.size() > p->L.max_units || (int)members.size() > p->L.max_members)
     return fail(p, GAMBIT_ERR_UNSUPPORTED, "plan exceeds workspace bounds");
@@ -680,8 +700,10 @@ gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, 
   gambit::AttnLaunch A{};
   A.q = static_cast<const uint16_t*>(q);
   A.units = ws_ptr<AttnUnit>(p, p->L.units);
-  std::memcpy(A.xcd_off, p->xcd_off, sizeof A.xcd_off);
-  A.grid = p->grid;
+  std::memcpy(A.coop_off, p->coop_off, sizeof A.coop_off);
+  std::memcpy(A.narrow_off, p->narrow_off, sizeof A.narrow_off);
+  A.coop_grid = p->coop_grid;
+  A.narrow_grid = p->narrow_grid;
   A.members = ws_ptr<int32_t>(p, p->L.members);
   A.nk = ws_ptr<int32_t>(p, p->L.nk);
   A.part_acc = ws_ptr<float>(p, p->L.part_acc);

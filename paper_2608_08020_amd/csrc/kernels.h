@@ -10,10 +10,13 @@ namespace gambit {
 
 constexpr int kBlock = 16;     // tokens per KV block
 constexpr int kHeadDim = 128;  // head dimension the kernels implement
-constexpr int kRowsPerWG = 128;  // attention rows (trace x q-head) one workgroup holds
+constexpr int kRowsPerUnit = 16;  // attention rows (trace x q-head) of one unit (one wavefront)
+constexpr int kUnitsPerWG = 4;
 
-// One attention work unit: a run of blocks that the same member traces share,
-// for one KV head and one tile of member traces.
+// One attention work entry: a chunk of a run of blocks that the same member
+// traces share, for one KV head, and either one block of <= 16 rows (a
+// narrow unit, one wavefront) or up to 64 rows (a cooperative item, one
+// workgroup).
 struct AttnUnit {
   int32_t owner;    // trace whose block-table row lists the run's blocks
   int32_t jb0;      // first logical block of the run
@@ -22,8 +25,10 @@ struct AttnUnit {
   int32_t mem_off;  // first member (list position) in the member array
   int32_t mem_cnt;  // members in this tile; 0 = padding unit (does nothing)
   int32_t kidx;     // partial slot of this run for every member
-  int32_t pad;
+  int32_t flags;    // reserved, 0
 };
+
+constexpr int kRowsPerCoop = 64;  // rows of one cooperative item (4 waves x 1 row block)
 
 // Device view of a pool.
 struct DevPool {
@@ -49,9 +54,11 @@ enum : int32_t {
 
 struct AttnLaunch {
   const uint16_t* q;        // [n][Hq][128] bf16
-  const AttnUnit* units;    // grouped by XCD: XCD x runs units [xcd_off[x], xcd_off[x+1])
-  int32_t xcd_off[9];
-  int32_t grid;             // 8 * (largest per-XCD count)
+  const AttnUnit* units;    // cooperative items, then narrow units, each list grouped by XCD
+  int32_t coop_off[9];      // XCD x runs cooperative items [coop_off[x], coop_off[x+1]), one per workgroup
+  int32_t narrow_off[9];    // and narrow units [narrow_off[x], narrow_off[x+1]), four per workgroup
+  int32_t coop_grid;        // 8 * (largest per-XCD item count)
+  int32_t narrow_grid;      // 8 * (largest per-XCD count of 4-unit workgroups)
   const int32_t* members;   // list positions
   const int32_t* nk;        // [n] partials per list position
   float* part_acc;          // [n][Hq][kmax][128]
