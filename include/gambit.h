@@ -88,7 +88,7 @@ typedef struct {
   int32_t kv_dtype;              /* GAMBIT_KV_*                             */
   int32_t max_traces;            /* trace ids are 0 .. max_traces-1         */
   int32_t max_blocks_per_trace;
-  int32_t max_splits;            /* attention partials per (trace, head); 0 = 64 */
+  int32_t max_splits;            /* attention partials per (trace, head), <= 64; 0 = 64 */
   float fp8_append_scale;        /* scale of blocks a decode step allocates; 0 = 2^-6 */
   void* k_cache;
   void* v_cache;

@@ -10,7 +10,7 @@
 // partial (reference max, sum, accumulator) that the merge kernel combines
 // by log-sum-exp.
 //
-// Two kinds of workgroup share one launch:
+// Two kinds of workgroup share one launch, interleaved on every XCD:
 //  * narrow: four independent one-row-block units, one per wave.  A wave
 //    streams its chunk 32 tokens at a time straight from HBM into matrix-core
 //    operand layouts, double-buffered in registers, with no LDS and no
@@ -576,45 +576,65 @@ __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit&
 }
 
 // Workgroups are dispatched round-robin over the 8 XCDs, so workgroup bid
-// runs on XCD bid % 8.  The plan lists every XCD's work contiguously.
+// runs on XCD bid % 8.  The plan lists every XCD's workgroup slots
+// contiguously, four entries per slot: a cooperative item (flagged in its
+// first entry) or four narrow units.  Cooperative (compute-bound) and
+// narrow (HBM-bound) slots are interleaved so both kinds share every CU.
 template <bool FP8>
-__global__ __launch_bounds__(kThreads, 3) void attn_coop_kernel(DevPool P, AttnLaunch A) {
+__global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(DevPool P, AttnLaunch A) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[2][2][32 * kLdsRow];
   const int x = blockIdx.x & 7, slot = blockIdx.x >> 3;
-  const int item = A.coop_off[x] + slot;
-  if (item >= A.coop_off[x + 1]) return;  // uniform over the workgroup
-  const AttnUnit U = A.units[item];
-  if (U.mem_cnt > 0) coop_unit<FP8>(P, A, U, threadIdx.x >> 6, threadIdx.x & 63, lds);
+  const int base = A.xcd_off[x] + 4 * slot, end = A.xcd_off[x + 1];
+  if (base >= end) return;  // uniform over the workgroup
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const AttnUnit U0 = A.units[base];
+  if (U0.flags & kUnitCoop) {
+    if (U0.mem_cnt > 0) coop_unit<FP8>(P, A, U0, wave, lane, lds);
+    return;
+  }
+  if (base + wave >= end) return;  // no barrier on the narrow path
+  const AttnUnit U = A.units[base + wave];
+  if (U.mem_cnt > 0) narrow_unit<FP8>(P, A, U, lane);
 }
 
-template <bool FP8>
-__global__ __launch_bounds__(kThreads, 2) void attn_narrow_kernel(DevPool P, AttnLaunch A) {
-  const int x = blockIdx.x & 7, slot = blockIdx.x >> 3;
-  const int u = A.narrow_off[x] + 4 * slot + (threadIdx.x >> 6);
-  if (u >= A.narrow_off[x + 1]) return;  // no barrier in this kernel
-  const AttnUnit U = A.units[u];
-  if (U.mem_cnt > 0) narrow_unit<FP8>(P, A, U, threadIdx.x & 63);
-}
-
-// Log-sum-exp merge of a row's partials, in partial-slot order.  One wave
-// per (list position, query head); lane l owns d = 2 l, 2 l + 1.
+// Log-sum-exp merge of a row's partials.  One wave per (list position,
+// query head): lane k < nk reads partial k's (max, sum), the wave reduces the
+// maximum and the weighted sum, then every lane accumulates its two d values
+// over the partials with the weights broadcast from their lanes.
 __global__ __launch_bounds__(256) void merge_kernel(DevPool P, AttnLaunch A) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= A.n * P.Hq) return;
   const int lane = threadIdx.x & 63;
   const int pos = row / P.Hq;
-  const int nk = A.nk[pos];
+  const int nk = A.nk[pos];  // <= kmax <= 64
   const float2* ml = A.part_ml + (size_t)row * A.kmax;
   const float* pa = A.part_acc + (size_t)row * A.kmax * kHeadDim;
-  float M = -INFINITY;
-  for (int k = 0; k < nk; ++k) M = fmaxf(M, ml[k].x);
-  float L = 0.f, o0 = 0.f, o1 = 0.f;
-  for (int k = 0; k < nk; ++k) {
-    const float w = exp2f(ml[k].x - M);
-    L += w * ml[k].y;
+  const float2 mine = lane < nk ? ml[lane] : float2{-INFINITY, 0.f};
+  float M = mine.x;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+  const float w = lane < nk ? exp2f(mine.x - M) : 0.f;
+  float L = w * mine.y;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) L += __shfl_xor(L, off);
+  float o0 = 0.f, o1 = 0.f;
+  int k = 0;
+  for (; k + 4 <= nk; k += 4) {
+    float2 a[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) a[j] = *reinterpret_cast<const float2*>(pa + (size_t)(k + j) * kHeadDim + 2 * lane);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float wk = __shfl(w, k + j);
+      o0 += wk * a[j].x;
+      o1 += wk * a[j].y;
+    }
+  }
+  for (; k < nk; ++k) {
     const float2 a = *reinterpret_cast<const float2*>(pa + (size_t)k * kHeadDim + 2 * lane);
-    o0 += w * a.x;
-    o1 += w * a.y;
+    const float wk = __shfl(w, k);
+    o0 += wk * a.x;
+    o1 += wk * a.y;
   }
   const float inv = 1.f / L;
   o0 *= inv;
@@ -629,21 +649,11 @@ __global__ __launch_bounds__(256) void merge_kernel(DevPool P, AttnLaunch A) {
 }  // namespace
 
 hipError_t launch_attention_units(const DevPool& P, const AttnLaunch& A, hipStream_t s) {
-  if (A.n <= 0) return hipSuccess;
-  if (A.coop_grid > 0) {
-    if (P.esize == 1)
-      hipLaunchKernelGGL(attn_coop_kernel<true>, dim3(A.coop_grid), dim3(kThreads), 0, s, P, A);
-    else
-      hipLaunchKernelGGL(attn_coop_kernel<false>, dim3(A.coop_grid), dim3(kThreads), 0, s, P, A);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  if (A.narrow_grid > 0) {
-    if (P.esize == 1)
-      hipLaunchKernelGGL(attn_narrow_kernel<true>, dim3(A.narrow_grid), dim3(kThreads), 0, s, P, A);
-    else
-      hipLaunchKernelGGL(attn_narrow_kernel<false>, dim3(A.narrow_grid), dim3(kThreads), 0, s, P, A);
-  }
+  if (A.n <= 0 || A.grid <= 0) return hipSuccess;
+  if (P.esize == 1)
+    hipLaunchKernelGGL(attn_units_kernel<true>, dim3(A.grid), dim3(kThreads), 0, s, P, A);
+  else
+    hipLaunchKernelGGL(attn_units_kernel<false>, dim3(A.grid), dim3(kThreads), 0, s, P, A);
   return hipGetLastError();
 }
 

@@ -50,7 +50,7 @@ bool layout_of(const gambit_pool_desc* d, Layout* L) {
   const int g = d->num_q_heads / d->num_kv_heads;
   if (g != 1 && g != 2 && g != 4 && g != 8 && g != 16) return false;
   if (d->kv_dtype != GAMBIT_KV_BF16 && d->kv_dtype != GAMBIT_KV_FP8_E4M3) return false;
-  if (d->max_traces <= 0 || d->max_blocks_per_trace <= 0 || d->max_splits < 0) return false;
+  if (d->max_traces <= 0 || d->max_blocks_per_trace <= 0 || d->max_splits < 0 || d->max_splits > 64) return false;
   const int T = d->max_traces;
   const int kmax = d->max_splits ? d->max_splits : kDefaultSplits;
   size_t o = 0;
@@ -61,7 +61,7 @@ bool layout_of(const gambit_pool_desc* d, Layout* L) {
   };
   L->kmax = kmax;
   L->nwords = cdiv(d->num_blocks, 32);
-  L->max_units = T * kmax * d->num_kv_heads + 64;
+  L->max_units = 2 * T * kmax * d->num_kv_heads + 64;
   L->max_members = T * kmax;
   L->list = take(4 * (size_t)T);
   L->ids = take(4 * (size_t)T);
@@ -111,8 +111,8 @@ struct gambit_pool {
   // attention plan
   bool plan_valid = false;
   std::vector<int32_t> plan_list;
-  int coop_off[9] = {0}, narrow_off[9] = {0};
-  int coop_grid = 0, narrow_grid = 0;
+  int xcd_off[9] = {0};
+  int grid = 0;
   int n_units = 0;
   int max_splits_used = 0;
   std::vector<int32_t> cnt, first, csr_off, csr_fill, csr;  // per-block planner scratch
@@ -330,7 +330,7 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
         gr.cost = 0;
         for (int m0 = 0; m0 < mcnt; m0 += item_members) {
           const int mc = std::min(item_members, mcnt - m0);
-          gr.coop.push_back(AttnUnit{ids[owner_pos], jb0, nblk, h, moff + m0, mc, kidx, 0});
+          gr.coop.push_back(AttnUnit{ids[owner_pos], jb0, nblk, h, moff + m0, mc, kidx, gambit::kUnitCoop});
           gr.cost += 6.0 * tok;
         }
         groups.push_back(std::move(gr));
@@ -401,24 +401,37 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
     load[x] += groups[gi].cost;
     per[x].push_back(gi);
   }
-  // cooperative items (one workgroup each), then narrow units (four per
-  // workgroup), each list grouped by XCD
+  // Workgroup slots of four entries per XCD: a cooperative item (repeated
+  // four times, flagged) or four narrow units.  The two kinds are interleaved
+  // in proportion so compute-bound and HBM-bound workgroups share every CU.
   std::vector<AttnUnit> units;
-  int maxc = 0, maxn = 0;
+  int maxs = 0;
+  const AttnUnit empty{0, 0, 0, 0, 0, 0, 0, 0};
   for (int x = 0; x < 8; ++x) {
-    p->coop_off[x] = (int)units.size();
-    for (int gi : per[x]) units.insert(units.end(), groups[gi].coop.begin(), groups[gi].coop.end());
-    maxc = std::max(maxc, (int)units.size() - p->coop_off[x]);
+    p->xcd_off[x] = (int)units.size();
+    std::vector<AttnUnit> C, N;
+    for (int gi : per[x]) {
+      C.insert(C.end(), groups[gi].coop.begin(), groups[gi].coop.end());
+      N.insert(N.end(), groups[gi].narrow.begin(), groups[gi].narrow.end());
+    }
+    const long nC = (long)C.size(), nN = cdiv((int)N.size(), gambit::kUnitsPerWG);
+    long ci = 0, ni = 0;
+    while (ci < nC || ni < nN) {
+      if (ni >= nN || (ci < nC && ci * nN <= ni * nC)) {
+        for (int w = 0; w < gambit::kUnitsPerWG; ++w) units.push_back(C[ci]);
+        ++ci;
+      } else {
+        for (int w = 0; w < gambit::kUnitsPerWG; ++w) {
+          const size_t k = (size_t)ni * gambit::kUnitsPerWG + w;
+          units.push_back(k < N.size() ? N[k] : empty);
+        }
+        ++ni;
+      }
+    }
+    maxs = std::max(maxs, (int)((units.size() - p->xcd_off[x]) / gambit::kUnitsPerWG));
   }
-  p->coop_off[8] = (int)units.size();
-  for (int x = 0; x < 8; ++x) {
-    p->narrow_off[x] = (int)units.size();
-    for (int gi : per[x]) units.insert(units.end(), groups[gi].narrow.begin(), groups[gi].narrow.end());
-    maxn = std::max(maxn, (int)units.size() - p->narrow_off[x]);
-  }
-  p->narrow_off[8] = (int)units.size();
-  p->coop_grid = 8 * maxc;
-  p->narrow_grid = 8 * cdiv(maxn, gambit::kUnitsPerWG);
+  p->xcd_off[8] = (int)units.size();
+  p->grid = 8 * maxs;
   p->n_units = (int)units.size();
   if ((int)units.size() > p->L.max_units || (int)members.size() > p->L.max_members)
     return fail(p, GAMBIT_ERR_UNSUPPORTED, "plan exceeds workspace bounds");
@@ -527,6 +540,7 @@ gambit_status gambit_pool_create(const gambit_pool_desc* desc, void* stream, gam
   if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void**>(&p->plan_stage), p->plan_stage_bytes, hipHostMallocDefault);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&p->stage_ev, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&p->plan_ev, hipEventDisableTiming);
+
   if (e == hipSuccess) e = hipEventRecord(p->stage_ev, S(stream));
   if (e == hipSuccess) e = hipEventRecord(p->plan_ev, S(stream));
   if (e == hipSuccess) e = hipMemsetAsync(p->ws + L.ticket, 0, 64, S(stream));
@@ -548,6 +562,7 @@ gambit_status gambit_pool_destroy(gambit_pool* p) {
   for (hipEvent_t e : p->prof_ev) (void)hipEventDestroy(e);
   if (p->stage_ev) (void)hipEventDestroy(p->stage_ev);
   if (p->plan_ev) (void)hipEventDestroy(p->plan_ev);
+
   delete p;
   return GAMBIT_OK;
 }
@@ -700,10 +715,8 @@ gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, 
   gambit::AttnLaunch A{};
   A.q = static_cast<const uint16_t*>(q);
   A.units = ws_ptr<AttnUnit>(p, p->L.units);
-  std::memcpy(A.coop_off, p->coop_off, sizeof A.coop_off);
-  std::memcpy(A.narrow_off, p->narrow_off, sizeof A.narrow_off);
-  A.coop_grid = p->coop_grid;
-  A.narrow_grid = p->narrow_grid;
+  std::memcpy(A.xcd_off, p->xcd_off, sizeof A.xcd_off);
+  A.grid = p->grid;
   A.members = ws_ptr<int32_t>(p, p->L.members);
   A.nk = ws_ptr<int32_t>(p, p->L.nk);
   A.part_acc = ws_ptr<float>(p, p->L.part_acc);

@@ -25,8 +25,10 @@ struct AttnUnit {
   int32_t mem_off;  // first member (list position) in the member array
   int32_t mem_cnt;  // members in this tile; 0 = padding unit (does nothing)
   int32_t kidx;     // partial slot of this run for every member
-  int32_t flags;    // reserved, 0
+  int32_t flags;    // kUnitCoop in the first entry of a cooperative workgroup slot
 };
+
+enum : int32_t { kUnitCoop = 1 };
 
 constexpr int kRowsPerCoop = 64;  // rows of one cooperative item (4 waves x 1 row block)
 
@@ -54,11 +56,9 @@ enum : int32_t {
 
 struct AttnLaunch {
   const uint16_t* q;        // [n][Hq][128] bf16
-  const AttnUnit* units;    // cooperative items, then narrow units, each list grouped by XCD
-  int32_t coop_off[9];      // XCD x runs cooperative items [coop_off[x], coop_off[x+1]), one per workgroup
-  int32_t narrow_off[9];    // and narrow units [narrow_off[x], narrow_off[x+1]), four per workgroup
-  int32_t coop_grid;        // 8 * (largest per-XCD item count)
-  int32_t narrow_grid;      // 8 * (largest per-XCD count of 4-unit workgroups)
+  const AttnUnit* units;    // workgroup slots of 4 entries, grouped by XCD
+  int32_t xcd_off[9];       // XCD x runs entries [xcd_off[x], xcd_off[x+1])
+  int32_t grid;             // 8 * (largest per-XCD slot count)
   const int32_t* members;   // list positions
   const int32_t* nk;        // [n] partials per list position
   float* part_acc;          // [n][Hq][kmax][128]
