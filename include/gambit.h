@@ -69,8 +69,15 @@ typedef struct gambit_pool gambit_pool;
 
 /*
  * Pool description.  Layouts (all device memory, caller-owned):
- *   k_cache, v_cache  [num_blocks][num_kv_heads][block_size][head_dim]
- *                     bf16, or OCP E4M3FN bytes for GAMBIT_KV_FP8_E4M3
+ *   k_cache, v_cache  num_blocks x num_kv_heads tiles of block_size x
+ *                     head_dim elements, bf16 or OCP E4M3FN bytes for
+ *                     GAMBIT_KV_FP8_E4M3 (tile bytes = 16 * 128 * element
+ *                     size).  Inside a tile, with C = 16 / element size:
+ *                       K element (token t, dim d) at element index
+ *                         ((d / C) * 16 + p(t)) * C + d % C,
+ *                         p(t) = t with its bits 2 and 3 swapped;
+ *                       V element (t, d) at element index d * 16 + t.
+ *                     Only the library's kernels write the caches.
  *   kv_scale          [num_blocks][2] fp32 (K scale, V scale); fp8 only,
  *                     NULL for bf16.  A stored fp8 value means code * scale.
  *   block_table       [max_traces][max_blocks_per_trace] int32, -1 = none

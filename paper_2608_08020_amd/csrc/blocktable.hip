@@ -107,19 +107,28 @@ __global__ __launch_bounds__(kAllocThreads) void alloc_kernel(DevPool P, const i
   }
 }
 
-// Copy one token's K and V (all KV heads) into the cache.  One workgroup per
-// token; chunks of 16 bytes.
+// Copy one token's K and V (all KV heads) into its cache slot: K in 16-byte
+// d-chunks at token row k_phys(row), V element-wise into the transposed tile.
 __device__ inline void copy_token(const DevPool& P, int blk, int row, const uint8_t* ksrc,
                                   const uint8_t* vsrc) {
-  const int row_bytes = kHeadDim * P.esize;           // one head, one token
-  const int chunks = P.Hkv * row_bytes / 16;
-  for (int c = threadIdx.x; c < chunks; c += blockDim.x) {
-    const int head = c / (row_bytes / 16);
-    const int cc = c % (row_bytes / 16);
-    const size_t dst = (((size_t)blk * P.Hkv + head) * kBlock + row) * row_bytes + cc * 16;
-    const size_t src = (size_t)head * row_bytes + cc * 16;
-    *reinterpret_cast<uint4*>(P.k_cache + dst) = *reinterpret_cast<const uint4*>(ksrc + src);
-    *reinterpret_cast<uint4*>(P.v_cache + dst) = *reinterpret_cast<const uint4*>(vsrc + src);
+  const int es = P.esize;
+  const int row_bytes = kHeadDim * es;  // one head, one token
+  const int kchunks = row_bytes / 16;
+  const size_t tile = (size_t)kBlock * row_bytes;
+  const size_t blk0 = (size_t)blk * P.Hkv * tile;
+  const int pr = k_phys(row);
+  for (int c = threadIdx.x; c < P.Hkv * kchunks; c += blockDim.x) {
+    const int head = c / kchunks, cc = c % kchunks;
+    const size_t dst = blk0 + head * tile + ((size_t)cc * kBlock + pr) * 16;
+    *reinterpret_cast<uint4*>(P.k_cache + dst) = *reinterpret_cast<const uint4*>(ksrc + (size_t)c * 16);
+  }
+  for (int e = threadIdx.x; e < P.Hkv * kHeadDim; e += blockDim.x) {
+    const int head = e / kHeadDim, d = e % kHeadDim;
+    const size_t dst = blk0 + head * tile + ((size_t)d * kBlock + row) * es;
+    if (es == 2)
+      *reinterpret_cast<uint16_t*>(P.v_cache + dst) = reinterpret_cast<const uint16_t*>(vsrc)[e];
+    else
+      P.v_cache[dst] = vsrc[e];
   }
 }
 
@@ -203,13 +212,13 @@ __global__ void fork_share_kernel(DevPool P, const int32_t* pairs, int32_t* req_
   }
 }
 
-// Branch, part 2: copy the partial tail (valid tokens, every KV head) and
-// its fp8 scales into the child's new block.
+// Branch, part 2: copy the partial tail block (every KV head; whole tiles,
+// the slots past the tail are never read unmasked) and its fp8 scales into
+// the child's new block.
 __global__ void fork_tail_kernel(DevPool P, const int32_t* pairs) {
   const int child = pairs[2 * blockIdx.x], parent = pairs[2 * blockIdx.x + 1];
   const int L = P.seq_len[parent];
-  const int tail = L % kBlock;
-  if (tail == 0) return;
+  if (L % kBlock == 0) return;
   const int j = L / kBlock;
   const int src = P.table[(size_t)parent * P.max_blocks + j];
   const int dst = P.table[(size_t)child * P.max_blocks + j];
@@ -217,17 +226,14 @@ __global__ void fork_tail_kernel(DevPool P, const int32_t* pairs) {
     if (threadIdx.x == 0) atomicOr(P.err, kErrBadBlock);
     return;
   }
-  const int row_bytes = kHeadDim * P.esize;
-  const int chunks_per_row = row_bytes / 16;
-  const int chunks = P.Hkv * tail * chunks_per_row;
-  for (int c = threadIdx.x; c < chunks; c += blockDim.x) {
-    const int head = c / (tail * chunks_per_row);
-    const int rem = c % (tail * chunks_per_row);
-    const int row = rem / chunks_per_row, cc = rem % chunks_per_row;
-    const size_t so = (((size_t)src * P.Hkv + head) * kBlock + row) * row_bytes + cc * 16;
-    const size_t d0 = (((size_t)dst * P.Hkv + head) * kBlock + row) * row_bytes + cc * 16;
-    *reinterpret_cast<uint4*>(P.k_cache + d0) = *reinterpret_cast<const uint4*>(P.k_cache + so);
-    *reinterpret_cast<uint4*>(P.v_cache + d0) = *reinterpret_cast<const uint4*>(P.v_cache + so);
+  const size_t blk_bytes = (size_t)P.Hkv * kBlock * kHeadDim * P.esize;
+  const uint4* ks = reinterpret_cast<const uint4*>(P.k_cache + (size_t)src * blk_bytes);
+  const uint4* vs = reinterpret_cast<const uint4*>(P.v_cache + (size_t)src * blk_bytes);
+  uint4* kd = reinterpret_cast<uint4*>(P.k_cache + (size_t)dst * blk_bytes);
+  uint4* vd = reinterpret_cast<uint4*>(P.v_cache + (size_t)dst * blk_bytes);
+  for (size_t c = threadIdx.x; c < blk_bytes / 16; c += blockDim.x) {
+    kd[c] = ks[c];
+    vd[c] = vs[c];
   }
   if (P.kv_scale && threadIdx.x == 0) {
     P.kv_scale[2 * dst] = P.kv_scale[2 * src];

@@ -13,26 +13,27 @@
 // Two kinds of workgroup share one launch, interleaved on every XCD:
 //  * narrow: four independent one-row-block units, one per wave.  A wave
 //    streams its chunk 32 tokens at a time straight from HBM into matrix-core
-//    operand layouts, double-buffered in registers, with no LDS and no
-//    barrier (this is where most of the bytes are: chunks that 1-4 traces
-//    share).
+//    operand registers, double-buffered, with no LDS and no barrier (this is
+//    where most of the bytes are: chunks that 1-4 traces share).
 //  * cooperative: one chunk with 2-4 row blocks (more rows become several
 //    workgroups).  The workgroup stages each 32-token tile into LDS once
 //    (double-buffered) and each wave applies it to its row block, so a chunk
 //    is read from L2/HBM once per four row blocks instead of once per row
-//    block; many row blocks re-reading one chunk through L2 otherwise
-//    contend for the same L2 channels.
+//    block.
 //
 // The contractions run on the bf16 matrix cores (v_mfma_f32_16x16x32_bf16):
 //   S^T[token][row] = K[token][:] . Q[row][:]          (A = K, B = Q^T)
 //   O^T[d][row]    += V^T[d][token] . P^T[token][row]   (A = V^T, B = P^T)
-// Computing S transposed leaves each lane holding, for one row, four
-// consecutive tokens of each 16-token half, which is exactly the B-operand
-// layout of the second product, so P never moves between lanes.  V is read
-// as 16 bytes of d for each of a lane's 8 tokens and transposed in
-// registers.  P is split into bf16 hi + lo parts (two MFMAs) so the P.V
-// product keeps ~16 bits of P.  fp8 E4M3 K/V are widened to bf16 (exact);
-// a block's K scale multiplies its 16 scores and the V scale multiplies P.
+// Of a 32-token tile (blocks b0, b1), the first S^T product takes tokens
+// 8 j + {0..3} and the second 8 j + {4..7} (j = 0..3) as its 16 A rows, so
+// lane group q ends up holding, for its row, the scores of tokens 8 q .. 8 q
+// + 7: exactly the B operand of the second product, and V^T's A operand is
+// then 8 consecutive tokens of one d.  The cache tile layout (K in 16-byte
+// d-chunks with token rows in k_phys order, V transposed) makes each
+// operand one 16-byte load per lane and each load instruction a few whole
+// 128-byte lines.  P is split into bf16 hi + lo parts (two MFMAs) so the P.V
+// product keeps ~16 bits of P.  fp8 E4M3 K/V are widened to bf16 (exact); a
+// block's K scale multiplies its scores and its V scale multiplies P.
 #include <cmath>
 
 #include "kernels.h"
@@ -41,26 +42,37 @@ namespace gambit {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;                      // four waves
+constexpr int kTileBytes = kBlock * kHeadDim * 2;  // one bf16 (block, head) tile
+// LDS stage of one 32-token tile, always bf16: K of the two blocks (the
+// second shifted by 128 bytes, so the two 128-byte halves of a K read fall
+// in different banks), then V^T of the two blocks, whose 16-byte halves of
+// a d row are swapped when bit 3 of d is set (conflict-free V reads).
+constexpr int kLdsK1 = kTileBytes + 128;
+constexpr int kLdsV = kLdsK1 + kTileBytes;
+constexpr int kStage = kLdsV + 2 * kTileBytes;
+
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kThreads = 256;          // four waves
-constexpr int kLdsRow = 2 * kHeadDim;  // bytes of one bf16 token row of one head
-
+// Two floats -> two bf16 (round to nearest even) in one dword, a in the low half.
 __device__ inline uint32_t pack_bf16x2(float a, float b) {
-  const __bf16 x = (__bf16)a, y = (__bf16)b;
-  return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
 }
 
-// 8 fp8 E4M3 codes (two dwords) -> 8 bf16.  The widening is exact.
-__device__ inline bf16x8 fp8x8_to_bf16(uint32_t w0, uint32_t w1) {
-  const f32x2 a = __builtin_amdgcn_cvt_pk_f32_fp8(w0, false);
-  const f32x2 b = __builtin_amdgcn_cvt_pk_f32_fp8(w0, true);
-  const f32x2 c = __builtin_amdgcn_cvt_pk_f32_fp8(w1, false);
-  const f32x2 d = __builtin_amdgcn_cvt_pk_f32_fp8(w1, true);
-  const uint4 u = make_uint4(pack_bf16x2(a[0], a[1]), pack_bf16x2(b[0], b[1]), pack_bf16x2(c[0], c[1]),
-                             pack_bf16x2(d[0], d[1]));
-  return __builtin_bit_cast(bf16x8, u);
+// fp8 E4M3 codes -> bf16 (exact: unit scale).  Code k of a dword becomes
+// element k of the result.
+__device__ inline uint2 fp8x4_to_bf16(uint32_t w) {
+  const bf16x2 a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.f, false);
+  const bf16x2 b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.f, true);
+  return make_uint2(__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b));
+}
+
+__device__ inline uint4 fp8x8_to_bf16(uint32_t w0, uint32_t w1) {
+  const uint2 a = fp8x4_to_bf16(w0), b = fp8x4_to_bf16(w1);
+  return make_uint4(a.x, a.y, b.x, b.y);
 }
 
 __device__ inline float wave_max_over_groups(float x) {
@@ -75,10 +87,6 @@ __device__ inline float wave_sum_over_groups(float x) {
   return x;
 }
 
-// Token of the 32-token tile that B-operand element e of lane group q holds:
-// 4 q + e for e < 4 (first 16-token half), 16 + 4 q + e - 4 otherwise.
-__device__ inline int tile_token(int q, int e) { return e < 4 ? 4 * q + e : 12 + 4 * q + e; }
-
 // d layout of the A/B operands of S^T (the same for K and Q):
 //   natural:  operand kb, lane group q, element e  ->  d = 32 kb + 8 q + e
 //   fp8 HBM:  operand kb, lane group q, element e  ->  d = 64 (kb/2) + 16 q + 8 (kb%2) + e
@@ -87,15 +95,28 @@ __device__ inline int q_offset(bool fp8_direct, int kb, int q) {
   return fp8_direct ? 64 * (kb >> 1) + 16 * q + 8 * (kb & 1) : 32 * kb + 8 * q;
 }
 
-// 16 chunks of 16 B per LDS token row, XOR-swizzled by the row so that the
-// K reads (one chunk index over 16 rows) and V reads (16 chunks of one row)
-// hit distinct banks.
-__device__ inline int lds_off(int row, int chunk) { return row * kLdsRow + ((chunk ^ (row & 15)) << 4); }
-
 template <bool FP8>
 __device__ inline size_t head_off(int b, int Hkv, int kvh) {
   constexpr size_t kTileHead = (size_t)kBlock * (FP8 ? kHeadDim : 2 * kHeadDim);
   return ((size_t)b * Hkv + kvh) * kTileHead;
+}
+
+// Keep the first nv of 8 bf16 values (two per dword).
+__device__ inline uint4 keep_first(uint4 x, int nv) {
+  x.x &= nv >= 2 ? 0xffffffffu : (nv == 1 ? 0xffffu : 0u);
+  x.y &= nv >= 4 ? 0xffffffffu : (nv == 3 ? 0xffffu : 0u);
+  x.z &= nv >= 6 ? 0xffffffffu : (nv == 5 ? 0xffffu : 0u);
+  x.w &= nv >= 8 ? 0xffffffffu : (nv == 7 ? 0xffffu : 0u);
+  return x;
+}
+
+// Keep the first nv of 16 fp8 codes (four per dword).
+__device__ inline uint32_t keep_bytes(uint32_t w, int n) {
+  return n >= 4 ? w : (n <= 0 ? 0u : w & ((1u << (8 * n)) - 1u));
+}
+
+__device__ inline uint4 keep_first16(uint4 x, int nv) {
+  return make_uint4(keep_bytes(x.x, nv), keep_bytes(x.y, nv - 4), keep_bytes(x.z, nv - 8), keep_bytes(x.w, nv - 12));
 }
 
 struct RowState {
@@ -125,76 +146,53 @@ __device__ inline void qk_mfma(const bf16x8 (&kf)[2][4], const bf16x8 (&qf)[4], 
   }
 }
 
-// Softmax update for one tile; returns P (scaled by the V scales) as bf16
-// hi + lo.  lane (lq, lr): s0[e] is token t0 + 4 lq + e, s1[e] token
-// t0 + 16 + 4 lq + e, of row lr.
-__device__ inline void softmax_p(f32x4 s0, f32x4 s1, int t0, int ntok, int lq, float c0, float c1, float vs0,
-                                 float vs1, RowState& st, bf16x8& ph, bf16x8& pl) {
-  float sv[8];
+// Softmax update for one tile.  Lane (q, row): s0[e] and s1[e] are the raw
+// scores of tokens 8 q + e and 8 q + 4 + e; c = softmax scale x log2(e) x the
+// block's K scale; the first nv of the lane's 8 tokens exist when `partial`.
+// Returns P (times the block's V scale for fp8) as bf16 hi + lo.
+template <bool FP8>
+__device__ inline void softmax_p(const f32x4& s0, const f32x4& s1, bool partial, int nv, float c, float vsc,
+                                 RowState& st, bf16x8& ph, bf16x8& pl) {
+  float sv[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+  if (partial) {
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    sv[e] = s0[e] * c0;
-    sv[4 + e] = s1[e] * c1;
+    for (int e = 0; e < 8; ++e) sv[e] = e < nv ? sv[e] : -INFINITY;
   }
-  if (t0 + 32 > ntok) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (t0 + tile_token(lq, e) >= ntok) sv[e] = -INFINITY;
-  }
-  float mx = sv[0];
-#pragma unroll
-  for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
+  float mx = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])), fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
+  mx *= c;  // c > 0
   // Move a row's reference only when one of its scores outgrows it by more
   // than 2^kLazy (always on the first tile, whose reference is -inf).  The
   // lane-local test needs no cross-lane traffic; only when some lane fails
   // it are the row maxima reduced over the row's four lanes.
   if (__builtin_amdgcn_ballot_w64(mx > st.m + kLazy)) {
     mx = wave_max_over_groups(mx);
-    const bool move = mx > st.m + kLazy;
-    const float m_new = move ? mx : st.m;
-    const float alpha = exp2f(st.m - m_new);
+    const float m_new = mx > st.m + kLazy ? mx : st.m;
+    const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
     st.l *= alpha;
 #pragma unroll
     for (int r = 0; r < 8; ++r) st.acc[r] *= alpha;
     st.m = m_new;
   }
-  float psum = 0.f, hi[8], lo[8];
+  const float nm = -st.m;
+  float p[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const float p = exp2f(sv[e] - st.m);
-    psum += p;
-    const float pv = p * (e < 4 ? vs0 : vs1);
-    hi[e] = (float)(__bf16)pv;  // exact in fp32
-    lo[e] = pv - hi[e];
+  for (int e = 0; e < 8; ++e) p[e] = __builtin_amdgcn_exp2f(fmaf(sv[e], c, nm));
+  st.l += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+  uint32_t hw[4], lw[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float a = p[2 * j], b = p[2 * j + 1];
+    if constexpr (FP8) {
+      a *= vsc;
+      b *= vsc;
+    }
+    hw[j] = pack_bf16x2(a, b);
+    const float ah = __builtin_bit_cast(float, hw[j] << 16);
+    const float bh = __builtin_bit_cast(float, hw[j] & 0xffff0000u);
+    lw[j] = pack_bf16x2(a - ah, b - bh);  // both differences are exact in fp32
   }
-  st.l += psum;
-  ph = __builtin_bit_cast(bf16x8, make_uint4(pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3]),
-                                             pack_bf16x2(hi[4], hi[5]), pack_bf16x2(hi[6], hi[7])));
-  pl = __builtin_bit_cast(bf16x8, make_uint4(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]),
-                                             pack_bf16x2(lo[4], lo[5]), pack_bf16x2(lo[6], lo[7])));
-}
-
-// V^T operands from the lane's 8 token rows (d-chunk lr of each): operand r
-// holds d = 8 lr + r of the 8 tokens.  An 8 x 8 transpose of 16-bit values
-// in 32 byte-selects: dword j of operand r pairs element r of rows 2 j and
-// 2 j + 1 (low halves for even r, high halves for odd r).
-__device__ inline void transpose_v(const uint4 (&vraw)[8], bf16x8 (&vf)[8]) {
-  uint32_t w[8][4];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    w[e][0] = vraw[e].x;
-    w[e][1] = vraw[e].y;
-    w[e][2] = vraw[e].z;
-    w[e][3] = vraw[e].w;
-  }
-#pragma unroll
-  for (int r = 0; r < 8; ++r) {
-    const uint32_t sel = (r & 1) ? 0x07060302u : 0x05040100u;
-    uint32_t o[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) o[j] = __builtin_amdgcn_perm(w[2 * j + 1][r >> 1], w[2 * j][r >> 1], sel);
-    vf[r] = __builtin_bit_cast(bf16x8, make_uint4(o[0], o[1], o[2], o[3]));
-  }
+  ph = __builtin_bit_cast(bf16x8, make_uint4(hw[0], hw[1], hw[2], hw[3]));
+  pl = __builtin_bit_cast(bf16x8, make_uint4(lw[0], lw[1], lw[2], lw[3]));
 }
 
 __device__ inline void pv_mfma(const bf16x8 (&vf)[8], const bf16x8& ph, const bf16x8& pl, RowState& st) {
@@ -205,10 +203,9 @@ __device__ inline void pv_mfma(const bf16x8 (&vf)[8], const bf16x8& ph, const bf
   }
 }
 
-// Partials: lane (lq, lr) holds O[row lr][32 lq .. 32 lq + 31] with
-// acc[r][e] at d = 32 lq + 8 e + r.
+// Partials: lane (q, lr) holds O[row lr][16 r + 4 q + e] in acc[r][e].
 __device__ inline void write_partial(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int row0, int R,
-                                     int lq, int lr, const RowState& st) {
+                                     int q, int lr, const RowState& st) {
   const float l = wave_sum_over_groups(st.l);
   const int r = row0 + lr;
   if (r >= R) return;
@@ -216,26 +213,23 @@ __device__ inline void write_partial(const DevPool& P, const AttnLaunch& A, cons
   const int pos = A.members[U.mem_off + r / g];
   const int h = U.kvh * g + r % g;
   const size_t idx = ((size_t)pos * P.Hq + h) * A.kmax + U.kidx;
-  f32x4* dst = reinterpret_cast<f32x4*>(A.part_acc + idx * kHeadDim + 32 * lq);
+  f32x4* dst = reinterpret_cast<f32x4*>(A.part_acc + idx * kHeadDim + 4 * q);
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int e = k >> 1, rb = 4 * (k & 1);
-    dst[k] = f32x4{st.acc[rb][e], st.acc[rb + 1][e], st.acc[rb + 2][e], st.acc[rb + 3][e]};
-  }
-  if (lq == 0) A.part_ml[idx] = float2{st.m, l};
+  for (int k = 0; k < 8; ++k) dst[4 * k] = st.acc[k];
+  if (q == 0) A.part_ml[idx] = float2{st.m, l};
 }
 
-// Q^T operand of the row block starting at row0: lane (lq, lr) holds row
+// Q^T operand of the row block starting at row0: lane (q, lr) holds row
 // row0 + lr in the given d layout (zeros past the unit's rows).
 __device__ inline void load_q(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int row0, int R, bool fp8_direct,
-                              int lq, int lr, bf16x8 (&qf)[4]) {
+                              int q, int lr, bf16x8 (&qf)[4]) {
   const int r = row0 + lr;
   if (r < R) {
     const int pos = A.members[U.mem_off + r / P.g];
     const int h = U.kvh * P.g + r % P.g;
     const uint16_t* qrow = A.q + ((size_t)pos * P.Hq + h) * kHeadDim;
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) qf[kb] = *reinterpret_cast<const bf16x8*>(qrow + q_offset(fp8_direct, kb, lq));
+    for (int kb = 0; kb < 4; ++kb) qf[kb] = *reinterpret_cast<const bf16x8*>(qrow + q_offset(fp8_direct, kb, q));
   } else {
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) qf[kb] = bf16x8{};
@@ -305,60 +299,83 @@ struct TileMeta {
   float ks0, ks1, vs0, vs1;
 };
 
+// Per-lane constants of one 32-token tile.  Lane (q, i): K operands read A
+// row i (block i / 8, token row k_phys order 8 h + i % 8 of half h), d-chunk
+// 4 kb + q; V^T operands read d = 16 r + lr, tokens 8 q .. 8 q + 7 (block
+// q / 2).
+struct LaneGeom {
+  int q, lr;
+  bool kb1, vb1;  // K / V operands of this lane come from the tile's second block
+};
+
+__device__ inline LaneGeom lane_geom(int lane) {
+  LaneGeom g;
+  g.q = lane >> 4;
+  g.lr = lane & 15;
+  g.kb1 = (lane & 8) != 0;
+  g.vb1 = (g.q & 2) != 0;
+  return g;
+}
+
+// Scale of the scores / of P for the lane's 8 tokens (all in one block).
+__device__ inline void lane_scales(const LaneGeom& g, const TileMeta& m, float sl, float& c, float& vsc) {
+  c = sl * (g.vb1 ? m.ks1 : m.ks0);
+  vsc = g.vb1 ? m.vs1 : m.vs0;
+}
+
 // ---------------------------------------------------------------- narrow --
 // Raw operands of one 32-token tile, loaded straight from HBM.  bf16: K 2
-// halves x 4 d-groups of 16 bytes, V 8 tokens x 16 bytes.  fp8: half the
-// bytes (K in k[.][0..1], V in the low 8 bytes of each v[e]).
-struct Tile {
+// halves x 4 d-groups of 16 bytes, V^T 8 operands of 16 bytes.  fp8: half
+// the bytes (a 16-byte K load feeds two operands).
+template <bool FP8>
+struct Tile;
+template <>
+struct Tile<false> {
   uint4 k[2][4];
   uint4 v[8];
 };
+template <>
+struct Tile<true> {
+  uint4 k[2][2];
+  uint2 v[8];
+};
 
 template <bool FP8>
-__device__ inline void load_k(const uint8_t* base0, const uint8_t* base1, int lq, int lr, Tile& t) {
-  constexpr int RB = FP8 ? kHeadDim : 2 * kHeadDim;  // bytes of one token row of one head
+__device__ inline void load_k(const uint8_t* kc0, const uint8_t* kc1, const LaneGeom& g, int lane, Tile<FP8>& t) {
+  const uint8_t* base = (g.kb1 ? kc1 : kc0) + g.q * 256 + (lane & 7) * 16;
 #pragma unroll
-  for (int hf = 0; hf < 2; ++hf) {  // lane (lq, lr) reads token lr of each half
-    const uint8_t* row = (hf ? base1 : base0) + lr * RB;
-    if constexpr (!FP8) {
+  for (int h = 0; h < 2; ++h) {
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) t.k[hf][kb] = *reinterpret_cast<const uint4*>(row + 64 * kb + 16 * lq);
-    } else {
-#pragma unroll
-      for (int i = 0; i < 2; ++i) t.k[hf][i] = *reinterpret_cast<const uint4*>(row + 64 * i + 16 * lq);
-    }
+    for (int j = 0; j < (FP8 ? 2 : 4); ++j) t.k[h][j] = *reinterpret_cast<const uint4*>(base + j * 1024 + h * 128);
   }
 }
 
 template <bool FP8>
-__device__ inline void load_v(const uint8_t* base0, const uint8_t* base1, int lq, int lr, Tile& t) {
-  constexpr int RB = FP8 ? kHeadDim : 2 * kHeadDim;
+__device__ inline void load_v(const uint8_t* vc0, const uint8_t* vc1, const LaneGeom& g, Tile<FP8>& t) {
+  if constexpr (!FP8) {
+    const uint8_t* base = (g.vb1 ? vc1 : vc0) + g.lr * 32 + (g.q & 1) * 16;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {  // lane (lq, lr) reads d-chunk lr of its 8 tokens
-    const int tok = tile_token(lq, e);
-    const uint8_t* row = (tok < 16 ? base0 : base1) + (tok & 15) * RB;
-    if constexpr (!FP8) {
-      t.v[e] = *reinterpret_cast<const uint4*>(row + 16 * lr);
-    } else {
-      const uint2 x = *reinterpret_cast<const uint2*>(row + 8 * lr);
-      t.v[e] = make_uint4(x.x, x.y, 0, 0);
-    }
+    for (int r = 0; r < 8; ++r) t.v[r] = *reinterpret_cast<const uint4*>(base + r * 512);
+  } else {
+    const uint8_t* base = (g.vb1 ? vc1 : vc0) + g.lr * 16 + (g.q & 1) * 8;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) t.v[r] = *reinterpret_cast<const uint2*>(base + r * 256);
   }
 }
 
 template <bool FP8>
-__device__ inline void qk_direct(const Tile& t, const bf16x8 (&qf)[4], f32x4& s0, f32x4& s1) {
+__device__ inline void qk_direct(const Tile<FP8>& t, const bf16x8 (&qf)[4], f32x4& s0, f32x4& s1) {
   bf16x8 kf[2][4];
 #pragma unroll
-  for (int hf = 0; hf < 2; ++hf) {
+  for (int h = 0; h < 2; ++h) {
     if constexpr (!FP8) {
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) kf[hf][kb] = __builtin_bit_cast(bf16x8, t.k[hf][kb]);
+      for (int kb = 0; kb < 4; ++kb) kf[h][kb] = __builtin_bit_cast(bf16x8, t.k[h][kb]);
     } else {
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        kf[hf][2 * i] = fp8x8_to_bf16(t.k[hf][i].x, t.k[hf][i].y);
-        kf[hf][2 * i + 1] = fp8x8_to_bf16(t.k[hf][i].z, t.k[hf][i].w);
+      for (int j = 0; j < 2; ++j) {
+        kf[h][2 * j] = __builtin_bit_cast(bf16x8, fp8x8_to_bf16(t.k[h][j].x, t.k[h][j].y));
+        kf[h][2 * j + 1] = __builtin_bit_cast(bf16x8, fp8x8_to_bf16(t.k[h][j].z, t.k[h][j].w));
       }
     }
   }
@@ -366,27 +383,33 @@ __device__ inline void qk_direct(const Tile& t, const bf16x8 (&qf)[4], f32x4& s0
 }
 
 template <bool FP8>
-__device__ inline void pv_direct(Tile& t, f32x4 s0, f32x4 s1, int t0, int ntok, int lq, const TileMeta& m,
-                                 float sl, RowState& st) {
+__device__ inline void pv_direct(Tile<FP8>& t, f32x4 s0, f32x4 s1, int t0, int ntok, const LaneGeom& g,
+                                 const TileMeta& m, float sl, RowState& st) {
+  const bool partial = t0 + 32 > ntok;
+  const int nv = min(max(ntok - t0 - 8 * g.q, 0), 8);
+  float c, vsc;
+  lane_scales(g, m, sl, c, vsc);
   bf16x8 ph, pl;
-  softmax_p(s0, s1, t0, ntok, lq, sl * m.ks0, sl * m.ks1, m.vs0, m.vs1, st, ph, pl);
-  // a token past the end reads as zero (its P is zero, but the slot may
-  // hold stale bits)
-  if (t0 + 32 > ntok) {
+  softmax_p<FP8>(s0, s1, partial, nv, c, vsc, st, ph, pl);
+  // A token past the end reads as zero (its P is zero, but the slot may
+  // hold stale bits).  Masked in place, so the common path copies nothing.
+  if (partial) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (t0 + tile_token(lq, e) >= ntok) t.v[e] = make_uint4(0, 0, 0, 0);
+    for (int r = 0; r < 8; ++r) {
+      if constexpr (!FP8)
+        t.v[r] = keep_first(t.v[r], nv);
+      else
+        t.v[r] = make_uint2(keep_bytes(t.v[r].x, nv), keep_bytes(t.v[r].y, nv - 4));
+    }
   }
-  uint4 vraw[8];
   bf16x8 vf[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
+  for (int r = 0; r < 8; ++r) {
     if constexpr (!FP8)
-      vraw[e] = t.v[e];
+      vf[r] = __builtin_bit_cast(bf16x8, t.v[r]);
     else
-      vraw[e] = __builtin_bit_cast(uint4, fp8x8_to_bf16(t.v[e].x, t.v[e].y));
+      vf[r] = __builtin_bit_cast(bf16x8, fp8x8_to_bf16(t.v[r].x, t.v[r].y));
   }
-  transpose_v(vraw, vf);
   pv_mfma(vf, ph, pl, st);
 }
 
@@ -401,26 +424,25 @@ __device__ void narrow_unit(const DevPool& P, const AttnLaunch& A, const AttnUni
   const int ntok = U.nblk >= 0 ? U.nblk * kBlock : P.seq_len[U.owner] - U.jb0 * kBlock;
   if (ntok <= 0) return;
   const int R = U.mem_cnt * P.g;  // <= 16
-  const int lq = lane >> 4, lr = lane & 15;
+  const LaneGeom g = lane_geom(lane);
   const int nblk = (ntok + kBlock - 1) / kBlock;
   const int ntile = (ntok + 31) / 32;
   BlockIds<FP8> ids(P, brow, nblk, lane);
   bf16x8 qf[4];
-  load_q(P, A, U, 0, R, FP8, lq, lr, qf);
+  load_q(P, A, U, 0, R, FP8, g.q, g.lr, qf);
   RowState st;
   row_init(st);
   const float sl = A.scale_log2;
 
-  auto fetch_k = [&](const TileMeta& m, Tile& t) {
-    load_k<FP8>(P.k_cache + head_off<FP8>(m.b0, P.Hkv, U.kvh), P.k_cache + head_off<FP8>(m.b1, P.Hkv, U.kvh), lq,
-                lr, t);
+  auto fetch_k = [&](const TileMeta& m, Tile<FP8>& t) {
+    load_k<FP8>(P.k_cache + head_off<FP8>(m.b0, P.Hkv, U.kvh), P.k_cache + head_off<FP8>(m.b1, P.Hkv, U.kvh), g,
+                lane, t);
   };
-  auto fetch_v = [&](const TileMeta& m, Tile& t) {
-    load_v<FP8>(P.v_cache + head_off<FP8>(m.b0, P.Hkv, U.kvh), P.v_cache + head_off<FP8>(m.b1, P.Hkv, U.kvh), lq,
-                lr, t);
+  auto fetch_v = [&](const TileMeta& m, Tile<FP8>& t) {
+    load_v<FP8>(P.v_cache + head_off<FP8>(m.b0, P.Hkv, U.kvh), P.v_cache + head_off<FP8>(m.b1, P.Hkv, U.kvh), g, t);
   };
   auto meta = [&](int i, TileMeta& m) { ids.tile(i, m.b0, m.b1, m.ks0, m.ks1, m.vs0, m.vs1); };
-  Tile ta, tb;
+  Tile<FP8> ta, tb;
   TileMeta ma{}, mb{}, na{}, nb{};  // current and next (tile + 2) metadata of buffers A and B
   meta(0, ma);
   fetch_k(ma, ta);
@@ -436,7 +458,7 @@ __device__ void narrow_unit(const DevPool& P, const AttnLaunch& A, const AttnUni
     meta(2, na);
     fetch_k(na, ta);
   }
-  auto step = [&](int i, Tile& t, TileMeta& m, TileMeta& n, Tile& to, TileMeta& no) {
+  auto step = [&](int i, Tile<FP8>& t, TileMeta& m, TileMeta& n, Tile<FP8>& to, TileMeta& no) {
     const f32x4 r0 = s0, r1 = s1;
     if (i + 1 < ntile) {
       qk_direct<FP8>(to, qf, s0, s1);
@@ -445,7 +467,7 @@ __device__ void narrow_unit(const DevPool& P, const AttnLaunch& A, const AttnUni
         fetch_k(no, to);
       }
     }
-    pv_direct<FP8>(t, r0, r1, 32 * i, ntok, lq, m, sl, st);
+    pv_direct<FP8>(t, r0, r1, 32 * i, ntok, g, m, sl, st);
     if (i + 2 < ntile) {
       fetch_v(n, t);
       m = n;
@@ -455,58 +477,67 @@ __device__ void narrow_unit(const DevPool& P, const AttnLaunch& A, const AttnUni
     step(i, ta, ma, na, tb, nb);
     if (i + 1 < ntile) step(i + 1, tb, mb, nb, ta, na);
   }
-  write_partial(P, A, U, 0, R, lq, lr, st);
+  write_partial(P, A, U, 0, R, g.q, g.lr, st);
 }
 
 // ----------------------------------------------------------- cooperative --
 // Staging registers of one 32-token tile: each of the 256 threads moves two
 // 16-byte chunks of K and two of V (bf16), or one of each (fp8).
+template <bool FP8>
 struct Stage {
-  uint4 k[2], v[2];
+  uint4 k[FP8 ? 1 : 2], v[FP8 ? 1 : 2];
 };
 
 template <bool FP8>
-__device__ inline void stage_load(const DevPool& P, int kvh, const TileMeta& m, int t0, int ntok, Stage& s) {
+__device__ inline void stage_load(const DevPool& P, int kvh, const TileMeta& m, Stage<FP8>& s) {
   const int t = threadIdx.x;
   if constexpr (!FP8) {
-    // thread t moves chunk t & 15 of token t >> 4 of each 16-token half
-    const int tok = t >> 4, ch = t & 15;
-    const size_t in_blk = (size_t)tok * kLdsRow + ch * 16;
-    const size_t o0 = head_off<false>(m.b0, P.Hkv, kvh) + in_blk;
-    const size_t o1 = head_off<false>(m.b1, P.Hkv, kvh) + in_blk;
-    const bool v0 = t0 + tok < ntok, v1 = t0 + 16 + tok < ntok;
-    s.k[0] = v0 ? *reinterpret_cast<const uint4*>(P.k_cache + o0) : make_uint4(0, 0, 0, 0);
-    s.v[0] = v0 ? *reinterpret_cast<const uint4*>(P.v_cache + o0) : make_uint4(0, 0, 0, 0);
-    s.k[1] = v1 ? *reinterpret_cast<const uint4*>(P.k_cache + o1) : make_uint4(0, 0, 0, 0);
-    s.v[1] = v1 ? *reinterpret_cast<const uint4*>(P.v_cache + o1) : make_uint4(0, 0, 0, 0);
+    // chunk t of each block's K and V tile (4096 bytes = 256 chunks)
+    const size_t o0 = head_off<false>(m.b0, P.Hkv, kvh) + t * 16;
+    const size_t o1 = head_off<false>(m.b1, P.Hkv, kvh) + t * 16;
+    s.k[0] = *reinterpret_cast<const uint4*>(P.k_cache + o0);
+    s.v[0] = *reinterpret_cast<const uint4*>(P.v_cache + o0);
+    s.k[1] = *reinterpret_cast<const uint4*>(P.k_cache + o1);
+    s.v[1] = *reinterpret_cast<const uint4*>(P.v_cache + o1);
   } else {
-    const int tok = t >> 3, ch8 = t & 7;  // 32 tokens x 8 chunks of 16 fp8 codes
-    if (t0 + tok < ntok) {
-      const size_t off = head_off<true>(tok < 16 ? m.b0 : m.b1, P.Hkv, kvh) + (tok & 15) * kHeadDim + ch8 * 16;
-      s.k[0] = *reinterpret_cast<const uint4*>(P.k_cache + off);
-      s.v[0] = *reinterpret_cast<const uint4*>(P.v_cache + off);
-    } else {
-      s.k[0] = s.v[0] = make_uint4(0, 0, 0, 0);
-    }
+    // chunk t % 128 of block t / 128 (2048-byte fp8 tiles)
+    const size_t o = head_off<true>(t < 128 ? m.b0 : m.b1, P.Hkv, kvh) + (t & 127) * 16;
+    s.k[0] = *reinterpret_cast<const uint4*>(P.k_cache + o);
+    s.v[0] = *reinterpret_cast<const uint4*>(P.v_cache + o);
   }
 }
 
+__device__ inline int lds_v(int blk, int d, int half) { return kLdsV + blk * kTileBytes + d * 32 + 16 * (half ^ ((d >> 3) & 1)); }
+
+// Writes the staged tile into an LDS stage as bf16; with `partial`, tokens
+// at or past nrem (tokens left in the chunk from this tile on) become zeros.
 template <bool FP8>
-__device__ inline void stage_store(uint8_t* kl, uint8_t* vl, const Stage& s) {
+__device__ inline void stage_store(uint8_t* stg, const Stage<FP8>& s, bool partial, int nrem) {
   const int t = threadIdx.x;
   if constexpr (!FP8) {
-    const int tok = t >> 4, ch = t & 15;
-    *reinterpret_cast<uint4*>(kl + lds_off(tok, ch)) = s.k[0];
-    *reinterpret_cast<uint4*>(vl + lds_off(tok, ch)) = s.v[0];
-    *reinterpret_cast<uint4*>(kl + lds_off(16 + tok, ch)) = s.k[1];
-    *reinterpret_cast<uint4*>(vl + lds_off(16 + tok, ch)) = s.v[1];
+    const int tok = k_phys(t & 15), d = t >> 1, half = t & 1;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      uint4 k = s.k[b], v = s.v[b];
+      if (partial) {
+        if (16 * b + tok >= nrem) k = make_uint4(0, 0, 0, 0);
+        v = keep_first(v, min(max(nrem - 16 * b - 8 * half, 0), 8));
+      }
+      *reinterpret_cast<uint4*>(stg + (b ? kLdsK1 : 0) + t * 16) = k;
+      *reinterpret_cast<uint4*>(stg + lds_v(b, d, half)) = v;
+    }
   } else {
-    const int tok = t >> 3, ch8 = t & 7;
-    const uint4 k0 = s.k[0], v0 = s.v[0];
-    *reinterpret_cast<bf16x8*>(kl + lds_off(tok, 2 * ch8)) = fp8x8_to_bf16(k0.x, k0.y);
-    *reinterpret_cast<bf16x8*>(kl + lds_off(tok, 2 * ch8 + 1)) = fp8x8_to_bf16(k0.z, k0.w);
-    *reinterpret_cast<bf16x8*>(vl + lds_off(tok, 2 * ch8)) = fp8x8_to_bf16(v0.x, v0.y);
-    *reinterpret_cast<bf16x8*>(vl + lds_off(tok, 2 * ch8 + 1)) = fp8x8_to_bf16(v0.z, v0.w);
+    const int b = t >> 7, ci = t & 127, c16 = ci >> 4, phys = ci & 15;
+    uint4 k = s.k[0], v = s.v[0];
+    if (partial) {
+      if (16 * b + k_phys(phys) >= nrem) k = make_uint4(0, 0, 0, 0);
+      v = keep_first16(v, nrem - 16 * b);
+    }
+    uint8_t* kb = stg + (b ? kLdsK1 : 0);
+    *reinterpret_cast<uint4*>(kb + ((2 * c16) * 16 + phys) * 16) = fp8x8_to_bf16(k.x, k.y);
+    *reinterpret_cast<uint4*>(kb + ((2 * c16 + 1) * 16 + phys) * 16) = fp8x8_to_bf16(k.z, k.w);
+    *reinterpret_cast<uint4*>(stg + lds_v(b, ci, 0)) = fp8x8_to_bf16(v.x, v.y);
+    *reinterpret_cast<uint4*>(stg + lds_v(b, ci, 1)) = fp8x8_to_bf16(v.z, v.w);
   }
 }
 
@@ -514,65 +545,71 @@ __device__ inline void stage_store(uint8_t* kl, uint8_t* vl, const Stage& s) {
 // Every wave takes part in every barrier.
 template <bool FP8>
 __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int wave, int lane,
-                          uint8_t (&lds)[2][2][32 * kLdsRow]) {
+                          uint8_t* lds) {
   const int32_t* brow = P.table + (size_t)U.owner * P.max_blocks + U.jb0;
   const int ntok = U.nblk >= 0 ? U.nblk * kBlock : P.seq_len[U.owner] - U.jb0 * kBlock;
   if (ntok <= 0) return;  // uniform over the workgroup
   const int R = U.mem_cnt * P.g;  // <= 64
-  const int lq = lane >> 4, lr = lane & 15;
+  const LaneGeom g = lane_geom(lane);
   const int nblk = (ntok + kBlock - 1) / kBlock;
   const int ntile = (ntok + 31) / 32;
   const int row0 = 16 * wave;
   const bool active = row0 < R;
   BlockIds<FP8> ids(P, brow, nblk, lane);
   bf16x8 qf[4];
-  load_q(P, A, U, row0, R, false, lq, lr, qf);
+  load_q(P, A, U, row0, R, false, g.q, g.lr, qf);
   RowState st;
   row_init(st);
   const float sl = A.scale_log2;
+  const int koff = (g.kb1 ? kLdsK1 : 0) + g.q * 256 + (lane & 7) * 16;
+  const int voff = lds_v(g.vb1 ? 1 : 0, g.lr, g.q & 1);
+
+  auto compute = [&](const uint8_t* stg, int i, const TileMeta& m) {
+    f32x4 s0, s1;
+    {
+      bf16x8 kf[2][4];
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) kf[h][kb] = *reinterpret_cast<const bf16x8*>(stg + koff + kb * 1024 + h * 128);
+      qk_mfma(kf, qf, s0, s1);
+    }
+    const int t0 = 32 * i;
+    float c, vsc;
+    lane_scales(g, m, sl, c, vsc);
+    bf16x8 ph, pl;
+    softmax_p<FP8>(s0, s1, t0 + 32 > ntok, min(max(ntok - t0 - 8 * g.q, 0), 8), c, vsc, st, ph, pl);
+    bf16x8 vf[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) vf[r] = *reinterpret_cast<const bf16x8*>(stg + voff + r * 512);
+    pv_mfma(vf, ph, pl, st);
+  };
 
   TileMeta m{}, mn{};
   ids.tile(0, m.b0, m.b1, m.ks0, m.ks1, m.vs0, m.vs1);
-  Stage stg;
-  stage_load<FP8>(P, U.kvh, m, 0, ntok, stg);
-  stage_store<FP8>(lds[0][0], lds[0][1], stg);
+  Stage<FP8> sg;
+  stage_load<FP8>(P, U.kvh, m, sg);
+  stage_store<FP8>(lds, sg, 32 > ntok, ntok);
   __syncthreads();
-  for (int i = 0; i < ntile; ++i) {
-    const int buf = i & 1;
+  auto step = [&](int i, const uint8_t* cur, uint8_t* nxt) {
     const bool more = i + 1 < ntile;
     if (more) {
       ids.tile(i + 1, mn.b0, mn.b1, mn.ks0, mn.ks1, mn.vs0, mn.vs1);
-      stage_load<FP8>(P, U.kvh, mn, 32 * (i + 1), ntok, stg);
+      stage_load<FP8>(P, U.kvh, mn, sg);
     }
-    if (active) {
-      const uint8_t* kl = lds[buf][0];
-      const uint8_t* vl = lds[buf][1];
-      f32x4 s0, s1;
-      {
-        bf16x8 kf[2][4];
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-          for (int kb = 0; kb < 4; ++kb)
-            kf[hf][kb] = *reinterpret_cast<const bf16x8*>(kl + lds_off(16 * hf + lr, 4 * kb + lq));
-        qk_mfma(kf, qf, s0, s1);
-      }
-      bf16x8 ph, pl;
-      softmax_p(s0, s1, 32 * i, ntok, lq, sl * m.ks0, sl * m.ks1, m.vs0, m.vs1, st, ph, pl);
-      uint4 vraw[8];
-      bf16x8 vf[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) vraw[e] = *reinterpret_cast<const uint4*>(vl + lds_off(tile_token(lq, e), lr));
-      transpose_v(vraw, vf);
-      pv_mfma(vf, ph, pl, st);
-    }
+    if (active) compute(cur, i, m);
     if (more) {
-      stage_store<FP8>(lds[buf ^ 1][0], lds[buf ^ 1][1], stg);
+      const int t1 = 32 * (i + 1);
+      stage_store<FP8>(nxt, sg, t1 + 32 > ntok, ntok - t1);
       m = mn;
     }
     __syncthreads();
+  };
+  for (int i = 0; i < ntile; i += 2) {
+    step(i, lds, lds + kStage);
+    if (i + 1 < ntile) step(i + 1, lds + kStage, lds);
   }
-  if (active) write_partial(P, A, U, row0, R, lq, lr, st);
+  if (active) write_partial(P, A, U, row0, R, g.q, g.lr, st);
 }
 
 // Workgroups are dispatched round-robin over the 8 XCDs, so workgroup bid
@@ -582,7 +619,7 @@ __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit&
 // narrow (HBM-bound) slots are interleaved so both kinds share every CU.
 template <bool FP8>
 __global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(DevPool P, AttnLaunch A) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2][2][32 * kLdsRow];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kStage];
   const int x = blockIdx.x & 7, slot = blockIdx.x >> 3;
   const int base = A.xcd_off[x] + 4 * slot, end = A.xcd_off[x + 1];
   if (base >= end) return;  // uniform over the workgroup

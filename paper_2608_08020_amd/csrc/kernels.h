@@ -13,6 +13,15 @@ constexpr int kHeadDim = 128;  // head dimension the kernels implement
 constexpr int kRowsPerUnit = 16;  // attention rows (trace x q-head) of one unit (one wavefront)
 constexpr int kUnitsPerWG = 4;
 
+// Layout of one (block, KV head) tile of 16 tokens x 128 d in the caches,
+// chosen so that every matrix-core operand of the attention kernel is one
+// 16-byte load per lane:
+//  K: [d / C][k_phys(token)][C], C = 16 / element bytes (16-byte d-chunks;
+//     within a chunk the token rows are stored with bits 2 and 3 of the
+//     token index swapped).
+//  V: [d][token] (transposed).
+__host__ __device__ inline int k_phys(int t) { return (t & 3) | ((t >> 1) & 4) | ((t << 1) & 8); }
+
 // One attention work entry: a chunk of a run of blocks that the same member
 // traces share, for one KV head, and either one block of <= 16 rows (a
 // narrow unit, one wavefront) or up to 64 rows (a cooperative item, one

@@ -42,8 +42,11 @@ def test_workspace_size_validates_descriptions():
         d2 = gambit.PoolDesc.from_buffer_copy(d)
         setattr(d2, field, bad)
         assert gambit.workspace_size(d2) == 0, field
-    # more partial slots, more workspace
+    # fewer partial slots, less workspace
     d3 = gambit.PoolDesc.from_buffer_copy(d)
-    d3.max_splits = 128
-    assert gambit.workspace_size(d3) > ok
+    d3.max_splits = 16
+    assert 0 < gambit.workspace_size(d3) < ok
+    # the merge reads a row's partials one per lane: at most 64
+    d3.max_splits = 65
+    assert gambit.workspace_size(d3) == 0
     assert gambit.lib().gambit_status_str(-2).decode() == "out of KV blocks"
