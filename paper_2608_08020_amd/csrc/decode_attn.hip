@@ -49,8 +49,9 @@ constexpr int kThreads = 256;                      // four waves
 constexpr int kTileBytes = kBlock * kHeadDim * 2;  // one bf16 (block, head) tile
 // LDS stage of one 32-token tile, always bf16: K of the two blocks (the
 // second shifted by 128 bytes, so the two 128-byte halves of a K read fall
-// in different banks), then V^T of the two blocks, whose 16-byte halves of
-// a d row are swapped when bit 3 of d is set (conflict-free V reads).
+// in different banks), then V^T of the two blocks stored as [token half
+// (8 tokens)][d][16 bytes], so the lanes of a V read, which take 16
+// consecutive d of one half, read contiguous bytes (no bank conflicts).
 constexpr int kLdsK1 = kTileBytes + 128;
 constexpr int kLdsV = kLdsK1 + kTileBytes;
 constexpr int kStage = kLdsV + 2 * kTileBytes;
@@ -237,9 +238,11 @@ __device__ inline void load_q(const DevPool& P, const AttnLaunch& A, const AttnU
 }
 
 // The unit's block ids (and fp8 scales) 64 at a time, one per lane, read
-// back with readlane, so no tile waits on a table load.  Entries outside
-// the pool are never dereferenced: they become block 0 and the device error
-// word records them.
+// back with readlane.  Window w + 1 is fetched when the tiles enter window
+// w, so a tile never waits on a table load.  Entries outside the pool are
+// never dereferenced: they become block 0 and the device error word records
+// them (bf16 checks the id when a tile takes it; fp8 when the window is
+// fetched, before its scales are read).
 template <bool FP8>
 struct BlockIds {
   const DevPool& P;
@@ -253,43 +256,49 @@ struct BlockIds {
     fetch(0, cur_id, cur_ks, cur_vs);
     fetch(1, nxt_id, nxt_ks, nxt_vs);
   }
+  // Lanes past the unit's last block re-read its last entry (never used);
+  // the unconditional load lets the id land in place without a copy.
   __device__ void fetch(int w, int& id, float& ks, float& vs) {
-    id = 0;
+    id = brow[min(64 * w + lane, nblk - 1)];
     ks = vs = 1.f;
-    const int j = 64 * w + lane;
-    if (j < nblk) {
-      id = brow[j];
+    if constexpr (FP8) {
       if ((unsigned)id >= (unsigned)P.num_blocks) {
         atomicOr(P.err, kErrBadBlock);
         id = 0;
       }
-      if constexpr (FP8) {
-        ks = P.kv_scale[2 * id];
-        vs = P.kv_scale[2 * id + 1];
-      }
+      ks = P.kv_scale[2 * id];
+      vs = P.kv_scale[2 * id + 1];
     }
   }
-  // ids and scales of tile i (logical blocks 2 i and 2 i + 1; a missing
-  // second block aliases the first, its tokens are masked).  Tiles are
-  // visited in increasing order.
+  __device__ int checked(int b) {
+    if constexpr (!FP8) {
+      if ((unsigned)b >= (unsigned)P.num_blocks) {
+        if (lane == 0) atomicOr(P.err, kErrBadBlock);
+        b = 0;
+      }
+    }
+    return b;
+  }
+  // ids and scales of tile i (logical blocks 2 i and 2 i + 1, both in one
+  // window; a missing second block aliases the first, its tokens are
+  // masked).  Tiles are visited in increasing order.
   __device__ void tile(int i, int& b0, int& b1, float& ks0, float& ks1, float& vs0, float& vs1) {
     const int j0 = 2 * i, j1 = 2 * i + 1 < nblk ? 2 * i + 1 : 2 * i;
-    if ((j1 >> 6) > win + 1) {
+    if ((j0 >> 6) > win) {
       cur_id = nxt_id;
       cur_ks = nxt_ks;
       cur_vs = nxt_vs;
       ++win;
       fetch(win + 1, nxt_id, nxt_ks, nxt_vs);
     }
-    const bool c0 = (j0 >> 6) == win, c1 = (j1 >> 6) == win;
-    b0 = __builtin_amdgcn_readlane(c0 ? cur_id : nxt_id, j0 & 63);
-    b1 = __builtin_amdgcn_readlane(c1 ? cur_id : nxt_id, j1 & 63);
+    b0 = checked(__builtin_amdgcn_readlane(cur_id, j0 & 63));
+    b1 = checked(__builtin_amdgcn_readlane(cur_id, j1 & 63));
     ks0 = ks1 = vs0 = vs1 = 1.f;
     if constexpr (FP8) {
-      ks0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c0 ? cur_ks : nxt_ks), j0 & 63));
-      vs0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c0 ? cur_vs : nxt_vs), j0 & 63));
-      ks1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c1 ? cur_ks : nxt_ks), j1 & 63));
-      vs1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c1 ? cur_vs : nxt_vs), j1 & 63));
+      ks0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, cur_ks), j0 & 63));
+      vs0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, cur_vs), j0 & 63));
+      ks1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, cur_ks), j1 & 63));
+      vs1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, cur_vs), j1 & 63));
     }
   }
 };
@@ -507,7 +516,66 @@ __device__ inline void stage_load(const DevPool& P, int kvh, const TileMeta& m, 
   }
 }
 
-__device__ inline int lds_v(int blk, int d, int half) { return kLdsV + blk * kTileBytes + d * 32 + 16 * (half ^ ((d >> 3) & 1)); }
+__device__ inline int lds_v(int blk, int d, int half) { return kLdsV + blk * kTileBytes + half * 2048 + d * 16; }
+
+// bf16 tiles reach LDS by direct global->LDS loads (no registers): a ring of
+// kRing stages with kAhead tiles in flight, so a workgroup waits for a
+// tile's L2/HBM round trip only once per kAhead tiles.
+constexpr int kRing = 4;
+constexpr int kAhead = 3;
+constexpr int kDmaPerTile = 4;  // 16-byte loads per thread per tile
+
+// Direct global->LDS loads: 16 (or 4) bytes per lane into LDS at l + 16
+// (4) x lane, l wave-uniform.  Written as inline assembly so the compiler
+// does not track them: it would otherwise wait for every one in flight
+// before any LDS read.  Completion is waited for explicitly (wait_tiles);
+// waits the compiler derives for other loads stay correct (untracked loads
+// only make them wait longer).
+__device__ inline uint32_t lds_addr(const void* l) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)l;
+}
+
+// M0 carries the LDS address; it is saved and restored around the load, so
+// the compiler's view of M0 never changes.
+__device__ inline void dma16(const void* g, uint8_t* l) {
+  uint32_t save;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_nop 0\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(save)
+      : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds_addr(l)))
+      : "memory");
+}
+
+__device__ inline void dma4(const void* g, void* l) {
+  uint32_t save;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %1, off\n\ts_nop 0\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(save)
+      : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds_addr(l)))
+      : "memory");
+}
+
+constexpr int kIdsBytes = 2 * 64 * 4;  // two windows of 64 block ids
+
+// Waits until at most `later` tiles' direct loads of this wave are still in
+// flight (loads retire in issue order).
+__device__ inline void wait_tiles(int later) {
+  // s_waitcnt immediate: vmcnt in bits 3:0, expcnt 6:4 and lgkmcnt 11:8 at
+  // their maxima (no wait).
+  if (later >= 2)
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (2 * kDmaPerTile));
+  else if (later == 1)
+    __builtin_amdgcn_s_waitcnt(0x0F70 | kDmaPerTile);
+  else
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+}
+
+// Workgroup barrier that keeps the compiler from moving memory accesses
+// across it but adds no wait for outstanding loads (a fenced barrier would
+// wait for every in-flight direct load, emptying the ring).
+__device__ inline void barrier_no_fence() { asm volatile("s_barrier" ::: "memory"); }
 
 // Writes the staged tile into an LDS stage as bf16; with `partial`, tokens
 // at or past nrem (tokens left in the chunk from this tile on) become zeros.
@@ -541,75 +609,170 @@ __device__ inline void stage_store(uint8_t* stg, const Stage<FP8>& s, bool parti
   }
 }
 
-// One workgroup, one chunk, up to 4 row blocks: wave w owns row block w.
-// Every wave takes part in every barrier.
-template <bool FP8>
+// One workgroup, one chunk, up to 4 x RB row blocks: wave w owns row
+// blocks RB w .. RB w + RB - 1, so each K/V operand a wave reads from LDS
+// feeds RB row blocks (and RB independent chains of products overlap in
+// the wave).  Every wave takes part in every barrier.
+template <bool FP8, int RB>
 __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int wave, int lane,
                           uint8_t* lds) {
   const int32_t* brow = P.table + (size_t)U.owner * P.max_blocks + U.jb0;
   const int ntok = U.nblk >= 0 ? U.nblk * kBlock : P.seq_len[U.owner] - U.jb0 * kBlock;
   if (ntok <= 0) return;  // uniform over the workgroup
-  const int R = U.mem_cnt * P.g;  // <= 64
+  const int R = U.mem_cnt * P.g;  // <= 64 RB
   const LaneGeom g = lane_geom(lane);
   const int nblk = (ntok + kBlock - 1) / kBlock;
   const int ntile = (ntok + 31) / 32;
-  const int row0 = 16 * wave;
+  const int row0 = 16 * RB * wave;
   const bool active = row0 < R;
-  BlockIds<FP8> ids(P, brow, nblk, lane);
-  bf16x8 qf[4];
-  load_q(P, A, U, row0, R, false, g.q, g.lr, qf);
-  RowState st;
-  row_init(st);
+  bf16x8 qf[RB][4];
+  RowState st[RB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) {
+    load_q(P, A, U, row0 + 16 * r, R, false, g.q, g.lr, qf[r]);
+    row_init(st[r]);
+  }
   const float sl = A.scale_log2;
   const int koff = (g.kb1 ? kLdsK1 : 0) + g.q * 256 + (lane & 7) * 16;
   const int voff = lds_v(g.vb1 ? 1 : 0, g.lr, g.q & 1);
 
-  auto compute = [&](const uint8_t* stg, int i, const TileMeta& m) {
-    f32x4 s0, s1;
-    {
-      bf16x8 kf[2][4];
+  // Scores of one tile for every row block (K from the stage holding it).
+  auto qk = [&](const uint8_t* stg, f32x4 (&s0)[RB], f32x4 (&s1)[RB]) {
+    bf16x8 kf[2][4];
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) kf[h][kb] = *reinterpret_cast<const bf16x8*>(stg + koff + kb * 1024 + h * 128);
-      qk_mfma(kf, qf, s0, s1);
-    }
+      for (int kb = 0; kb < 4; ++kb) kf[h][kb] = *reinterpret_cast<const bf16x8*>(stg + koff + kb * 1024 + h * 128);
+#pragma unroll
+    for (int r = 0; r < RB; ++r) qk_mfma(kf, qf[r], s0[r], s1[r]);
+  };
+  // Softmax and P.V of tile i from its scores.  mask_v: zero V of tokens
+  // past the end (the stage holds stale bits there).
+  auto pv = [&](const uint8_t* stg, int i, const TileMeta& m, bool mask_v, const f32x4 (&s0)[RB],
+                const f32x4 (&s1)[RB]) {
     const int t0 = 32 * i;
+    const bool partial = t0 + 32 > ntok;
+    const int nv = min(max(ntok - t0 - 8 * g.q, 0), 8);
+    uint4 vr[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) vr[r] = *reinterpret_cast<const uint4*>(stg + voff + r * 256);
     float c, vsc;
     lane_scales(g, m, sl, c, vsc);
-    bf16x8 ph, pl;
-    softmax_p<FP8>(s0, s1, t0 + 32 > ntok, min(max(ntok - t0 - 8 * g.q, 0), 8), c, vsc, st, ph, pl);
+    bf16x8 ph[RB], pl[RB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) softmax_p<FP8>(s0[r], s1[r], partial, nv, c, vsc, st[r], ph[r], pl[r]);
+    if (mask_v && partial) {
+#pragma unroll
+      for (int r = 0; r < 8; ++r) vr[r] = keep_first(vr[r], nv);
+    }
     bf16x8 vf[8];
 #pragma unroll
-    for (int r = 0; r < 8; ++r) vf[r] = *reinterpret_cast<const bf16x8*>(stg + voff + r * 512);
-    pv_mfma(vf, ph, pl, st);
+    for (int r = 0; r < 8; ++r) vf[r] = __builtin_bit_cast(bf16x8, vr[r]);
+#pragma unroll
+    for (int r = 0; r < RB; ++r) pv_mfma(vf, ph[r], pl[r], st[r]);
+  };
+  auto compute = [&](const uint8_t* stg, int i, const TileMeta& m, bool mask_v) {
+    f32x4 s0[RB], s1[RB];
+    qk(stg, s0, s1);
+    pv(stg, i, m, mask_v, s0, s1);
   };
 
-  TileMeta m{}, mn{};
-  ids.tile(0, m.b0, m.b1, m.ks0, m.ks1, m.vs0, m.vs1);
-  Stage<FP8> sg;
-  stage_load<FP8>(P, U.kvh, m, sg);
-  stage_store<FP8>(lds, sg, 32 > ntok, ntok);
-  __syncthreads();
-  auto step = [&](int i, const uint8_t* cur, uint8_t* nxt) {
-    const bool more = i + 1 < ntile;
-    if (more) {
-      ids.tile(i + 1, mn.b0, mn.b1, mn.ks0, mn.ks1, mn.vs0, mn.vs1);
-      stage_load<FP8>(P, U.kvh, mn, sg);
+  if constexpr (!FP8) {
+    // Lane t of wave w loads a 16-byte chunk of each 4 KB region of a tile
+    // into LDS slot t: K chunk t, and the V^T chunk (d = t % 128, token half
+    // t / 128) that the LDS layout puts in slot t.
+    const int t = threadIdx.x;
+    const int kofs = t * 16;
+    const int vofs = (t & 127) * 32 + 16 * (t >> 7);
+    const int wb = wave * 1024;
+    // Block ids live in LDS, two windows of 64: wave 0 loads window w + 1
+    // when the tiles it issues enter window w.  Its completion is covered
+    // by the per-tile waits (it retires before the tile loads issued after
+    // it), and the tiles of window w - 1, whose slot it reuses, were issued
+    // before the barrier.
+    int32_t* idw = reinterpret_cast<int32_t*>(lds + kRing * kStage);
+    auto fetch_ids = [&](int w) {
+      if (wave == 0) dma4(brow + min(64 * w + lane, nblk - 1), idw + 64 * (w & 1));
+    };
+    auto issue = [&](int i) {
+      const int j0 = 2 * i;
+      if ((j0 & 63) == 0 && j0 > 0) fetch_ids((j0 >> 6) + 1);
+      const int2 pr = *reinterpret_cast<const int2*>(idw + 64 * ((j0 >> 6) & 1) + (j0 & 63));
+      int b0 = __builtin_amdgcn_readfirstlane(pr.x);
+      int b1 = j0 + 1 < nblk ? __builtin_amdgcn_readfirstlane(pr.y) : b0;
+      if ((unsigned)b0 >= (unsigned)P.num_blocks || (unsigned)b1 >= (unsigned)P.num_blocks) {
+        if (t == 0) atomicOr(P.err, kErrBadBlock);
+        b0 = (unsigned)b0 < (unsigned)P.num_blocks ? b0 : 0;
+        b1 = (unsigned)b1 < (unsigned)P.num_blocks ? b1 : 0;
+      }
+      uint8_t* stg = lds + (i % kRing) * kStage + wb;
+      const size_t o0 = head_off<false>(b0, P.Hkv, U.kvh), o1 = head_off<false>(b1, P.Hkv, U.kvh);
+      dma16(P.k_cache + o0 + kofs, stg);
+      dma16(P.k_cache + o1 + kofs, stg + kLdsK1);
+      dma16(P.v_cache + o0 + vofs, stg + kLdsV);
+      dma16(P.v_cache + o1 + vofs, stg + kLdsV + kTileBytes);
+    };
+    const TileMeta unit{0, 0, 1.f, 1.f, 1.f, 1.f};  // bf16: no block scales
+    fetch_ids(0);
+    if (nblk > 64) fetch_ids(1);
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // Q operands and the first id windows are in
+    barrier_no_fence();
+    for (int i = 0; i < kAhead && i < ntile; ++i) issue(i);
+    wait_tiles(min(kAhead - 1, ntile - 1));  // tile 0 is in LDS
+    barrier_no_fence();
+    f32x4 s0[RB], s1[RB];
+    if (active) qk(lds, s0, s1);
+    // Iteration i issues the scores of tile i + 1 before the softmax and
+    // P.V of tile i, so the matrix cores work while the vector ALUs do the
+    // softmax.  Tile i + 1 must be in LDS first; stage (i - 1) % kRing, read
+    // for the last time in iteration i - 1, takes tile i + kAhead.
+    for (int i = 0; i < ntile; ++i) {
+      const bool more = i + 1 < ntile;
+      wait_tiles(i + 2 < ntile ? 1 : 0);  // this wave's loads of tile i + 1 are in LDS
+      barrier_no_fence();                  // ... and every wave's
+      if (i + kAhead < ntile) issue(i + kAhead);
+      if (active) {
+        f32x4 n0[RB], n1[RB];
+        if (more) qk(lds + ((i + 1) % kRing) * kStage, n0, n1);
+        pv(lds + (i % kRing) * kStage, i, unit, true, s0, s1);
+#pragma unroll
+        for (int r = 0; r < RB; ++r) {
+          s0[r] = n0[r];
+          s1[r] = n1[r];
+        }
+      }
     }
-    if (active) compute(cur, i, m);
-    if (more) {
-      const int t1 = 32 * (i + 1);
-      stage_store<FP8>(nxt, sg, t1 + 32 > ntok, ntok - t1);
-      m = mn;
-    }
+  } else {
+    BlockIds<FP8> ids(P, brow, nblk, lane);
+    TileMeta m{}, mn{};
+    ids.tile(0, m.b0, m.b1, m.ks0, m.ks1, m.vs0, m.vs1);
+    Stage<FP8> sg;
+    stage_load<FP8>(P, U.kvh, m, sg);
+    stage_store<FP8>(lds, sg, 32 > ntok, ntok);
     __syncthreads();
-  };
-  for (int i = 0; i < ntile; i += 2) {
-    step(i, lds, lds + kStage);
-    if (i + 1 < ntile) step(i + 1, lds + kStage, lds);
+    auto step = [&](int i, const uint8_t* cur, uint8_t* nxt) {
+      const bool more = i + 1 < ntile;
+      if (more) {
+        ids.tile(i + 1, mn.b0, mn.b1, mn.ks0, mn.ks1, mn.vs0, mn.vs1);
+        stage_load<FP8>(P, U.kvh, mn, sg);
+      }
+      if (active) compute(cur, i, m, false);
+      if (more) {
+        const int t1 = 32 * (i + 1);
+        stage_store<FP8>(nxt, sg, t1 + 32 > ntok, ntok - t1);
+        m = mn;
+      }
+      __syncthreads();
+    };
+    for (int i = 0; i < ntile; i += 2) {
+      step(i, lds, lds + kStage);
+      if (i + 1 < ntile) step(i + 1, lds + kStage, lds);
+    }
   }
-  if (active) write_partial(P, A, U, row0, R, g.q, g.lr, st);
+  if (active) {
+#pragma unroll
+    for (int r = 0; r < RB; ++r) write_partial(P, A, U, row0 + 16 * r, R, g.q, g.lr, st[r]);
+  }
 }
 
 // Workgroups are dispatched round-robin over the 8 XCDs, so workgroup bid
@@ -619,14 +782,18 @@ __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit&
 // narrow (HBM-bound) slots are interleaved so both kinds share every CU.
 template <bool FP8>
 __global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(DevPool P, AttnLaunch A) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kStage];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[FP8 ? 2 * kStage : kRing * kStage + kIdsBytes];
   const int x = blockIdx.x & 7, slot = blockIdx.x >> 3;
   const int base = A.xcd_off[x] + 4 * slot, end = A.xcd_off[x + 1];
   if (base >= end) return;  // uniform over the workgroup
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const AttnUnit U0 = A.units[base];
   if (U0.flags & kUnitCoop) {
-    if (U0.mem_cnt > 0) coop_unit<FP8>(P, A, U0, wave, lane, lds);
+    // up to 64 rows: one row block per wave; more: two
+    if (U0.mem_cnt * P.g > 4 * kRowsPerUnit)
+      coop_unit<FP8, 2>(P, A, U0, wave, lane, lds);
+    else if (U0.mem_cnt > 0)
+      coop_unit<FP8, 1>(P, A, U0, wave, lane, lds);
     return;
   }
   if (base + wave >= end) return;  // no barrier on the narrow path

@@ -331,7 +331,7 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
         for (int m0 = 0; m0 < mcnt; m0 += item_members) {
           const int mc = std::min(item_members, mcnt - m0);
           gr.coop.push_back(AttnUnit{ids[owner_pos], jb0, nblk, h, moff + m0, mc, kidx, gambit::kUnitCoop});
-          gr.cost += 6.0 * tok;
+          gr.cost += tok * (2.0 + 4.0 * mc * p->g / 64.0);  // staging + compute per row
         }
         groups.push_back(std::move(gr));
       }

@@ -39,7 +39,7 @@ struct AttnUnit {
 
 enum : int32_t { kUnitCoop = 1 };
 
-constexpr int kRowsPerCoop = 64;  // rows of one cooperative item (4 waves x 1 row block)
+constexpr int kRowsPerCoop = 128;  // rows of one cooperative item (4 waves x up to 2 row blocks)
 
 // Device view of a pool.
 struct DevPool {
