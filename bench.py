@@ -21,7 +21,6 @@ bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -33,7 +32,6 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0
 METRIC = "decode-attention trace-steps/sec + achieved HBM GB/s (% of MI355X peak)"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
-KERNEL_SRC = os.path.join(ROOT, "paper_2608_08020_amd", "csrc", "decode_attn.hip")
 
 
 def log(msg):
@@ -41,13 +39,13 @@ def log(msg):
 
 
 def kernel_sha() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    from paper_2608_08020_amd.profiling import source_sha
+    return source_sha()
 
 
 def measured_traffic(workload: str):
     """Per-launch HBM bytes from the committed rocprofv3 counter runs, if they
-    were taken on the current kernel source and this workload."""
+    were taken on the current kernel and planner sources and this workload."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)

@@ -344,7 +344,7 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
         const int c = p->cnt[row[j]];
         if (c == 1) {  // private run: through the trace's last block
           const int len = nb[pos] - j;
-          const int nch = std::max(1, cdiv(len, chunk_blocks));
+          const int nch = std::max(1, cdiv(len, 2 * chunk_blocks));
           for (int k = 0, jb = j; k < nch; ++k) {
             const int sz = len / nch + (k < len % nch ? 1 : 0);
             const bool last = k == nch - 1;
@@ -360,7 +360,7 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
         // a chunk is read by each of its row blocks, so wide runs take longer
         // chunks: fewer partials, the same bytes per row block
         const int nrb = cdiv(c * p->g, gambit::kRowsPerUnit);
-        const int nch = cdiv(len, chunk_blocks * std::min(nrb, 2));
+        const int nch = cdiv(len, chunk_blocks * (nrb == 1 ? 2 : std::min(nrb, 4)));
         const int b0 = row[j];
         for (int k = 0, jb = j; k < nch; ++k) {
           const int sz = len / nch + (k < len % nch ? 1 : 0);

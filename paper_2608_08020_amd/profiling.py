@@ -12,8 +12,8 @@
 * --calib-*: the same counters over hbm_calib.py, a plain copy of known
   size; counter / true bytes gives the scale applied to the attention counts.
 Writes the markdown summary and profiles/attn_traffic.json (per-launch HBM
-bytes keyed by the hash of the attention kernel source, which bench.py
-reports only while the source is unchanged).
+bytes keyed by the hash of the attention kernel and planner sources, which
+bench.py reports only while both are unchanged).
 """
 from __future__ import annotations
 
@@ -26,6 +26,16 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 KERNEL = "attn_units_kernel"
+# the attention kernel's traffic depends on its code and on the plan it runs
+TRAFFIC_SOURCES = ("decode_attn.hip", "gambit_pool.cpp")
+
+
+def source_sha() -> str:
+    h = hashlib.sha256()
+    for name in TRAFFIC_SOURCES:
+        with open(os.path.join(HERE, "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def _rows(path):
@@ -66,8 +76,7 @@ def main():
     wk, nw = _counter(a.write, KERNEL, "WRITE_SIZE", a.sampled)
     fetch_b = fk * 1024.0 * f_scale
     write_b = wk * 1024.0 * w_scale
-    with open(os.path.join(HERE, "csrc", "decode_attn.hip"), "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()[:16]
+    sha = source_sha()
     rec = {"workload": a.workload, "kernel_sha": sha, "bytes_per_launch": round(fetch_b + write_b),
            "fetch_bytes_per_launch": round(fetch_b), "write_bytes_per_launch": round(write_b),
            "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
@@ -93,7 +102,7 @@ def main():
               f"* total {(fetch_b + write_b) / 1e9:.3f} GB per launch"
               + (f" vs {a.alg_bytes / 1e9:.3f} GB algorithmic ({(fetch_b + write_b) / a.alg_bytes:.2f}x)"
                  if a.alg_bytes else ""),
-              f"* kernel source sha256[:16] = {sha}", ""]
+              f"* sha256[:16] of {' + '.join(TRAFFIC_SOURCES)} = {sha}", ""]
     with open(a.out, "w") as f:
         f.write("\n".join(lines))
     print("\n".join(lines))
