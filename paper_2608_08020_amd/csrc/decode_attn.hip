@@ -778,14 +778,45 @@ __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit&
 // Workgroups are dispatched round-robin over the 8 XCDs, so workgroup bid
 // runs on XCD bid % 8.  The plan lists every XCD's workgroup slots
 // contiguously, four entries per slot: a cooperative item (flagged in its
-// first entry) or four narrow units.  Cooperative (compute-bound) and
-// narrow (HBM-bound) slots are interleaved so both kinds share every CU.
+// first entry) or four narrow units, in the order they should start
+// (longest first).  Cooperative (compute-bound) and narrow (HBM-bound)
+// slots are interleaved so both kinds share every CU.  Workgroup j of an
+// XCD runs slot j, except in the XCD's last kTailSlots slots: those are
+// claimed at run time, from the front by the XCD's own workgroups and from
+// the back (the shortest slots) by workgroups of XCDs that have no work
+// left, so the XCDs finish together.  One atomic word per XCD holds both
+// claim counts (front in the low half), so front and back claims never
+// meet; there are at least as many workgroups as slots.
+
+__device__ inline int tail_start(const AttnLaunch& A, int x) {
+  return max((A.xcd_off[x + 1] - A.xcd_off[x]) / kUnitsPerWG - kTailSlots, 0);
+}
+
 template <bool FP8>
 __global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(DevPool P, AttnLaunch A) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[FP8 ? 2 * kStage : kRing * kStage + kIdsBytes];
-  const int x = blockIdx.x & 7, slot = blockIdx.x >> 3;
-  const int base = A.xcd_off[x] + 4 * slot, end = A.xcd_off[x + 1];
-  if (base >= end) return;  // uniform over the workgroup
+  __shared__ int claimed;
+  if (threadIdx.x == 0) {
+    const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+    int b = -1;
+    if (j < tail_start(A, x)) {
+      b = A.xcd_off[x] + kUnitsPerWG * j;
+    } else {
+      for (int k = 0; k < 8 && b < 0; ++k) {
+        const int y = (x + k) & 7;
+        const int s0 = tail_start(A, y);
+        const int m = (A.xcd_off[y + 1] - A.xcd_off[y]) / kUnitsPerWG - s0;
+        if (m <= 0) continue;
+        const unsigned old = atomicAdd(reinterpret_cast<unsigned*>(A.queues) + y, k == 0 ? 1u : 0x10000u);
+        const int f = (int)(old & 0xffffu), bk = (int)(old >> 16);
+        if (f + bk < m) b = A.xcd_off[y] + kUnitsPerWG * (s0 + (k == 0 ? f : m - 1 - bk));
+      }
+    }
+    claimed = b;
+  }
+  __syncthreads();
+  const int base = claimed;
+  if (base < 0) return;  // uniform over the workgroup
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const AttnUnit U0 = A.units[base];
   if (U0.flags & kUnitCoop) {
@@ -796,9 +827,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(DevPool P, Attn
       coop_unit<FP8, 1>(P, A, U0, wave, lane, lds);
     return;
   }
-  if (base + wave >= end) return;  // no barrier on the narrow path
-  const AttnUnit U = A.units[base + wave];
-  if (U.mem_cnt > 0) narrow_unit<FP8>(P, A, U, lane);
+  const AttnUnit U = A.units[base + wave];  // a narrow slot always has four entries
+  if (U.mem_cnt > 0) narrow_unit<FP8>(P, A, U, lane);  // no barrier on the narrow path
 }
 
 // Log-sum-exp merge of a row's partials.  One wave per (list position,
@@ -806,6 +836,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(DevPool P, Attn
 // maximum and the weighted sum, then every lane accumulates its two d values
 // over the partials with the weights broadcast from their lanes.
 __global__ __launch_bounds__(256) void merge_kernel(DevPool P, AttnLaunch A) {
+  if (blockIdx.x == 0 && threadIdx.x < 8) A.queues[threadIdx.x] = 0;  // for the next attention launch
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= A.n * P.Hq) return;
   const int lane = threadIdx.x & 63;

@@ -37,7 +37,7 @@ int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 // Workspace carve-up.  All offsets are kAlign-aligned.
 struct Layout {
-  size_t list, ids, req_trace, req_ntok, pairs, free_list, nk, ticket, err, scales, freebits,
+  size_t list, ids, req_trace, req_ntok, pairs, free_list, nk, ticket, queues, err, scales, freebits,
       alloc_list, units, members, part_ml, part_acc, total;
   int kmax, max_units, max_members, nwords;
 };
@@ -71,6 +71,7 @@ bool layout_of(const gambit_pool_desc* d, Layout* L) {
   L->free_list = take(4 * (size_t)T);
   L->nk = take(4 * (size_t)T);
   L->ticket = take(64);
+  L->queues = take(64);
   L->err = take(64);
   L->scales = take(8 * ((size_t)d->max_blocks_per_trace + 1));
   L->freebits = take(4 * (size_t)L->nwords);
@@ -114,6 +115,7 @@ struct gambit_pool {
   int xcd_off[9] = {0};
   int grid = 0;
   int n_units = 0;
+  bool queues_dirty = false;       // an attention launch was not followed by its merge
   int max_splits_used = 0;
   std::vector<int32_t> cnt, first, csr_off, csr_fill, csr;  // per-block planner scratch
   gambit_stats stats{};            // of plan_list, kept current by decode steps
@@ -405,7 +407,6 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
   // four times, flagged) or four narrow units.  The two kinds are interleaved
   // in proportion so compute-bound and HBM-bound workgroups share every CU.
   std::vector<AttnUnit> units;
-  int maxs = 0;
   const AttnUnit empty{0, 0, 0, 0, 0, 0, 0, 0};
   for (int x = 0; x < 8; ++x) {
     p->xcd_off[x] = (int)units.size();
@@ -428,10 +429,14 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
         ++ni;
       }
     }
-    maxs = std::max(maxs, (int)((units.size() - p->xcd_off[x]) / gambit::kUnitsPerWG));
   }
   p->xcd_off[8] = (int)units.size();
-  p->grid = 8 * maxs;
+  // one workgroup per slot, and at least as many per XCD as that XCD has
+  // slots outside its run-time claimed tail
+  int per_xcd = cdiv((int)units.size() / gambit::kUnitsPerWG, 8);
+  for (int x = 0; x < 8; ++x)
+    per_xcd = std::max(per_xcd, (p->xcd_off[x + 1] - p->xcd_off[x]) / gambit::kUnitsPerWG - gambit::kTailSlots);
+  p->grid = 8 * per_xcd;
   p->n_units = (int)units.size();
   if ((int)units.size() > p->L.max_units || (int)members.size() > p->L.max_members)
     return fail(p, GAMBIT_ERR_UNSUPPORTED, "plan exceeds workspace bounds");
@@ -544,6 +549,7 @@ gambit_status gambit_pool_create(const gambit_pool_desc* desc, void* stream, gam
   if (e == hipSuccess) e = hipEventRecord(p->stage_ev, S(stream));
   if (e == hipSuccess) e = hipEventRecord(p->plan_ev, S(stream));
   if (e == hipSuccess) e = hipMemsetAsync(p->ws + L.ticket, 0, 64, S(stream));
+  if (e == hipSuccess) e = hipMemsetAsync(p->ws + L.queues, 0, 64, S(stream));
   if (e == hipSuccess) e = gambit::launch_pool_init(D, S(stream));
   if (e != hipSuccess) {
     gambit_pool_destroy(p);
@@ -717,6 +723,7 @@ gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, 
   A.units = ws_ptr<AttnUnit>(p, p->L.units);
   std::memcpy(A.xcd_off, p->xcd_off, sizeof A.xcd_off);
   A.grid = p->grid;
+  A.queues = ws_ptr<int32_t>(p, p->L.queues);
   A.members = ws_ptr<int32_t>(p, p->L.members);
   A.nk = ws_ptr<int32_t>(p, p->L.nk);
   A.part_acc = ws_ptr<float>(p, p->L.part_acc);
@@ -726,6 +733,11 @@ gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, 
   A.scale_log2 = sm_scale * 1.4426950408889634f;
   A.out = out;
   A.out_f32 = out_dtype == GAMBIT_OUT_F32;
+  // The merge kernel leaves the slot counters at zero for the next launch;
+  // only after a launch that was not followed by its merge are they
+  // cleared here.
+  if (p->queues_dirty) HIP_TRY(p, hipMemsetAsync(A.queues, 0, 64, s), "slot counter reset");
+  p->queues_dirty = true;
   const bool timed = p->prof_on && p->prof_used + 2 <= (int)p->prof_ev.size();
   if (timed) HIP_TRY(p, hipEventRecord(p->prof_ev[p->prof_used], s), "profile event");
   HIP_TRY(p, gambit::launch_attention_units(p->dev, A, s), "attention");
@@ -734,6 +746,7 @@ gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, 
     p->prof_used += 2;
   }
   HIP_TRY(p, gambit::launch_attention_merge(p->dev, A, s), "attention merge");
+  p->queues_dirty = false;
   for (int i = 0; i < n; ++i) mirror_grow(p, ids[i], 1);
   p->stats.total_tokens += n;
   p->stats.unique_tokens += n;

@@ -40,6 +40,7 @@ struct AttnUnit {
 enum : int32_t { kUnitCoop = 1 };
 
 constexpr int kRowsPerCoop = 128;  // rows of one cooperative item (4 waves x up to 2 row blocks)
+constexpr int kTailSlots = 96;     // last workgroup slots of an XCD, claimed at run time
 
 // Device view of a pool.
 struct DevPool {
@@ -66,8 +67,10 @@ enum : int32_t {
 struct AttnLaunch {
   const uint16_t* q;        // [n][Hq][128] bf16
   const AttnUnit* units;    // workgroup slots of 4 entries, grouped by XCD
-  int32_t xcd_off[9];       // XCD x runs entries [xcd_off[x], xcd_off[x+1])
-  int32_t grid;             // 8 * (largest per-XCD slot count)
+  int32_t xcd_off[9];       // XCD x's workgroup slots: entries [xcd_off[x], xcd_off[x+1])
+  int32_t grid;             // one workgroup per slot, rounded up to a multiple of 8
+  int32_t* queues;          // [8] tail claims per XCD (front | back << 16); zero at launch,
+                            // reset by the merge kernel
   const int32_t* members;   // list positions
   const int32_t* nk;        // [n] partials per list position
   float* part_acc;          // [n][Hq][kmax][128]
