@@ -30,27 +30,37 @@ __global__ void pool_init_kernel(DevPool P) {
   if (i0 == 0) *P.err = 0;
 }
 
-// Exclusive scan of one int per thread across the workgroup (kAllocThreads).
+// Exclusive scan of one int per thread across the workgroup (kAllocThreads
+// = 16 waves): a shuffle scan inside each wave, then the wave totals.
 __device__ int wg_exclusive_scan(int v, int* total) {
-  __shared__ int s[kAllocThreads];
-  const int t = threadIdx.x;
-  s[t] = v;
-  __syncthreads();
-  for (int off = 1; off < kAllocThreads; off <<= 1) {
-    const int x = t >= off ? s[t - off] : 0;
-    __syncthreads();
-    s[t] += x;
-    __syncthreads();
+  __shared__ int wsum[kAllocThreads / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int x = __shfl_up(incl, off);
+    if (lane >= off) incl += x;
   }
-  const int incl = s[t];
-  *total = s[kAllocThreads - 1];
+  if (lane == 63) wsum[w] = incl;
   __syncthreads();
-  return incl - v;
+  int before = 0, all = 0;
+#pragma unroll
+  for (int k = 0; k < kAllocThreads / 64; ++k) {
+    const int s = wsum[k];
+    before += k < w ? s : 0;
+    all += s;
+  }
+  __syncthreads();  // wsum may be reused
+  *total = all;
+  return before + incl - v;
 }
 
 // One workgroup.  Request i extends trace req_trace[i] by its token count;
 // the blocks it needs are the next lowest free ids, in request order and
-// ascending logical index.
+// ascending logical index.  The free bitmap is read in coalesced passes of
+// one word per thread, only as far as the lowest `total` free blocks reach:
+// a counting pass first (so a short pool is left untouched), then the
+// assignment.
 __global__ __launch_bounds__(kAllocThreads) void alloc_kernel(DevPool P, const int32_t* req_trace,
                                                              const int32_t* req_ntok, int32_t uniform,
                                                              int32_t m, float new_scale) {
@@ -66,26 +76,38 @@ __global__ __launch_bounds__(kAllocThreads) void alloc_kernel(DevPool P, const i
   int total = 0;
   const int base = wg_exclusive_scan(need, &total);
   if (total > 0) {  // uniform across the workgroup
-    const int wpt = (P.nwords + kAllocThreads - 1) / kAllocThreads;
-    const int w0 = min(P.nwords, t * wpt), w1 = min(P.nwords, w0 + wpt);
-    int nfree = 0;
-    for (int w = w0; w < w1; ++w) nfree += __popc(P.freebits[w]);
-    int avail = 0;
-    int rank = wg_exclusive_scan(nfree, &avail);
-    if (avail < total) {  // the host mirror rules this out; leave the pool untouched
+    const int npass = (P.nwords + kAllocThreads - 1) / kAllocThreads;
+    int last = -1, found = 0;  // passes that hold the lowest `total` free blocks
+    for (int p = 0; p < npass && found < total; ++p) {
+      const int w = p * kAllocThreads + t;
+      int c = w < P.nwords ? __popc(P.freebits[w]) : 0, n = 0;
+      wg_exclusive_scan(c, &n);
+      found += n;
+      last = p;
+    }
+    if (found < total) {  // the host mirror rules this out; leave the pool untouched
       if (t == 0) atomicOr(P.err, kErrAllocShort);
       return;
     }
-    for (int w = w0; w < w1 && rank < total; ++w) {
-      uint32_t bits = P.freebits[w];
-      while (bits && rank < total) {
-        const int bit = __ffs(bits) - 1;
-        bits &= bits - 1;
-        P.alloc_list[rank++] = w * 32 + bit;
-        P.freebits[w] &= ~(1u << bit);
+    int acc = 0;
+    for (int p = 0; p <= last; ++p) {
+      const int w = p * kAllocThreads + t;
+      uint32_t bits = w < P.nwords ? P.freebits[w] : 0u;
+      int n = 0;
+      int rank = acc + wg_exclusive_scan(__popc(bits), &n);
+      if (rank < total && bits) {
+        uint32_t taken = 0;
+        while (bits && rank < total) {
+          const int bit = __ffs(bits) - 1;
+          bits &= bits - 1;
+          taken |= 1u << bit;
+          P.alloc_list[rank++] = w * 32 + bit;
+        }
+        P.freebits[w] &= ~taken;
       }
+      acc += n;
     }
-    __syncthreads();
+    __syncthreads();  // alloc_list is complete
   }
   int off = base;
   for (int i = r0; i < r1; ++i) {

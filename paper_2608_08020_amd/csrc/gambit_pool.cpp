@@ -344,9 +344,9 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
       int kidx = 0, j = 0;
       while (j < nb[pos]) {
         const int c = p->cnt[row[j]];
-        if (c == 1) {  // private run: through the trace's last block
+        if (c == 1) {  // private run: through the trace's last block, chunks of 4 chunk_blocks
           const int len = nb[pos] - j;
-          const int nch = std::max(1, cdiv(len, 2 * chunk_blocks));
+          const int nch = std::max(1, cdiv(len, 4 * chunk_blocks));
           for (int k = 0, jb = j; k < nch; ++k) {
             const int sz = len / nch + (k < len % nch ? 1 : 0);
             const bool last = k == nch - 1;
@@ -359,10 +359,14 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
         int j1 = j + 1;
         while (j1 < nb[pos] && p->cnt[row[j1]] == c) ++j1;
         const int len = j1 - j;
-        // a chunk is read by each of its row blocks, so wide runs take longer
-        // chunks: fewer partials, the same bytes per row block
+        // Chunk lengths (in units of chunk_blocks, 64 at first): 4 for runs of
+        // one row block (narrow units), the row-block count up to 8 for wider
+        // runs (cooperative items re-read their chunk per item, so longer
+        // chunks mean fewer partials for the same bytes per row block).
+        // Measured on the 512-trace workload; shorter chunks lose more to
+        // per-unit start-up and merging than they gain at the launch's tail.
         const int nrb = cdiv(c * p->g, gambit::kRowsPerUnit);
-        const int nch = cdiv(len, chunk_blocks * (nrb == 1 ? 2 : std::min(nrb, 4)));
+        const int nch = cdiv(len, chunk_blocks * (nrb == 1 ? 4 : std::min(nrb, 8)));
         const int b0 = row[j];
         for (int k = 0, jb = j; k < nch; ++k) {
           const int sz = len / nch + (k < len % nch ? 1 : 0);
