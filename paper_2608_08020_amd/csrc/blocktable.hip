@@ -173,22 +173,6 @@ __global__ void write_kernel(DevPool P, int32_t trace, int32_t pos0, const uint8
   }
 }
 
-// The decode step's append: list position i writes its new token at
-// position seq_len - 1 (the allocator already advanced seq_len).
-__global__ void append_write_kernel(DevPool P, const int32_t* list, const uint8_t* k_new,
-                                    const uint8_t* v_new) {
-  const int i = blockIdx.x;
-  const int tr = list[i];
-  const int pos = P.seq_len[tr] - 1;
-  const int blk = pos >= 0 ? P.table[(size_t)tr * P.max_blocks + pos / kBlock] : -1;
-  if ((unsigned)blk >= (unsigned)P.num_blocks) {
-    if (threadIdx.x == 0) atomicOr(P.err, kErrBadBlock);
-    return;
-  }
-  const size_t tok_bytes = (size_t)P.Hkv * kHeadDim * P.esize;
-  copy_token(P, blk, pos % kBlock, k_new + i * tok_bytes, v_new + i * tok_bytes);
-}
-
 // Prune: one workgroup per trace.
 __global__ void free_kernel(DevPool P, const int32_t* ids) {
   const int tr = ids[blockIdx.x];
@@ -283,14 +267,6 @@ hipError_t launch_write(const DevPool& P, int32_t trace, int32_t pos0, int32_t n
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(write_kernel, dim3(n), dim3(128), 0, s, P, trace, pos0,
                      static_cast<const uint8_t*>(k), static_cast<const uint8_t*>(v), started_scales);
-  return hipGetLastError();
-}
-
-hipError_t launch_append_write(const DevPool& P, const int32_t* list, int32_t n, const void* k_new,
-                               const void* v_new, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(append_write_kernel, dim3(n), dim3(128), 0, s, P, list,
-                     static_cast<const uint8_t*>(k_new), static_cast<const uint8_t*>(v_new));
   return hipGetLastError();
 }
 

@@ -427,11 +427,43 @@ __device__ inline void pv_direct(Tile<FP8>& t, f32x4 s0, f32x4 s1, int t0, int n
 // i, so the matrix cores and the vector ALUs overlap; a buffer's K half is
 // refilled with tile j + 2 right after QK(j) and its V half right after
 // P.V(j), so two tiles are always in flight.
+// The decode step's append, for one KV head: the unit whose end is read at
+// run time covers its trace's last block (the allocator has already
+// advanced the length), so it writes the new token there; the unit waits
+// for the stores before its first tile load.  Only this wave touches this
+// (block, head) tile in the launch.
+template <bool FP8>
+__device__ inline void append_token(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int lane) {
+  constexpr int es = FP8 ? 1 : 2;
+  const int tpos = P.seq_len[U.owner] - 1;
+  const int b = P.table[(size_t)U.owner * P.max_blocks + (tpos >> 4)];
+  if ((unsigned)b >= (unsigned)P.num_blocks) {
+    if (lane == 0) atomicOr(P.err, kErrBadBlock);
+    return;
+  }
+  const int row = tpos & 15, pos = A.members[U.mem_off];
+  const size_t src = ((size_t)pos * P.Hkv + U.kvh) * kHeadDim * es;
+  const size_t tile = head_off<FP8>(b, P.Hkv, U.kvh);
+  if (lane < kHeadDim * es / 16)  // K: 16-byte d-chunks at token row k_phys(row)
+    *reinterpret_cast<uint4*>(P.k_cache + tile + ((size_t)lane * kBlock + k_phys(row)) * 16) =
+        *reinterpret_cast<const uint4*>(A.k_new + src + lane * 16);
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {  // V transposed: element d at d * 16 + row
+    const int d = 2 * lane + e;
+    if constexpr (FP8)
+      P.v_cache[tile + (size_t)d * kBlock + row] = A.v_new[src + d];
+    else
+      *reinterpret_cast<uint16_t*>(P.v_cache + tile + ((size_t)d * kBlock + row) * 2) =
+          reinterpret_cast<const uint16_t*>(A.v_new + src)[d];
+  }
+}
+
 template <bool FP8>
 __device__ void narrow_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int lane) {
   const int32_t* brow = P.table + (size_t)U.owner * P.max_blocks + U.jb0;
   const int ntok = U.nblk >= 0 ? U.nblk * kBlock : P.seq_len[U.owner] - U.jb0 * kBlock;
   if (ntok <= 0) return;
+  if (U.nblk < 0) append_token<FP8>(P, A, U, lane);
   const int R = U.mem_cnt * P.g;  // <= 16
   const LaneGeom g = lane_geom(lane);
   const int nblk = (ntok + kBlock - 1) / kBlock;
@@ -453,6 +485,7 @@ __device__ void narrow_unit(const DevPool& P, const AttnLaunch& A, const AttnUni
   auto meta = [&](int i, TileMeta& m) { ids.tile(i, m.b0, m.b1, m.ks0, m.ks1, m.vs0, m.vs1); };
   Tile<FP8> ta, tb;
   TileMeta ma{}, mb{}, na{}, nb{};  // current and next (tile + 2) metadata of buffers A and B
+  if (U.nblk < 0) __builtin_amdgcn_s_waitcnt(0);  // the appended token is in the cache
   meta(0, ma);
   fetch_k(ma, ta);
   fetch_v(ma, ta);

@@ -721,9 +721,10 @@ gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, 
   }
   const int32_t* dlist = ws_ptr<int32_t>(p, p->L.list);
   HIP_TRY(p, gambit::launch_alloc(p->dev, dlist, nullptr, 1, n, p->append_scale, s), "append alloc");
-  HIP_TRY(p, gambit::launch_append_write(p->dev, dlist, n, k_new, v_new, s), "append write");
   gambit::AttnLaunch A{};
   A.q = static_cast<const uint16_t*>(q);
+  A.k_new = static_cast<const uint8_t*>(k_new);  // appended by the attention launch
+  A.v_new = static_cast<const uint8_t*>(v_new);
   A.units = ws_ptr<AttnUnit>(p, p->L.units);
   std::memcpy(A.xcd_off, p->xcd_off, sizeof A.xcd_off);
   A.grid = p->grid;

@@ -66,6 +66,8 @@ enum : int32_t {
 
 struct AttnLaunch {
   const uint16_t* q;        // [n][Hq][128] bf16
+  const uint8_t* k_new;     // [n][Hkv][128] cache elements: this step's token, written by the
+  const uint8_t* v_new;     //   unit that covers the trace's last block (end read at run time)
   const AttnUnit* units;    // workgroup slots of 4 entries, grouped by XCD
   int32_t xcd_off[9];       // XCD x's workgroup slots: entries [xcd_off[x], xcd_off[x+1])
   int32_t grid;             // one workgroup per slot, rounded up to a multiple of 8
@@ -89,8 +91,6 @@ hipError_t launch_alloc(const DevPool& P, const int32_t* req_trace, const int32_
                         int32_t uniform_ntok, int32_t m, float new_scale, hipStream_t s);
 hipError_t launch_write(const DevPool& P, int32_t trace, int32_t pos0, int32_t n, const void* k,
                         const void* v, const float* started_scales, hipStream_t s);
-hipError_t launch_append_write(const DevPool& P, const int32_t* list, int32_t n, const void* k_new,
-                               const void* v_new, hipStream_t s);
 hipError_t launch_free(const DevPool& P, const int32_t* ids, int32_t n, hipStream_t s);
 // pairs: device [n][2] (child, parent).  req_trace/req_ntok: scratch [n].
 hipError_t launch_fork(const DevPool& P, const int32_t* pairs, int32_t n, int32_t* req_trace,
