@@ -22,13 +22,20 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-mcode
          "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 
 
+# The attention kernel takes maxima of matrix-core results.  In IEEE mode
+# every such max first quiets its operands (one extra instruction each); no
+# NaN ever reaches a max there (cache slots past a chunk's end are replaced
+# by a select before any max), so that source is built without IEEE mode.
+EXTRA = {"decode_attn.hip": ["-fno-honor-nans", "-mno-amdgpu-ieee"]}
+
+
 def build(verbose: bool = False) -> str:
     objs = []
     build_dir = os.path.join(HERE, "_build")
     os.makedirs(build_dir, exist_ok=True)
     for src in SOURCES:
         obj = os.path.join(build_dir, src + ".o")
-        cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         r = subprocess.run(cmd, capture_output=True, text=True)
