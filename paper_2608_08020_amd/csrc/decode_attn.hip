@@ -120,6 +120,26 @@ __device__ inline uint4 keep_first16(uint4 x, int nv) {
   return make_uint4(keep_bytes(x.x, nv), keep_bytes(x.y, nv - 4), keep_bytes(x.z, nv - 8), keep_bytes(x.w, nv - 12));
 }
 
+// The narrow path's KV reads are streaming: each byte is read once per
+// launch by one wave and the working set is far larger than L2 and the
+// memory-side cache, so they carry the non-temporal hint (on gfx950 a plain
+// read stream sustains ~6.4 TB/s without it and ~7.2 TB/s with it).  The
+// cooperative path keeps the default policy: items that split one chunk's
+// rows re-read it and should find it in L2 (measured: the hint there costs
+// more than it saves, even for chunks no other item reads).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ inline uint4 ld_stream16(const uint8_t* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ inline uint2 ld_stream8(const uint8_t* p) {
+  const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+  return make_uint2(v.x, v.y);
+}
+
 struct RowState {
   float m, l;  // reference max (log2 units) and per-lane running sum of exp2(s - m)
   f32x4 acc[8];
@@ -355,7 +375,7 @@ __device__ inline void load_k(const uint8_t* kc0, const uint8_t* kc1, const Lane
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
 #pragma unroll
-    for (int j = 0; j < (FP8 ? 2 : 4); ++j) t.k[h][j] = *reinterpret_cast<const uint4*>(base + j * 1024 + h * 128);
+    for (int j = 0; j < (FP8 ? 2 : 4); ++j) t.k[h][j] = ld_stream16(base + j * 1024 + h * 128);
   }
 }
 
@@ -364,11 +384,11 @@ __device__ inline void load_v(const uint8_t* vc0, const uint8_t* vc1, const Lane
   if constexpr (!FP8) {
     const uint8_t* base = (g.vb1 ? vc1 : vc0) + g.lr * 32 + (g.q & 1) * 16;
 #pragma unroll
-    for (int r = 0; r < 8; ++r) t.v[r] = *reinterpret_cast<const uint4*>(base + r * 512);
+    for (int r = 0; r < 8; ++r) t.v[r] = ld_stream16(base + r * 512);
   } else {
     const uint8_t* base = (g.vb1 ? vc1 : vc0) + g.lr * 16 + (g.q & 1) * 8;
 #pragma unroll
-    for (int r = 0; r < 8; ++r) t.v[r] = *reinterpret_cast<const uint2*>(base + r * 256);
+    for (int r = 0; r < 8; ++r) t.v[r] = ld_stream8(base + r * 256);
   }
 }
 

@@ -18,7 +18,6 @@
 #include <cstring>
 #include <numeric>
 #include <string>
-#include <unordered_map>
 #include <vector>
 
 #include "../../include/gambit.h"
@@ -252,10 +251,8 @@ struct Group {
 gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t s) {
   const int Hkv = p->d.num_kv_heads;
   const int kmax = p->L.kmax;
-  const int tile_members = gambit::kRowsPerUnit / p->g;
   const int nb_total = p->d.num_blocks;
-  if ((int)p->cnt.size() != nb_total) {
-    p->cnt.assign(nb_total, 0);
+  if ((int)p->first.size() != nb_total) {
     p->first.assign(nb_total, -1);
     p->csr_off.assign(nb_total, 0);
     p->csr_fill.assign(nb_total, 0);
@@ -538,6 +535,7 @@ gambit_status gambit_pool_create(const gambit_pool_desc* desc, void* stream, gam
   p->table.assign(desc->max_traces, {});
   p->seq_len.assign(desc->max_traces, 0);
   p->refcount.assign(desc->num_blocks, 0);
+  p->cnt.assign(desc->num_blocks, 0);  // per-block counter of the planner and the round's out-of-blocks test
   p->freebits.assign(cdiv(desc->num_blocks, 64), ~0ull);
   if (desc->num_blocks % 64) p->freebits.back() = (1ull << (desc->num_blocks % 64)) - 1;
   p->nfree = desc->num_blocks;
@@ -821,16 +819,20 @@ gambit_status gambit_score_prune_branch(gambit_pool* p, int32_t n, const int32_t
     if (pairs[2 * j] != freed[j] || pairs[2 * j + 1] != kept[j / c])
       return fail(p, GAMBIT_ERR_DEVICE, "device prune/branch plan disagrees with the ranking");
   if (nfree_traces == 0) return GAMBIT_OK;
-  std::unordered_map<int, int> drop;
-  int released = 0;
-  for (int t : freed)
-    for (int blk : p->table[t]) ++drop[blk];
-  for (auto& kv : drop) released += p->refcount[kv.first] == kv.second;
   int tails = 0;
   for (int j = 0; j < nfree_traces; ++j) tails += p->seq_len[kept[j / c]] % 16 ? 1 : 0;
-  if (tails > p->nfree + released)
-    return fail(p, GAMBIT_ERR_OUT_OF_BLOCKS, "branching needs %d blocks, %d free after pruning", tails,
-                p->nfree + released);
+  if (tails > p->nfree) {
+    // Only now count the blocks pruning releases: references the pruned
+    // rows drop per block (the planner's per-block counter, left at zero).
+    int released = 0;
+    for (int t : freed)
+      for (int blk : p->table[t]) released += ++p->cnt[blk] == p->refcount[blk];
+    for (int t : freed)
+      for (int blk : p->table[t]) p->cnt[blk] = 0;
+    if (tails > p->nfree + released)
+      return fail(p, GAMBIT_ERR_OUT_OF_BLOCKS, "branching needs %d blocks, %d free after pruning", tails,
+                  p->nfree + released);
+  }
   HIP_TRY(p, gambit::launch_free(p->dev, PL.free_list, nfree_traces, s), "free kernel");
   HIP_TRY(p, gambit::launch_fork(p->dev, child_parent_out, nfree_traces, ws_ptr<int32_t>(p, p->L.req_trace),
                                  ws_ptr<int32_t>(p, p->L.req_ntok), s),
