@@ -176,6 +176,9 @@ __device__ inline void softmax_p(const f32x4& s0, const f32x4& s1, bool partial,
                                  RowState& st, bf16x8& ph, bf16x8& pl) {
   float sv[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
   if (partial) {
+    // Only a chunk's last tile is partial; the empty asm keeps this a branch
+    // (if-converted, the selects would run on every tile).
+    asm volatile("");
 #pragma unroll
     for (int e = 0; e < 8; ++e) sv[e] = e < nv ? sv[e] : -INFINITY;
   }
@@ -236,7 +239,7 @@ __device__ inline void write_partial(const DevPool& P, const AttnLaunch& A, cons
   const size_t idx = ((size_t)pos * P.Hq + h) * A.kmax + U.kidx;
   f32x4* dst = reinterpret_cast<f32x4*>(A.part_acc + idx * kHeadDim + 4 * q);
 #pragma unroll
-  for (int k = 0; k < 8; ++k) dst[4 * k] = st.acc[k];
+  for (int k = 0; k < 8; ++k) __builtin_nontemporal_store(st.acc[k], dst + 4 * k);  // read once, by the merge
   if (q == 0) A.part_ml[idx] = float2{st.m, l};
 }
 
