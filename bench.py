@@ -14,7 +14,8 @@ warm-up covers the first round, so the timed steps measure the steady state.
 Prints one JSON line.  `value` is trace-steps/s over the timed steps with
 every input already resident in HBM.  `roofline` prices the dominant kernel
 (split-K attention) by its algorithmic bytes - every distinct KV block the
-population references read once, plus queries and block-table entries - over
+population references read once, plus queries, block-table entries and the
+step's append that the same launch performs (new K/V read and written) - over
 its event-timed average duration.  `cpu_baseline` times the CPU oracle on a
 bounded sample of the same workload.
 """
@@ -144,8 +145,10 @@ def main():
     for s in range(W, W + K):
         run.decode(s, out=out)
         st = pool.plan_stats(ids)
+        # every distinct block once (valid tokens), fp8 scales, queries, table
+        # entries, and the step's append (new K/V read, written into the cache)
         alg_bytes.append(st.unique_tokens * Hkv * D * 2 * e + (8 * st.unique_blocks if e == 1 else 0)
-                         + T * Hq * D * 2 + 4 * st.table_entries)
+                         + T * Hq * D * 2 + 4 * st.table_entries + 2 * T * Hkv * D * 2 * e)
         ctx_tokens += st.total_tokens
         if s in round_of:
             run.round(round_of[s])
