@@ -28,6 +28,11 @@ Contents and the passages each part follows:
                   blocks + copy the partial tail, free = drop references
                   (Sec. 4.1 Case 2: pruning frees the non-shared blocks, the
                   child inherits the parent's KV through prefix caching).
+* ``tournament`` - the full tournament of Alg. 1 over the pool model:
+                  running-mean scores, GenLen eligibility, Case 1 fill
+                  (Eq. 2), Case 2 swap (Eq. 3), scheduler eviction of the
+                  lowest-scoring running trace into a ghost that keeps its
+                  place in the tree view (Sec. 4.2).
 
 Parity status: every function is pinned by the ``-m "not gpu"`` tests
 (closed forms, library special cases, invariants, brute force, exhaustive
