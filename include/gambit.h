@@ -127,7 +127,8 @@ gambit_status gambit_pool_destroy(gambit_pool* pool);
 
 /* Extend each listed trace by n_tokens[i] positions (allocation rule above).
  * trace_ids, n_tokens: host [n].  The new positions hold no data until
- * written.  fp8: new blocks get scale (1, 1). */
+ * written.  fp8: new blocks get scale (1, 1).  A ghost's slot (see
+ * gambit_evict) cannot be extended. */
 gambit_status gambit_kv_alloc(gambit_pool* pool, int32_t n, const int32_t* trace_ids,
                               const int32_t* n_tokens, void* stream);
 
@@ -144,7 +145,8 @@ gambit_status gambit_kv_write(gambit_pool* pool, int32_t trace_id, int32_t pos0,
  * prefix of parent_ids[i].  The child row lists the parent's full blocks
  * (refcount + 1 each); a partial last block is copied into one new block
  * (with its fp8 scales); the child's length equals the parent's.  Children
- * must be empty, distinct, and not parents in the same call.
+ * must be empty (neither running nor a ghost), distinct, and not parents in
+ * the same call; a child takes its parent's tournament scores (see below).
  * parent_ids, child_ids: host [n]. */
 gambit_status gambit_kv_fork(gambit_pool* pool, int32_t n, const int32_t* parent_ids,
                              const int32_t* child_ids, void* stream);
@@ -198,9 +200,76 @@ gambit_status gambit_score_prune_branch(gambit_pool* pool, int32_t n, const int3
 gambit_status gambit_rank_topk(int32_t n, const int32_t* trace_ids, const float* scores,
                                int32_t keep, int32_t* keep_out, void* stream);
 
+/*
+ * The full tournament of Alg. 1.  Per trace slot the pool keeps the running
+ * mean score s_bar over the trace's thoughts and their number n, the tokens
+ * the trace has generated since its creation (GenLen: decode steps count,
+ * kv_alloc/kv_write do not; a child starts at 0), and a ghost flag.  Two
+ * views of the population (Sec. 4.2): the scheduler view is the running
+ * traces (they hold KV blocks); the tree view adds the ghosts, traces the
+ * scheduler evicted under memory pressure - no KV, no tokens, but they keep
+ * their score and their place in the ranking, so capacity is counted on the
+ * tree view.  A fork gives the child its parent's (s_bar, n); a trace that
+ * ends (kv_free, pruning) clears its slot's state.
+ */
+typedef struct {
+  int32_t case_taken;            /* 1: under capacity (Eq. 2), 2: swap (Eq. 3), 0: empty tree view */
+  int32_t n_active;              /* N, the tree view's size before the round      */
+  int32_t n_pruned;              /* entries written to pruned_out                 */
+  int32_t n_children;            /* (child, parent) pairs written                 */
+} gambit_round;
+
+/* Alg. 1 Generate, scoring: each listed trace completed a thought; its score
+ * is f = 1 / (1 + exp(-(h . w + b))) and its running mean becomes
+ * s_bar + (f - s_bar) / (n + 1) over n + 1 thoughts (the mean of the thought
+ * scores of Sec. 4.1).
+ *   trace_ids   host [n], running traces, distinct
+ *   h           device [n][Dh] bf16 (Dh a multiple of 8); w device [Dh] fp32
+ *   scores_out  device [n] fp32: f in list order */
+gambit_status gambit_score_update(gambit_pool* pool, int32_t n, const int32_t* trace_ids, const void* h,
+                                  int32_t Dh, const float* w, float b, float* scores_out, void* stream);
+
+/* Alg. 1 Schedule (Sec. 4.2): of the listed running traces, the one of
+ * lowest s_bar (on equal scores the higher id) is evicted - its blocks are
+ * released as by kv_free, but it becomes a ghost that keeps its score.
+ *   trace_ids   host [n], running traces, n <= 4096;  victim_out host [1]
+ * Blocks until the choice is known (one device-to-host copy). */
+gambit_status gambit_evict(gambit_pool* pool, int32_t n, const int32_t* trace_ids, int32_t* victim_out,
+                           void* stream);
+
+/* Alg. 1 Tournament (Eqs. 2-3) over the tree view.  Rank it by s_bar
+ * (descending; equal scores: lower id first).  Eligible parents: running
+ * traces with GenLen >= warmup.  With N traces in the tree view:
+ *   N < capacity (Case 1): branch the top min(capacity - N, |eligible|);
+ *   N >= capacity (Case 2): prune the bottom min(swap_k, N) - running ones
+ *     release their blocks, ghosts leave the tree view - then branch the top
+ *     min(swap_k, |eligible not pruned|).
+ * Children take the lowest vacant slots (neither running nor ghost, after
+ * the pruning) in ascending order, one per parent in rank order; a branch is
+ * a kv_fork (the parent continues, App. A.5).  Pruned slots are freed, in
+ * ascending order, before any fork.
+ *   capacity in 1 .. max_traces (<= 4096);  swap_k, warmup >= 0
+ *   round_out         host: what the round did
+ *   pruned_out        host [>= swap_k]: pruned ids, ascending
+ *   child_parent_out  host [max_traces][2]: (child, parent) pairs
+ *   ranked_out        device [max_traces] int32 or NULL: the tree view in
+ *                     rank order (first n_active entries)
+ * The plan is computed on the device, read back once, checked against the
+ * host mirror (everything but the scores) and the out-of-blocks test, and
+ * only then applied; on error nothing has changed. */
+gambit_status gambit_tournament(gambit_pool* pool, int32_t capacity, int32_t swap_k, int32_t warmup,
+                                gambit_round* round_out, int32_t* pruned_out, int32_t* child_parent_out,
+                                int32_t* ranked_out, void* stream);
+
+/* Tournament state of the listed slots (host outputs, any may be NULL);
+ * synchronises `stream`.  sbar fp32, nscore/gen int32, ghost 0/1. */
+gambit_status gambit_trace_state(gambit_pool* pool, int32_t n, const int32_t* trace_ids, float* sbar_out,
+                                 int32_t* nscore_out, int32_t* gen_out, int32_t* ghost_out, void* stream);
+
 /* Synchronise `stream`, then compare the device block table, lengths,
- * refcounts and free set with the host mirror and read the device error
- * word.  GAMBIT_OK when all agree. */
+ * refcounts, free set and tournament bookkeeping (scored thoughts, GenLen,
+ * ghost flags) with the host mirror and read the device error word.
+ * GAMBIT_OK when all agree. */
 gambit_status gambit_pool_check(gambit_pool* pool, void* stream);
 
 /* Statistics of the attention work for a trace list (host only, no sync). */

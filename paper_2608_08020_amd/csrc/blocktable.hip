@@ -20,7 +20,13 @@ __global__ void pool_init_kernel(DevPool P) {
   const size_t i0 = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   const size_t ntab = (size_t)P.max_traces * P.max_blocks;
   for (size_t i = i0; i < ntab; i += stride) P.table[i] = -1;
-  for (size_t i = i0; i < (size_t)P.max_traces; i += stride) P.seq_len[i] = 0;
+  for (size_t i = i0; i < (size_t)P.max_traces; i += stride) {
+    P.seq_len[i] = 0;
+    P.sbar[i] = 0.f;
+    P.nscore[i] = 0;
+    P.gen[i] = 0;
+    P.ghost[i] = 0;
+  }
   for (size_t i = i0; i < (size_t)P.num_blocks; i += stride) P.refcount[i] = 0;
   for (size_t w = i0; w < (size_t)P.nwords; w += stride) {
     const int lo = (int)w * 32;
@@ -63,7 +69,7 @@ __device__ int wg_exclusive_scan(int v, int* total) {
 // assignment.
 __global__ __launch_bounds__(kAllocThreads) void alloc_kernel(DevPool P, const int32_t* req_trace,
                                                              const int32_t* req_ntok, int32_t uniform,
-                                                             int32_t m, float new_scale) {
+                                                             int32_t m, float new_scale, int32_t generated) {
   const int t = threadIdx.x;
   const int rpt = (m + kAllocThreads - 1) / kAllocThreads;
   const int r0 = min(m, t * rpt), r1 = min(m, r0 + rpt);
@@ -126,6 +132,7 @@ __global__ __launch_bounds__(kAllocThreads) void alloc_kernel(DevPool P, const i
       }
     }
     P.seq_len[tr] = L + nt;
+    if (generated) P.gen[tr] += nt;
   }
 }
 
@@ -173,8 +180,9 @@ __global__ void write_kernel(DevPool P, int32_t trace, int32_t pos0, const uint8
   }
 }
 
-// Prune: one workgroup per trace.
-__global__ void free_kernel(DevPool P, const int32_t* ids) {
+// Prune (or evict): one workgroup per trace.  A row may be empty (a ghost
+// leaving the tree view).
+__global__ void free_kernel(DevPool P, const int32_t* ids, int32_t mode) {
   const int tr = ids[blockIdx.x];
   const int nb = cdiv16(P.seq_len[tr]);
   int32_t* row = P.table + (size_t)tr * P.max_blocks;
@@ -190,7 +198,17 @@ __global__ void free_kernel(DevPool P, const int32_t* ids) {
     if (old < 1) atomicOr(P.err, kErrRefUnderflow);
   }
   __syncthreads();
-  if (threadIdx.x == 0) P.seq_len[tr] = 0;
+  if (threadIdx.x == 0) {
+    P.seq_len[tr] = 0;
+    P.gen[tr] = 0;
+    if (mode == kFreeEvict) {
+      P.ghost[tr] = 1;  // keeps its score and its place in the tree view
+    } else {
+      P.ghost[tr] = 0;
+      P.sbar[tr] = 0.f;
+      P.nscore[tr] = 0;
+    }
+  }
 }
 
 // Branch, part 1: the child row takes the parent's full blocks (refcount + 1)
@@ -215,6 +233,12 @@ __global__ void fork_share_kernel(DevPool P, const int32_t* pairs, int32_t* req_
     P.seq_len[child] = full * kBlock;
     req_trace[blockIdx.x] = child;
     req_ntok[blockIdx.x] = L % kBlock;
+    // the child's trace is the parent's prefix: it inherits the parent's
+    // thought scores, and has generated nothing of its own yet
+    P.sbar[child] = P.sbar[parent];
+    P.nscore[child] = P.nscore[parent];
+    P.gen[child] = 0;
+    P.ghost[child] = 0;
   }
 }
 
@@ -255,10 +279,10 @@ hipError_t launch_pool_init(const DevPool& P, hipStream_t s) {
 }
 
 hipError_t launch_alloc(const DevPool& P, const int32_t* req_trace, const int32_t* req_ntok,
-                        int32_t uniform_ntok, int32_t m, float new_scale, hipStream_t s) {
+                        int32_t uniform_ntok, int32_t m, float new_scale, bool generated, hipStream_t s) {
   if (m <= 0) return hipSuccess;
   hipLaunchKernelGGL(alloc_kernel, dim3(1), dim3(kAllocThreads), 0, s, P, req_trace, req_ntok,
-                     uniform_ntok, m, new_scale);
+                     uniform_ntok, m, new_scale, (int32_t)generated);
   return hipGetLastError();
 }
 
@@ -270,9 +294,9 @@ hipError_t launch_write(const DevPool& P, int32_t trace, int32_t pos0, int32_t n
   return hipGetLastError();
 }
 
-hipError_t launch_free(const DevPool& P, const int32_t* ids, int32_t n, hipStream_t s) {
+hipError_t launch_free(const DevPool& P, const int32_t* ids, int32_t n, int32_t mode, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(free_kernel, dim3(n), dim3(256), 0, s, P, ids);
+  hipLaunchKernelGGL(free_kernel, dim3(n), dim3(256), 0, s, P, ids, mode);
   return hipGetLastError();
 }
 
@@ -282,7 +306,7 @@ hipError_t launch_fork(const DevPool& P, const int32_t* pairs, int32_t n, int32_
   hipLaunchKernelGGL(fork_share_kernel, dim3(n), dim3(256), 0, s, P, pairs, req_trace, req_ntok);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = launch_alloc(P, req_trace, req_ntok, -1, n, 1.0f, s);
+  e = launch_alloc(P, req_trace, req_ntok, -1, n, 1.0f, false, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(fork_tail_kernel, dim3(n), dim3(256), 0, s, P, pairs);
   return hipGetLastError();

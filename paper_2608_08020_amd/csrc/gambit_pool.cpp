@@ -37,7 +37,7 @@ int cdiv(int a, int b) { return (a + b - 1) / b; }
 // Workspace carve-up.  All offsets are kAlign-aligned.
 struct Layout {
   size_t list, ids, req_trace, req_ntok, pairs, free_list, nk, ticket, queues, err, scales, freebits,
-      alloc_list, units, members, part_ml, part_acc, total;
+      alloc_list, units, members, part_ml, part_acc, sbar, nscore, gen, ghost, tourn, total;
   int kmax, max_units, max_members, nwords;
 };
 
@@ -79,6 +79,11 @@ bool layout_of(const gambit_pool_desc* d, Layout* L) {
   L->members = take(4 * (size_t)L->max_members);
   L->part_ml = take(8 * (size_t)T * d->num_q_heads * kmax);
   L->part_acc = take(4 * (size_t)T * d->num_q_heads * kmax * gambit::kHeadDim);
+  L->sbar = take(4 * (size_t)T);
+  L->nscore = take(4 * (size_t)T);
+  L->gen = take(4 * (size_t)T);
+  L->ghost = take(4 * (size_t)T);
+  L->tourn = take(4 * ((size_t)gambit::kTournHeader + 3 * (size_t)T));
   L->total = o;
   return true;
 }
@@ -96,6 +101,10 @@ struct gambit_pool {
   // host mirror
   std::vector<std::vector<int32_t>> table;
   std::vector<int32_t> seq_len, refcount;
+  // tournament bookkeeping (Alg. 1): scored thoughts, tokens generated since
+  // creation, ghost flag; the scores themselves live on the device only
+  std::vector<int32_t> nscore, gen;
+  std::vector<char> ghost;
   std::vector<uint64_t> freebits;  // bit set = free
   int32_t nfree = 0;
   size_t hint = 0;                 // no free bit below word `hint`
@@ -196,13 +205,30 @@ void mirror_fork(gambit_pool* p, int parent, int child) {
   for (int b : c) ++p->refcount[b];
   p->seq_len[child] = full * 16;
   mirror_grow(p, child, L % 16);
+  p->nscore[child] = p->nscore[parent];
+  p->gen[child] = 0;
+  p->ghost[child] = 0;
 }
 
-void mirror_free(gambit_pool* p, int t) {
+void mirror_release_rows(gambit_pool* p, int t) {
   for (int b : p->table[t])
     if (--p->refcount[b] == 0) release(p, b);
   p->table[t].clear();
   p->seq_len[t] = 0;
+  p->gen[t] = 0;
+}
+
+// The trace ends (pruned, completed, or a ghost leaving the tree view).
+void mirror_free(gambit_pool* p, int t) {
+  mirror_release_rows(p, t);
+  p->nscore[t] = 0;
+  p->ghost[t] = 0;
+}
+
+// The scheduler evicts the trace: no KV, but it stays in the tree view.
+void mirror_evict(gambit_pool* p, int t) {
+  mirror_release_rows(p, t);
+  p->ghost[t] = 1;
 }
 
 // ---- staging ---------------------------------------------------------------
@@ -523,6 +549,10 @@ gambit_status gambit_pool_create(const gambit_pool_desc* desc, void* stream, gam
   D.freebits = ws_ptr<uint32_t>(p, L.freebits);
   D.alloc_list = ws_ptr<int32_t>(p, L.alloc_list);
   D.err = ws_ptr<int32_t>(p, L.err);
+  D.sbar = ws_ptr<float>(p, L.sbar);
+  D.nscore = ws_ptr<int32_t>(p, L.nscore);
+  D.gen = ws_ptr<int32_t>(p, L.gen);
+  D.ghost = ws_ptr<int32_t>(p, L.ghost);
   D.num_blocks = desc->num_blocks;
   D.nwords = L.nwords;
   D.max_traces = desc->max_traces;
@@ -535,6 +565,9 @@ gambit_status gambit_pool_create(const gambit_pool_desc* desc, void* stream, gam
   p->table.assign(desc->max_traces, {});
   p->seq_len.assign(desc->max_traces, 0);
   p->refcount.assign(desc->num_blocks, 0);
+  p->nscore.assign(desc->max_traces, 0);
+  p->gen.assign(desc->max_traces, 0);
+  p->ghost.assign(desc->max_traces, 0);
   p->cnt.assign(desc->num_blocks, 0);  // per-block counter of the planner and the round's out-of-blocks test
   p->freebits.assign(cdiv(desc->num_blocks, 64), ~0ull);
   if (desc->num_blocks % 64) p->freebits.back() = (1ull << (desc->num_blocks % 64)) - 1;
@@ -590,6 +623,7 @@ gambit_status gambit_kv_alloc(gambit_pool* p, int32_t n, const int32_t* ids, con
   long need = 0;
   for (int i = 0; i < n; ++i) {
     if (ntok[i] < 0) return fail(p, GAMBIT_ERR_INVALID, "negative token count");
+    if (p->ghost[ids[i]]) return fail(p, GAMBIT_ERR_INVALID, "slot %d holds a ghost trace", ids[i]);
     const long L = p->seq_len[ids[i]];
     if (cdiv((int)std::min<long>(L + ntok[i], 1L << 30), 16) > p->d.max_blocks_per_trace)
       return fail(p, GAMBIT_ERR_INVALID, "trace %d would exceed max_blocks_per_trace", ids[i]);
@@ -606,7 +640,7 @@ gambit_status gambit_kv_alloc(gambit_pool* p, int32_t n, const int32_t* ids, con
   HIP_TRY(p, hipMemcpyAsync(rt, p->stage, 4 * (size_t)n, hipMemcpyHostToDevice, S(stream)), "upload");
   HIP_TRY(p, hipMemcpyAsync(rn, p->stage + n, 4 * (size_t)n, hipMemcpyHostToDevice, S(stream)), "upload");
   HIP_TRY(p, hipEventRecord(p->stage_ev, S(stream)), "staging fence");
-  HIP_TRY(p, gambit::launch_alloc(p->dev, rt, rn, -1, n, 1.0f, S(stream)), "alloc kernel");
+  HIP_TRY(p, gambit::launch_alloc(p->dev, rt, rn, -1, n, 1.0f, false, S(stream)), "alloc kernel");
   for (int i = 0; i < n; ++i) mirror_grow(p, ids[i], ntok[i]);
   invalidate_plan(p);
   return GAMBIT_OK;
@@ -652,7 +686,7 @@ gambit_status gambit_kv_fork(gambit_pool* p, int32_t n, const int32_t* parents, 
     const int par = parents[i], ch = children[i];
     if (par < 0 || par >= p->d.max_traces) return fail(p, GAMBIT_ERR_INVALID, "parent id %d out of range", par);
     if (is_child[par]) return fail(p, GAMBIT_ERR_INVALID, "trace %d is both parent and child", par);
-    if (p->seq_len[ch] != 0) return fail(p, GAMBIT_ERR_INVALID, "child slot %d is not empty", ch);
+    if (p->seq_len[ch] != 0 || p->ghost[ch]) return fail(p, GAMBIT_ERR_INVALID, "child slot %d is not empty", ch);
     if (p->seq_len[par] == 0) return fail(p, GAMBIT_ERR_INVALID, "parent %d is empty", par);
     tails += p->seq_len[par] % 16 ? 1 : 0;
   }
@@ -685,7 +719,7 @@ gambit_status gambit_kv_free(gambit_pool* p, int32_t n, const int32_t* ids, void
   int32_t* d = ws_ptr<int32_t>(p, p->L.ids);
   st = upload_ints(p, d, ids, n, S(stream));
   if (st) return st;
-  HIP_TRY(p, gambit::launch_free(p->dev, d, n, S(stream)), "free kernel");
+  HIP_TRY(p, gambit::launch_free(p->dev, d, n, gambit::kFreeEnd, S(stream)), "free kernel");
   for (int i = 0; i < n; ++i) mirror_free(p, ids[i]);
   invalidate_plan(p);
   return GAMBIT_OK;
@@ -718,7 +752,7 @@ gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, 
     if (st) return st;
   }
   const int32_t* dlist = ws_ptr<int32_t>(p, p->L.list);
-  HIP_TRY(p, gambit::launch_alloc(p->dev, dlist, nullptr, 1, n, p->append_scale, s), "append alloc");
+  HIP_TRY(p, gambit::launch_alloc(p->dev, dlist, nullptr, 1, n, p->append_scale, true, s), "append alloc");
   gambit::AttnLaunch A{};
   A.q = static_cast<const uint16_t*>(q);
   A.k_new = static_cast<const uint8_t*>(k_new);  // appended by the attention launch
@@ -750,7 +784,10 @@ gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, 
   }
   HIP_TRY(p, gambit::launch_attention_merge(p->dev, A, s), "attention merge");
   p->queues_dirty = false;
-  for (int i = 0; i < n; ++i) mirror_grow(p, ids[i], 1);
+  for (int i = 0; i < n; ++i) {
+    mirror_grow(p, ids[i], 1);
+    ++p->gen[ids[i]];
+  }
   p->stats.total_tokens += n;
   p->stats.unique_tokens += n;
   p->stats.unique_blocks += need;
@@ -833,7 +870,7 @@ gambit_status gambit_score_prune_branch(gambit_pool* p, int32_t n, const int32_t
       return fail(p, GAMBIT_ERR_OUT_OF_BLOCKS, "branching needs %d blocks, %d free after pruning", tails,
                   p->nfree + released);
   }
-  HIP_TRY(p, gambit::launch_free(p->dev, PL.free_list, nfree_traces, s), "free kernel");
+  HIP_TRY(p, gambit::launch_free(p->dev, PL.free_list, nfree_traces, gambit::kFreeEnd, s), "free kernel");
   HIP_TRY(p, gambit::launch_fork(p->dev, child_parent_out, nfree_traces, ws_ptr<int32_t>(p, p->L.req_trace),
                                  ws_ptr<int32_t>(p, p->L.req_ntok), s),
           "fork kernels");
@@ -851,6 +888,160 @@ gambit_status gambit_rank_topk(int32_t n, const int32_t* ids, const float* score
                                                                                              : GAMBIT_ERR_DEVICE;
 }
 
+namespace {
+
+// Traces listed for scoring or eviction must be running.
+gambit_status check_running(gambit_pool* p, int32_t n, const int32_t* ids) {
+  gambit_status st = check_ids(p, n, ids, "trace");
+  if (st) return st;
+  for (int i = 0; i < n; ++i)
+    if (p->seq_len[ids[i]] == 0) return fail(p, GAMBIT_ERR_INVALID, "trace %d is not running", ids[i]);
+  return GAMBIT_OK;
+}
+
+}  // namespace
+
+gambit_status gambit_score_update(gambit_pool* p, int32_t n, const int32_t* ids, const void* h, int32_t Dh,
+                                  const float* w, float b, float* scores_out, void* stream) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  gambit_status st = check_running(p, n, ids);
+  if (st) return st;
+  if (n == 0) return GAMBIT_OK;
+  if (!h || !w || !scores_out) return fail(p, GAMBIT_ERR_INVALID, "NULL buffer");
+  if (Dh <= 0 || Dh % 8) return fail(p, GAMBIT_ERR_INVALID, "probe dimension %d is not a multiple of 8", Dh);
+  int32_t* d = ws_ptr<int32_t>(p, p->L.ids);
+  st = upload_ints(p, d, ids, n, S(stream));
+  if (st) return st;
+  gambit::ScoreLaunch L{d, n, static_cast<const uint16_t*>(h), Dh, w, b, scores_out};
+  HIP_TRY(p, gambit::launch_score_update(p->dev, L, S(stream)), "score kernel");
+  for (int i = 0; i < n; ++i) ++p->nscore[ids[i]];
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_evict(gambit_pool* p, int32_t n, const int32_t* ids, int32_t* victim_out, void* stream) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  gambit_status st = check_running(p, n, ids);
+  if (st) return st;
+  if (n == 0 || !victim_out) return fail(p, GAMBIT_ERR_INVALID, "no eviction candidates");
+  if (n > gambit::kMaxRank) return fail(p, GAMBIT_ERR_UNSUPPORTED, "%d candidates", n);
+  hipStream_t s = S(stream);
+  int32_t* d = ws_ptr<int32_t>(p, p->L.ids);
+  int32_t* out = ws_ptr<int32_t>(p, p->L.tourn);
+  st = upload_ints(p, d, ids, n, s);
+  if (st) return st;
+  HIP_TRY(p, gambit::launch_evict_pick(p->dev, d, n, out, s), "eviction kernel");
+  int32_t v = -1;
+  HIP_TRY(p, hipMemcpyAsync(&v, out, 4, hipMemcpyDeviceToHost, s), "readback");
+  HIP_TRY(p, hipStreamSynchronize(s), "readback");
+  if (std::find(ids, ids + n, v) == ids + n) return fail(p, GAMBIT_ERR_DEVICE, "device chose a non-candidate %d", v);
+  HIP_TRY(p, gambit::launch_free(p->dev, out, 1, gambit::kFreeEvict, s), "free kernel");
+  mirror_evict(p, v);
+  invalidate_plan(p);
+  *victim_out = v;
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_tournament(gambit_pool* p, int32_t capacity, int32_t swap_k, int32_t warmup,
+                                gambit_round* round_out, int32_t* pruned_out, int32_t* child_parent_out,
+                                int32_t* ranked_out, void* stream) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  const int T = p->d.max_traces;
+  if (T > gambit::kMaxRank) return fail(p, GAMBIT_ERR_UNSUPPORTED, "%d trace slots", T);
+  if (capacity < 1 || capacity > T || swap_k < 0 || warmup < 0)
+    return fail(p, GAMBIT_ERR_INVALID, "capacity %d (slots %d), swap %d, warmup %d", capacity, T, swap_k, warmup);
+  if (!round_out || !pruned_out || !child_parent_out) return fail(p, GAMBIT_ERR_INVALID, "NULL output");
+  hipStream_t s = S(stream);
+  int32_t* out = ws_ptr<int32_t>(p, p->L.tourn);
+  HIP_TRY(p, gambit::launch_tournament(p->dev, capacity, swap_k, warmup, out, ranked_out, s), "tournament kernel");
+  std::vector<int32_t> h((size_t)gambit::kTournHeader + 3 * (size_t)T);
+  HIP_TRY(p, hipMemcpyAsync(h.data(), out, 4 * h.size(), hipMemcpyDeviceToHost, s), "readback");
+  HIP_TRY(p, hipStreamSynchronize(s), "readback");
+  // check the device plan against everything the mirror knows (all but the scores)
+  const int kase = h[0], N = h[1], npr = h[2], m = h[3], nvac = h[4];
+  const int32_t* pr = h.data() + gambit::kTournHeader;
+  const int32_t* pairs = pr + T;
+  int Nh = 0;
+  for (int t = 0; t < T; ++t) Nh += p->seq_len[t] > 0 || p->ghost[t];
+  const int kase_h = Nh == 0 ? 0 : (Nh < capacity ? 1 : 2);
+  const int npr_h = kase_h == 2 ? std::min(swap_k, Nh) : 0;
+  if (N != Nh || kase != kase_h || npr != npr_h)
+    return fail(p, GAMBIT_ERR_DEVICE, "device tournament (case %d, N %d, pruned %d) disagrees with the mirror "
+                "(case %d, N %d, pruned %d)", kase, N, npr, kase_h, Nh, npr_h);
+  std::vector<char> gone(T, 0), par(T, 0);
+  for (int i = 0; i < npr; ++i) {
+    const int t = pr[i];
+    if (t < 0 || t >= T || !(p->seq_len[t] > 0 || p->ghost[t]) || (i && pr[i - 1] >= t))
+      return fail(p, GAMBIT_ERR_DEVICE, "device pruned an invalid trace %d", t);
+    gone[t] = 1;
+  }
+  int nb = 0;
+  for (int t = 0; t < T; ++t) nb += !gone[t] && p->seq_len[t] > 0 && !p->ghost[t] && p->gen[t] >= warmup;
+  const int m_h = kase_h == 1 ? std::min(capacity - Nh, nb) : (kase_h == 2 ? std::min(swap_k, nb) : 0);
+  std::vector<int32_t> vac;
+  for (int t = 0; t < T; ++t)
+    if ((p->seq_len[t] == 0 && !p->ghost[t]) || gone[t]) vac.push_back(t);
+  if (m != m_h || nvac != (int)vac.size() || nvac < m)
+    return fail(p, GAMBIT_ERR_DEVICE, "device tournament branches %d (mirror %d), vacant %d (mirror %d)", m, m_h,
+                nvac, (int)vac.size());
+  int tails = 0;
+  for (int j = 0; j < m; ++j) {
+    const int c = pairs[2 * j], q = pairs[2 * j + 1];
+    if (c != vac[j] || q < 0 || q >= T || gone[q] || p->seq_len[q] == 0 || p->ghost[q] || p->gen[q] < warmup ||
+        par[q])
+      return fail(p, GAMBIT_ERR_DEVICE, "device branch %d -> %d is invalid", q, c);
+    par[q] = 1;
+    tails += p->seq_len[q] % 16 ? 1 : 0;
+  }
+  if (tails > p->nfree) {
+    int released = 0;
+    for (int i = 0; i < npr; ++i)
+      for (int blk : p->table[pr[i]]) released += ++p->cnt[blk] == p->refcount[blk];
+    for (int i = 0; i < npr; ++i)
+      for (int blk : p->table[pr[i]]) p->cnt[blk] = 0;
+    if (tails > p->nfree + released)
+      return fail(p, GAMBIT_ERR_OUT_OF_BLOCKS, "branching needs %d blocks, %d free after pruning", tails,
+                  p->nfree + released);
+  }
+  // apply: end the pruned traces (running and ghost), then branch
+  HIP_TRY(p, gambit::launch_free(p->dev, out + gambit::kTournHeader, npr, gambit::kFreeEnd, s), "free kernel");
+  HIP_TRY(p, gambit::launch_fork(p->dev, out + gambit::kTournHeader + T, m, ws_ptr<int32_t>(p, p->L.req_trace),
+                                 ws_ptr<int32_t>(p, p->L.req_ntok), s),
+          "fork kernels");
+  for (int i = 0; i < npr; ++i) mirror_free(p, pr[i]);
+  for (int j = 0; j < m; ++j) mirror_fork(p, pairs[2 * j + 1], pairs[2 * j]);
+  invalidate_plan(p);
+  round_out->case_taken = kase;
+  round_out->n_active = N;
+  round_out->n_pruned = npr;
+  round_out->n_children = m;
+  std::copy(pr, pr + npr, pruned_out);
+  std::copy(pairs, pairs + 2 * m, child_parent_out);
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_trace_state(gambit_pool* p, int32_t n, const int32_t* ids, float* sbar_out,
+                                 int32_t* nscore_out, int32_t* gen_out, int32_t* ghost_out, void* stream) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  gambit_status st = check_ids(p, n, ids, "trace");
+  if (st) return st;
+  const int T = p->d.max_traces;
+  std::vector<float> sb(T);
+  std::vector<int32_t> ns(T), ge(T), gh(T);
+  HIP_TRY(p, hipStreamSynchronize(S(stream)), "sync");
+  HIP_TRY(p, hipMemcpy(sb.data(), p->ws + p->L.sbar, 4 * (size_t)T, hipMemcpyDeviceToHost), "state read");
+  HIP_TRY(p, hipMemcpy(ns.data(), p->ws + p->L.nscore, 4 * (size_t)T, hipMemcpyDeviceToHost), "state read");
+  HIP_TRY(p, hipMemcpy(ge.data(), p->ws + p->L.gen, 4 * (size_t)T, hipMemcpyDeviceToHost), "state read");
+  HIP_TRY(p, hipMemcpy(gh.data(), p->ws + p->L.ghost, 4 * (size_t)T, hipMemcpyDeviceToHost), "state read");
+  for (int i = 0; i < n; ++i) {
+    const int t = ids[i];
+    if (sbar_out) sbar_out[i] = sb[t];
+    if (nscore_out) nscore_out[i] = ns[t];
+    if (gen_out) gen_out[i] = ge[t];
+    if (ghost_out) ghost_out[i] = gh[t];
+  }
+  return GAMBIT_OK;
+}
+
 gambit_status gambit_pool_check(gambit_pool* p, void* stream) {
   if (!p) return GAMBIT_ERR_INVALID;
   hipStream_t s = S(stream);
@@ -863,7 +1054,15 @@ gambit_status gambit_pool_check(gambit_pool* p, void* stream) {
   HIP_TRY(p, hipMemcpy(ref.data(), p->d.refcount, 4 * (size_t)NB, hipMemcpyDeviceToHost), "check read");
   HIP_TRY(p, hipMemcpy(err.data(), p->ws + p->L.err, 4, hipMemcpyDeviceToHost), "check read");
   HIP_TRY(p, hipMemcpy(bits.data(), p->ws + p->L.freebits, 4 * bits.size(), hipMemcpyDeviceToHost), "check read");
+  std::vector<int32_t> nsc(T), gen(T), gh(T);
+  HIP_TRY(p, hipMemcpy(nsc.data(), p->ws + p->L.nscore, 4 * (size_t)T, hipMemcpyDeviceToHost), "check read");
+  HIP_TRY(p, hipMemcpy(gen.data(), p->ws + p->L.gen, 4 * (size_t)T, hipMemcpyDeviceToHost), "check read");
+  HIP_TRY(p, hipMemcpy(gh.data(), p->ws + p->L.ghost, 4 * (size_t)T, hipMemcpyDeviceToHost), "check read");
   if (err[0]) return fail(p, GAMBIT_ERR_DEVICE, "device error word 0x%x", err[0]);
+  for (int t = 0; t < T; ++t)
+    if (nsc[t] != p->nscore[t] || gen[t] != p->gen[t] || (gh[t] != 0) != (p->ghost[t] != 0))
+      return fail(p, GAMBIT_ERR_DEVICE, "tournament state of trace %d: device (%d, %d, %d), host (%d, %d, %d)", t,
+                  nsc[t], gen[t], gh[t], p->nscore[t], p->gen[t], (int)p->ghost[t]);
   for (int t = 0; t < T; ++t) {
     if (len[t] != p->seq_len[t]) return fail(p, GAMBIT_ERR_DEVICE, "seq_len[%d]: device %d, host %d", t, len[t], p->seq_len[t]);
     const auto& row = p->table[t];

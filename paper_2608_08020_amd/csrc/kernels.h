@@ -53,6 +53,13 @@ struct DevPool {
   uint32_t* freebits;     // [nwords], bit set = block free
   int32_t* alloc_list;    // [num_blocks] scratch of the allocator
   int32_t* err;           // device error word
+  // tournament state per trace slot (Alg. 1): running mean score, scored
+  // thoughts, tokens generated since creation, ghost flag (evicted by the
+  // scheduler, still in the tree view)
+  float* sbar;            // [max_traces]
+  int32_t* nscore;        // [max_traces]
+  int32_t* gen;           // [max_traces]
+  int32_t* ghost;         // [max_traces]
   int32_t num_blocks, nwords, max_traces, max_blocks;
   int32_t Hq, Hkv, g;
   int32_t esize;          // bytes per cache element (2 bf16, 1 fp8)
@@ -87,11 +94,16 @@ struct AttnLaunch {
 hipError_t launch_pool_init(const DevPool& P, hipStream_t s);
 // m requests (trace ids, token counts) on the device; uniform_ntok >= 0
 // overrides the counts.  fp8 pools give new blocks the scale `new_scale`.
+// `generated`: the tokens are a decode step's (they count towards GenLen).
 hipError_t launch_alloc(const DevPool& P, const int32_t* req_trace, const int32_t* req_ntok,
-                        int32_t uniform_ntok, int32_t m, float new_scale, hipStream_t s);
+                        int32_t uniform_ntok, int32_t m, float new_scale, bool generated, hipStream_t s);
 hipError_t launch_write(const DevPool& P, int32_t trace, int32_t pos0, int32_t n, const void* k,
                         const void* v, const float* started_scales, hipStream_t s);
-hipError_t launch_free(const DevPool& P, const int32_t* ids, int32_t n, hipStream_t s);
+// Free the listed traces' blocks.  kFreeEnd: the trace ends (its tournament
+// state is cleared, a ghost leaves the tree view; rows may be empty);
+// kFreeEvict: the scheduler evicts it (it becomes a ghost, its score stays).
+enum : int32_t { kFreeEnd = 0, kFreeEvict = 1 };
+hipError_t launch_free(const DevPool& P, const int32_t* ids, int32_t n, int32_t mode, hipStream_t s);
 // pairs: device [n][2] (child, parent).  req_trace/req_ntok: scratch [n].
 hipError_t launch_fork(const DevPool& P, const int32_t* pairs, int32_t n, int32_t* req_trace,
                        int32_t* req_ntok, hipStream_t s);
@@ -117,6 +129,32 @@ struct ProbeLaunch {
 hipError_t launch_probe_rank(const ProbeLaunch& L, hipStream_t s);
 hipError_t launch_rank_topk(int32_t n, const int32_t* ids, const float* scores, int32_t keep,
                             int32_t* keep_out, hipStream_t s);
+
+// Thought scores of the listed traces and their running means (Alg. 1
+// Generate): f = sigmoid(h . w + b), n += 1, s_bar += (f - s_bar) / n.
+struct ScoreLaunch {
+  const int32_t* list;      // device [n] trace ids
+  int32_t n;
+  const uint16_t* h;        // [n][Dh] bf16
+  int32_t Dh;
+  const float* w;
+  float b;
+  float* scores_out;        // [n]
+};
+hipError_t launch_score_update(const DevPool& P, const ScoreLaunch& L, hipStream_t s);
+
+// The eviction choice (Alg. 1 Schedule): out[0] = the listed trace ranked
+// last by (s_bar descending, id ascending).
+hipError_t launch_evict_pick(const DevPool& P, const int32_t* list, int32_t n, int32_t* out,
+                             hipStream_t s);
+
+// The tournament plan over the tree view (Alg. 1 Tournament, Eqs. 2-3).
+// out (device, kTournHeader + 3 * max_traces ints): header {case, N,
+// pruned, children, vacant}, then the pruned ids ascending (max_traces
+// entries), then (child, parent) pairs (2 * max_traces entries).
+constexpr int kTournHeader = 8;
+hipError_t launch_tournament(const DevPool& P, int32_t capacity, int32_t swap_k, int32_t warmup,
+                             int32_t* out, int32_t* ranked_out, hipStream_t s);
 
 constexpr int kMaxRank = 4096;  // largest population the in-LDS ranking handles
 

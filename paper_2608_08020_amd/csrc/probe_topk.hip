@@ -29,6 +29,29 @@ __device__ inline uint32_t orderable(float f) {
 __device__ inline float bf16_lo(uint32_t x) { return __builtin_bit_cast(float, x << 16); }
 __device__ inline float bf16_hi(uint32_t x) { return __builtin_bit_cast(float, x & 0xFFFF0000u); }
 
+// h . w over Dh (a multiple of 8) by one wave: each lane takes 8
+// consecutive elements per step (128-bit loads), then a shuffle reduction;
+// every lane returns the sum.
+__device__ inline float probe_dot(const uint16_t* h, const float* w, int Dh, int lane) {
+  float acc = 0.f;
+  for (int d = lane * 8; d < Dh; d += 64 * 8) {
+    const uint4 hv = *reinterpret_cast<const uint4*>(h + d);
+    const float4 w0 = *reinterpret_cast<const float4*>(w + d);
+    const float4 w1 = *reinterpret_cast<const float4*>(w + d + 4);
+    acc = fmaf(bf16_lo(hv.x), w0.x, acc);
+    acc = fmaf(bf16_hi(hv.x), w0.y, acc);
+    acc = fmaf(bf16_lo(hv.y), w0.z, acc);
+    acc = fmaf(bf16_hi(hv.y), w0.w, acc);
+    acc = fmaf(bf16_lo(hv.z), w1.x, acc);
+    acc = fmaf(bf16_hi(hv.z), w1.y, acc);
+    acc = fmaf(bf16_lo(hv.w), w1.z, acc);
+    acc = fmaf(bf16_hi(hv.w), w1.w, acc);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  return acc;
+}
+
 // Sort keys[0..N) descending (N a power of two) with all threads of the block.
 __device__ void bitonic_desc(uint64_t* keys, int N) {
   for (int k = 2; k <= N; k <<= 1) {
@@ -98,24 +121,7 @@ __global__ __launch_bounds__(kProbeThreads) void probe_rank_kernel(ProbeLaunch L
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int i = blockIdx.x * (kProbeThreads / 64) + wave;
   if (i < L.n) {
-    const uint16_t* h = L.h + (size_t)i * L.Dh;
-    float acc = 0.f;
-    // Dh is a multiple of 8: each lane takes 8 consecutive elements per step
-    for (int d = lane * 8; d < L.Dh; d += 64 * 8) {
-      const uint4 hv = *reinterpret_cast<const uint4*>(h + d);
-      const float4 w0 = *reinterpret_cast<const float4*>(L.w + d);
-      const float4 w1 = *reinterpret_cast<const float4*>(L.w + d + 4);
-      acc = fmaf(bf16_lo(hv.x), w0.x, acc);
-      acc = fmaf(bf16_hi(hv.x), w0.y, acc);
-      acc = fmaf(bf16_lo(hv.y), w0.z, acc);
-      acc = fmaf(bf16_hi(hv.y), w0.w, acc);
-      acc = fmaf(bf16_lo(hv.z), w1.x, acc);
-      acc = fmaf(bf16_hi(hv.z), w1.y, acc);
-      acc = fmaf(bf16_lo(hv.w), w1.z, acc);
-      acc = fmaf(bf16_hi(hv.w), w1.w, acc);
-    }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    const float acc = probe_dot(L.h + (size_t)i * L.Dh, L.w, L.Dh, lane);
     if (lane == 0) {
       const float z = acc + L.b;
       L.scores_out[i] = 1.f / (1.f + expf(-z));
@@ -143,7 +149,178 @@ __global__ __launch_bounds__(kProbeThreads) void rank_topk_kernel(int n, const i
   rank_and_plan(n, ids, scores, false, keep, 0, keep_out, nullptr, nullptr);
 }
 
+// ------------------------------------------------------------- tournament --
+// The full tournament of Alg. 1 keeps per trace slot a running mean score
+// s_bar over its thoughts, the tokens it has generated since its creation
+// (GenLen) and a ghost flag (Sec. 4.2: evicted by the scheduler, no KV, no
+// tokens, still in the tree view).
+
+constexpr int kTournThreads = 256;
+
+// Exclusive scan of one int per thread over the 256 threads.
+__device__ int scan256(int v, int* total) {
+  __shared__ int wsum[kTournThreads / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int x = __shfl_up(incl, off);
+    if (lane >= off) incl += x;
+  }
+  if (lane == 63) wsum[w] = incl;
+  __syncthreads();
+  int before = 0, all = 0;
+#pragma unroll
+  for (int k = 0; k < kTournThreads / 64; ++k) {
+    before += k < w ? wsum[k] : 0;
+    all += wsum[k];
+  }
+  __syncthreads();
+  *total = all;
+  return before + incl - v;
+}
+
+__device__ inline int key_id(uint64_t key) { return (int)~(uint32_t)key; }
+
+// One wave per listed trace: the thought score f = sigmoid(h . w + b), then
+// the running mean over the trace's thoughts (Alg. 1 Generate).
+__global__ __launch_bounds__(kProbeThreads) void score_update_kernel(DevPool P, ScoreLaunch L) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int i = blockIdx.x * (kProbeThreads / 64) + wave;
+  if (i >= L.n) return;
+  const float acc = probe_dot(L.h + (size_t)i * L.Dh, L.w, L.Dh, lane);
+  if (lane == 0) {
+    const float f = 1.f / (1.f + expf(-(acc + L.b)));
+    const int t = L.list[i];
+    const int n = P.nscore[t] + 1;
+    P.sbar[t] += (f - P.sbar[t]) / (float)n;
+    P.nscore[t] = n;
+    L.scores_out[i] = f;
+  }
+}
+
+// The listed trace ranked last by (s_bar descending, id ascending): the
+// smallest rank key.
+__global__ __launch_bounds__(kTournThreads) void evict_pick_kernel(DevPool P, const int32_t* list, int n,
+                                                                   int32_t* out) {
+  __shared__ uint64_t wmin[kTournThreads / 64];
+  uint64_t mn = ~0ull;
+  for (int i = threadIdx.x; i < n; i += kTournThreads) {
+    const int t = list[i];
+    const uint64_t k = rank_key(P.sbar[t], t);
+    mn = k < mn ? k : mn;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint64_t o = __shfl_xor(mn, off);
+    mn = o < mn ? o : mn;
+  }
+  if ((threadIdx.x & 63) == 0) wmin[threadIdx.x >> 6] = mn;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int k = 1; k < kTournThreads / 64; ++k) mn = wmin[k] < mn ? wmin[k] : mn;
+    out[0] = key_id(mn);
+  }
+}
+
+// One workgroup plans a tournament round over the tree view (every slot
+// that is running or a ghost): rank by (s_bar descending, id ascending);
+// N < C: Case 1, branch the top min(C - N, |B|) eligible traces (Eq. 2);
+// N >= C: Case 2, prune the bottom min(K, N), branch the top min(K, |B|)
+// eligible traces that were not pruned (Eq. 3).  Eligible: running (not a
+// ghost) with GenLen >= w.  Children take the lowest vacant slots
+// (ascending) after the pruning, one per parent in rank order.  The plan is
+// only written out; the host applies it after checking it.
+__global__ __launch_bounds__(kTournThreads) void tournament_kernel(DevPool P, int C, int K, int w,
+                                                                   int32_t* out, int32_t* ranked_out) {
+  __shared__ uint64_t keys[kMaxRank];
+  __shared__ uint8_t pruned[kMaxRank];
+  const int T = P.max_traces;
+  int Np2 = 1;
+  while (Np2 < T) Np2 <<= 1;
+  int nact = 0;
+  for (int i = threadIdx.x; i < Np2; i += kTournThreads) {
+    const bool act = i < T && (P.seq_len[i] > 0 || P.ghost[i] != 0);
+    keys[i] = act ? rank_key(P.sbar[i], i) : 0;  // inactive slots sort last
+    pruned[i] = 0;
+    nact += act;
+  }
+  int N = 0;
+  scan256(nact, &N);  // also a barrier
+  bitonic_desc(keys, Np2);
+  const int kase = N == 0 ? 0 : (N < C ? 1 : 2);
+  const int npr = kase == 2 ? min(K, N) : 0;
+  for (int r = N - npr + threadIdx.x; r < N; r += kTournThreads) pruned[key_id(keys[r])] = 1;
+  __syncthreads();
+  int32_t* out_pruned = out + kTournHeader;
+  int32_t* out_pairs = out_pruned + T;
+  const int per = (T + kTournThreads - 1) / kTournThreads;
+  const int r0 = threadIdx.x * per, r1 = min(r0 + per, T);
+  // parents: eligible ranks in order
+  auto eligible = [&](int r) {
+    if (r >= N) return false;
+    const int t = key_id(keys[r]);
+    return !pruned[t] && P.seq_len[t] > 0 && P.ghost[t] == 0 && P.gen[t] >= w;
+  };
+  int cnt = 0;
+  for (int r = r0; r < r1; ++r) cnt += eligible(r);
+  int nb = 0;
+  int at = scan256(cnt, &nb);
+  const int m = kase == 1 ? min(C - N, nb) : (kase == 2 ? min(K, nb) : 0);
+  for (int r = r0; r < r1; ++r)
+    if (eligible(r)) {
+      if (at < m) out_pairs[2 * at + 1] = key_id(keys[r]);
+      ++at;
+    }
+  // children: the lowest vacant slots after the pruning
+  auto vacant = [&](int t) { return (P.seq_len[t] == 0 && P.ghost[t] == 0) || pruned[t]; };
+  cnt = 0;
+  for (int t = r0; t < r1; ++t) cnt += vacant(t);
+  int nvac = 0;
+  at = scan256(cnt, &nvac);
+  for (int t = r0; t < r1; ++t)
+    if (vacant(t)) {
+      if (at < m) out_pairs[2 * at] = t;
+      ++at;
+    }
+  // the pruned ids, ascending
+  cnt = 0;
+  for (int t = r0; t < r1; ++t) cnt += pruned[t];
+  int np = 0;
+  at = scan256(cnt, &np);
+  for (int t = r0; t < r1; ++t)
+    if (pruned[t]) out_pruned[at++] = t;
+  if (ranked_out)
+    for (int r = threadIdx.x; r < N; r += kTournThreads) ranked_out[r] = key_id(keys[r]);
+  if (threadIdx.x == 0) {
+    out[0] = kase;
+    out[1] = N;
+    out[2] = npr;
+    out[3] = m;
+    out[4] = nvac;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_score_update(const DevPool& P, const ScoreLaunch& L, hipStream_t s) {
+  if (L.n <= 0) return hipSuccess;
+  const int wpb = kProbeThreads / 64;
+  hipLaunchKernelGGL(score_update_kernel, dim3((L.n + wpb - 1) / wpb), dim3(kProbeThreads), 0, s, P, L);
+  return hipGetLastError();
+}
+
+hipError_t launch_evict_pick(const DevPool& P, const int32_t* list, int32_t n, int32_t* out, hipStream_t s) {
+  hipLaunchKernelGGL(evict_pick_kernel, dim3(1), dim3(kTournThreads), 0, s, P, list, n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_tournament(const DevPool& P, int32_t capacity, int32_t swap_k, int32_t warmup,
+                             int32_t* out, int32_t* ranked_out, hipStream_t s) {
+  hipLaunchKernelGGL(tournament_kernel, dim3(1), dim3(kTournThreads), 0, s, P, capacity, swap_k, warmup,
+                     out, ranked_out);
+  return hipGetLastError();
+}
 
 hipError_t launch_probe_rank(const ProbeLaunch& L, hipStream_t s) {
   const int wpb = kProbeThreads / 64;

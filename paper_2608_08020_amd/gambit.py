@@ -46,6 +46,11 @@ class PoolDesc(ctypes.Structure):
                 ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
 
 
+class Round(ctypes.Structure):
+    _fields_ = [("case_taken", ctypes.c_int32), ("n_active", ctypes.c_int32),
+                ("n_pruned", ctypes.c_int32), ("n_children", ctypes.c_int32)]
+
+
 class Stats(ctypes.Structure):
     _fields_ = [("total_tokens", ctypes.c_int64), ("unique_tokens", ctypes.c_int64),
                 ("unique_blocks", ctypes.c_int64), ("table_entries", ctypes.c_int64),
@@ -58,7 +63,8 @@ EXPORTS = ["gambit_workspace_size", "gambit_pool_create", "gambit_pool_destroy",
            "gambit_kv_write", "gambit_kv_fork", "gambit_kv_free", "gambit_decode_attn",
            "gambit_score_prune_branch", "gambit_rank_topk", "gambit_pool_check",
            "gambit_plan_stats", "gambit_seq_len", "gambit_free_blocks", "gambit_status_str",
-           "gambit_last_error", "gambit_profile_begin", "gambit_profile_end"]
+           "gambit_last_error", "gambit_profile_begin", "gambit_profile_end", "gambit_score_update",
+           "gambit_evict", "gambit_tournament", "gambit_trace_state"]
 
 
 def lib() -> ctypes.CDLL:
@@ -88,6 +94,10 @@ def lib() -> ctypes.CDLL:
         "gambit_last_error": (ctypes.c_char_p, [vp]),
         "gambit_profile_begin": (i32, [vp, i32]),
         "gambit_profile_end": (i32, [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)]),
+        "gambit_score_update": (i32, [vp, i32, vp, vp, i32, vp, f32, vp, vp]),
+        "gambit_evict": (i32, [vp, i32, vp, vp, vp]),
+        "gambit_tournament": (i32, [vp, i32, i32, i32, ctypes.POINTER(Round), vp, vp, vp, vp]),
+        "gambit_trace_state": (i32, [vp, i32, vp, vp, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -245,6 +255,48 @@ class Pool:
                                                     _dev(scores), _dev(keep_out), _dev(pairs),
                                                     _stream(stream)), "score_prune_branch")
         return scores, keep_out, pairs[:n - keep]
+
+    # -- the full tournament of Alg. 1
+    def score_update(self, ids, h: torch.Tensor, w: torch.Tensor, b: float, stream=None) -> torch.Tensor:
+        """gambit_score_update: thought scores f [n] (device); running means update in the pool."""
+        ids = _host_i32(ids)
+        n = ids.size
+        scores = torch.empty(max(n, 1), dtype=torch.float32, device=h.device)
+        _dev(h, torch.bfloat16)
+        self._check(lib().gambit_score_update(self._h, n, _ptr(ids), _dev(h), h.shape[1] if n else 8,
+                                              _dev(w, torch.float32), float(b), _dev(scores),
+                                              _stream(stream)), "score_update")
+        return scores[:n]
+
+    def evict(self, ids, stream=None) -> int:
+        """gambit_evict: the listed running trace of lowest running score becomes a ghost."""
+        ids = _host_i32(ids)
+        v = np.zeros(1, np.int32)
+        self._check(lib().gambit_evict(self._h, ids.size, _ptr(ids), _ptr(v), _stream(stream)), "evict")
+        return int(v[0])
+
+    def tournament(self, capacity: int, swap_k: int, warmup: int, want_ranked: bool = False, stream=None):
+        """gambit_tournament: (case, n_active, pruned ids, [(child, parent)], ranked ids or None)."""
+        r = Round()
+        pruned = np.zeros(max(swap_k, 1), np.int32)
+        pairs = np.zeros((self.max_traces, 2), np.int32)
+        ranked = torch.empty(self.max_traces, dtype=torch.int32, device="cuda") if want_ranked else None
+        self._check(lib().gambit_tournament(self._h, capacity, swap_k, warmup, ctypes.byref(r), _ptr(pruned),
+                                            _ptr(pairs), None if ranked is None else _dev(ranked),
+                                            _stream(stream)), "tournament")
+        pl = [(int(c), int(p)) for c, p in pairs[:r.n_children]]
+        rk = ranked[:r.n_active].cpu().numpy().tolist() if ranked is not None else None
+        return r.case_taken, r.n_active, pruned[:r.n_pruned].tolist(), pl, rk
+
+    def trace_state(self, ids, stream=None):
+        """gambit_trace_state: (s_bar fp32, scored thoughts, GenLen, ghost) per listed slot."""
+        ids = _host_i32(ids)
+        n = ids.size
+        sb, ns, ge, gh = (np.zeros(n, np.float32), np.zeros(n, np.int32), np.zeros(n, np.int32),
+                          np.zeros(n, np.int32))
+        self._check(lib().gambit_trace_state(self._h, n, _ptr(ids), _ptr(sb), _ptr(ns), _ptr(ge), _ptr(gh),
+                                             _stream(stream)), "trace_state")
+        return sb, ns, ge, gh
 
     def pool_check(self, stream=None):
         self._check(lib().gambit_pool_check(self._h, _stream(stream)), "pool_check")
