@@ -17,7 +17,10 @@ every input already resident in HBM.  `roofline` prices the dominant kernel
 population references read once, plus queries, block-table entries and the
 step's append that the same launch performs (new K/V read and written) - over
 its event-timed average duration.  `cpu_baseline` times the CPU oracle on a
-bounded sample of the same workload.
+bounded sample of the same workload.  `tournament` times rounds of the full
+tournament of Alg. 1 (C = 256, K = 16: running-mean scoring, an eviction
+into a ghost every other round, rank / prune / branch) and the oracle's
+rounds beside them.
 """
 from __future__ import annotations
 
@@ -88,6 +91,73 @@ def cpu_baseline(wl, budget_s: float):
                        f"{spent:.1f} s; {len(os.sched_getaffinity(0))} host cores visible")}
 
 
+def tournament_rounds(rounds: int = 24):
+    """The full tournament of Alg. 1 at C = 256, K = 16 (Sec. 5.1), Qwen3-8B
+    layer shape: per round every running trace is scored (running means), the
+    scheduler evicts one trace into a ghost every other round, and the
+    tournament ranks, prunes and branches (one readback).  Returns GPU wall
+    microseconds per round (median) and the oracle's per-round time on the
+    host for the same round sizes."""
+    import numpy as np
+    import torch
+
+    from oracle.pool import PoolModel
+    from oracle.tournament import TournamentModel
+    from paper_2608_08020_amd.gambit import Pool
+    from workload.tournament import TOURNAMENT_C256, TournamentWorkload
+
+    c = TOURNAMENT_C256
+    wl = TournamentWorkload(c)
+    p = Pool(num_blocks=c.num_blocks, num_q_heads=c.n_q_heads, num_kv_heads=c.n_kv_heads, max_traces=c.slots,
+             max_blocks_per_trace=c.max_blocks_per_trace)
+    lens = wl.prompt_lengths()
+    roots = list(range(c.roots))
+    p.kv_alloc(roots, lens)            # prompt contents do not enter the bookkeeping timed here
+    q = torch.randn((c.roots, c.n_q_heads, c.head_dim), device="cuda").to(torch.bfloat16)
+    kv = torch.randn((c.roots, c.n_kv_heads, c.head_dim), device="cuda").to(torch.bfloat16)
+    for _ in range(c.warmup):          # generate past the warm-up so traces are eligible
+        p.decode_attn(roots, q, kv, kv)
+    w, b = wl.probe_weights()
+    wd = torch.from_numpy(w).cuda()
+    h = torch.from_numpy(wl.round_h(0, c.slots).view(np.int16)).view(torch.bfloat16).cuda()
+    om = TournamentModel(PoolModel(num_blocks=c.num_blocks, n_kv_heads=c.n_kv_heads, head_dim=c.head_dim,
+                                   kv_dtype="bf16", max_traces=c.slots, max_blocks_per_trace=c.max_blocks_per_trace))
+    om.pool.alloc(roots, lens)
+    for _ in range(c.warmup):
+        om.decoded(roots)
+    rng = np.random.default_rng(0)
+    gpu_us, cpu_us, sizes = [], [], []
+    for r in range(rounds):
+        running = [t for t in range(c.slots) if p.seq_len_of(t) > 0]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        p.score_update(running, h[:len(running)], wd, b)
+        if r % 2:
+            p.evict(running)
+        case, n_act, pruned, pairs, _ = p.tournament(c.capacity, c.swap_k, c.warmup)
+        torch.cuda.synchronize()
+        gpu_us.append((time.perf_counter() - t0) * 1e6)
+        sizes.append((len(running), len(pruned), len(pairs)))
+        # the oracle, same round shape (its own scores), timed on the host
+        orun = om.scheduler_view()
+        f = rng.random(len(orun))
+        t0 = time.perf_counter()
+        om.score_update(orun, f)
+        if r % 2:
+            om.evict(orun)
+        om.tournament(c.capacity, c.swap_k, c.warmup)
+        cpu_us.append((time.perf_counter() - t0) * 1e6)
+    g = sorted(gpu_us[2:])
+    return {"workload": c.name, "capacity": c.capacity, "swap_k": c.swap_k, "rounds": rounds,
+            "round_us_median": round(g[len(g) // 2], 1), "round_us_max": round(g[-1], 1),
+            "mean_running": round(float(np.mean([x[0] for x in sizes])), 1),
+            "mean_pruned": round(float(np.mean([x[1] for x in sizes])), 2),
+            "mean_branched": round(float(np.mean([x[2] for x in sizes])), 2),
+            "cpu_oracle_round_us_median": round(sorted(cpu_us)[len(cpu_us) // 2], 1),
+            "note": "score update + eviction (every other round) + tournament incl. its readback, host check, "
+                    "prune and branch kernels; bound by latency (single-workgroup plan, one device-to-host copy)"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -96,6 +166,7 @@ def main():
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-tournament", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path shards by "
@@ -190,6 +261,9 @@ def main():
         "step_hbm_GBps": round(sum(alg_bytes) / wall / 1e9, 1),
         "event_ms_per_step": round(ev_ms / K, 4),
     }
+    if not args.no_tournament:
+        log("timing tournament rounds")
+        res["tournament"] = tournament_rounds()
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
         res["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
