@@ -33,6 +33,9 @@ Contents and the passages each part follows:
                   (Eq. 2), Case 2 swap (Eq. 3), scheduler eviction of the
                   lowest-scoring running trace into a ghost that keeps its
                   place in the tree view (Sec. 4.2).
+* ``mlp``       - the 2-layer MLP scorer sigmoid(w2 . act(W1 h + b1) + b2)
+                  (the paper's main-evaluation scorer family, Sec. 5.1;
+                  dimensions, activation and weights are parameters).
 
 Parity status: every function is pinned by the ``-m "not gpu"`` tests
 (closed forms, library special cases, invariants, brute force, exhaustive
