@@ -158,6 +158,45 @@ def tournament_rounds(rounds: int = 24):
                     "prune and branch kernels; bound by latency (single-workgroup plan, one device-to-host copy)"}
 
 
+def mlp_measure(reps: int = 20):
+    """The fused 2-layer MLP scorer on the 512-trace boundary (Dh 4096, hidden
+    1024, ReLU) with the fused top-128: event-timed average per launch, its
+    flops and bytes, and the oracle's time for the same scoring on the host."""
+    import numpy as np
+    import torch
+
+    from oracle.formats import bf16_to_f64
+    from oracle.mlp import mlp_scores
+    from paper_2608_08020_amd.gambit import mlp_score
+    from workload.mlp import MLP_512, hidden_states, weights
+
+    c = MLP_512
+    W1, b1, w2, b2 = weights(c)
+    h = hidden_states(c)
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()  # noqa: E731
+    hd, w1d, b1d, w2d = bf(h), bf(W1), torch.from_numpy(b1).cuda(), torch.from_numpy(w2).cuda()
+    ids = torch.arange(c.n, dtype=torch.int32, device="cuda")
+    for _ in range(3):
+        mlp_score(hd, w1d, b1d, w2d, b2, c.act, ids=ids, keep=128)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        mlp_score(hd, w1d, b1d, w2d, b2, c.act, ids=ids, keep=128)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    flops = 2.0 * c.n * c.dim * c.hidden
+    nbytes = 2.0 * (c.n * c.dim + c.hidden * c.dim)
+    t0 = time.perf_counter()
+    mlp_scores(bf16_to_f64(h), bf16_to_f64(W1), b1.astype(np.float64), w2.astype(np.float64), b2, c.act)
+    cpu_us = (time.perf_counter() - t0) * 1e6
+    return {"workload": c.name, "us_per_call": round(us, 2), "tflops": round(flops / us / 1e6, 2),
+            "gbps": round(nbytes / us / 1e3, 1), "mfma_peak_frac_bf16": round(flops / us / 1e6 / 2500.0, 4),
+            "hbm_peak_frac": round(nbytes / us / 1e3 / PEAK_HBM_GBPS, 4), "cpu_oracle_us": round(cpu_us, 1),
+            "note": "includes the finishing launch (partial-logit sums, sigmoid, top-128 rank) and host launch gaps"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -264,6 +303,8 @@ def main():
     if not args.no_tournament:
         log("timing tournament rounds")
         res["tournament"] = tournament_rounds()
+        log("timing the MLP scorer")
+        res["mlp_scorer"] = mlp_measure()
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
         res["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)

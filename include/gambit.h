@@ -261,6 +261,45 @@ gambit_status gambit_tournament(gambit_pool* pool, int32_t capacity, int32_t swa
                                 gambit_round* round_out, int32_t* pruned_out, int32_t* child_parent_out,
                                 int32_t* ranked_out, void* stream);
 
+/* Running means from thought scores computed elsewhere (for instance by
+ * gambit_mlp_score): as gambit_score_update with f given.
+ *   trace_ids host [n], running traces, distinct;  f device [n] fp32 */
+gambit_status gambit_record_scores(gambit_pool* pool, int32_t n, const int32_t* trace_ids, const float* f,
+                                   void* stream);
+
+/*
+ * The 2-layer MLP scorer of the paper's main evaluation (STEP's off-the-shelf
+ * probe on the thought-boundary hidden state, Sec. 4.1 and Sec. 5.1; the
+ * paper gives no dimensions, activation or weights, so they are parameters):
+ *     f(h) = 1 / (1 + exp(-(w2 . act(W1 h + b1) + b2)))
+ * with act = ReLU or GELU (x * Phi(x), erf form).  W1 h runs on the bf16
+ * matrix cores with fp32 accumulation; bias, activation and w2 are applied in
+ * the same tiles; the tiles' partial logits are summed in a fixed order.
+ */
+enum { GAMBIT_ACT_RELU = 0, GAMBIT_ACT_GELU = 1 };
+typedef struct {
+  int32_t dim;                   /* Dh, a multiple of 128                    */
+  int32_t hidden;                /* H1, a multiple of 64                     */
+  int32_t activation;            /* GAMBIT_ACT_*                             */
+  const void* w1;                /* device [hidden][dim] bf16                */
+  const float* b1;               /* device [hidden]                          */
+  const float* w2;               /* device [hidden]                          */
+  float b2;
+} gambit_mlp;
+
+/* Bytes of device workspace gambit_mlp_score needs (0: invalid sizes). */
+size_t gambit_mlp_workspace_size(int32_t n, int32_t hidden);
+
+/* Scores of n hidden states (n <= 4096).
+ *   h           device [n][dim] bf16;  scores_out device [n] fp32
+ *   keep > 0:   also rank (score descending, id ascending) and write the top
+ *               `keep` ids to keep_out (device [keep]); trace_ids device [n]
+ *   workspace   device, >= gambit_mlp_workspace_size(n, hidden) bytes
+ * Stateless; enqueued on `stream`. */
+gambit_status gambit_mlp_score(int32_t n, const void* h, const gambit_mlp* mlp, float* scores_out,
+                               const int32_t* trace_ids, int32_t keep, int32_t* keep_out, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
 /* Tournament state of the listed slots (host outputs, any may be NULL);
  * synchronises `stream`.  sbar fp32, nscore/gen int32, ghost 0/1. */
 gambit_status gambit_trace_state(gambit_pool* pool, int32_t n, const int32_t* trace_ids, float* sbar_out,

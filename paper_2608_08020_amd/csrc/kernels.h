@@ -158,4 +158,28 @@ hipError_t launch_tournament(const DevPool& P, int32_t capacity, int32_t swap_k,
 
 constexpr int kMaxRank = 4096;  // largest population the in-LDS ranking handles
 
+// The 2-layer MLP scorer f = sigmoid(w2 . act(W1 h + b1) + b2), fused:
+// tiles of 16 hidden states x 64 hidden units on the bf16 matrix cores with
+// bias, activation and the w2 product applied in the tile, then one
+// workgroup sums the tiles' partial logits in a fixed order, applies the
+// sigmoid and (keep > 0) ranks the top `keep` ids.
+constexpr int kMlpTileT = 16, kMlpTileH = 64;
+struct MlpLaunch {
+  int32_t n, dim, hidden, act;   // act: 0 ReLU, 1 GELU (erf)
+  const uint16_t* h;             // [n][dim] bf16
+  const uint16_t* w1;            // [hidden][dim] bf16
+  const float* b1;               // [hidden]
+  const float* w2;               // [hidden]
+  float b2;
+  float* parts;                  // [hidden / 64][n] partial logits
+  float* scores_out;             // [n]
+  const int32_t* ids;            // [n] or NULL (ranking only)
+  int32_t keep;
+  int32_t* keep_out;             // [keep]
+};
+hipError_t launch_mlp_score(const MlpLaunch& L, hipStream_t s);
+// Running means from thought scores computed elsewhere (f device [n]).
+hipError_t launch_record_scores(const DevPool& P, const int32_t* list, const float* f, int32_t n,
+                                hipStream_t s);
+
 }  // namespace gambit

@@ -301,7 +301,118 @@ __global__ __launch_bounds__(kTournThreads) void tournament_kernel(DevPool P, in
   }
 }
 
+// ------------------------------------------------------------- MLP scorer --
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ inline float mlp_act(float x, int act) {
+  return act == 0 ? fmaxf(x, 0.f) : 0.5f * x * (1.f + erff(x * 0.70710678118654752f));
+}
+
+// One workgroup: hidden states t0 .. t0 + 15 x hidden units h0 .. h0 + 63.
+// Z^T-free form: D[trace][unit] = sum_k h[trace][k] W1[unit][k] on
+// v_mfma_f32_16x16x32_bf16 (A = 16 hidden states x 32 k, B = 32 k x 16
+// units; each operand one 16-byte load per lane).  The four waves take the
+// four quarters of k; their sums meet in LDS.  Lane (q, j) of an output
+// block holds the traces 4q .. 4q + 3 of unit j.
+__global__ __launch_bounds__(256) void mlp_tile_kernel(MlpLaunch L) {
+  __shared__ f32x4 red[4][4][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int q = lane >> 4, j = lane & 15;
+  const int t0 = blockIdx.x * kMlpTileT, h0 = blockIdx.y * kMlpTileH;
+  const int tr = t0 + j;
+  const int kq = L.dim / 4, k0 = wave * kq;
+  const bf16x8 zero = {};
+  const uint16_t* hrow = L.h + (size_t)min(tr, L.n - 1) * L.dim + 8 * q + k0;
+  const uint16_t* wrow = L.w1 + (size_t)(h0 + j) * L.dim + 8 * q + k0;
+  const size_t wstep = (size_t)16 * L.dim;  // the next block of 16 units
+  f32x4 acc[4] = {};
+  int k = 0;
+  for (; k + 128 <= kq; k += 128) {  // four 32-wide steps per pass, loads first
+    bf16x8 a[4], b[4][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      a[u] = tr < L.n ? *reinterpret_cast<const bf16x8*>(hrow + k + 32 * u) : zero;
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb) b[u][bb] = *reinterpret_cast<const bf16x8*>(wrow + bb * wstep + k + 32 * u);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb) acc[bb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u], b[u][bb], acc[bb], 0, 0, 0);
+  }
+  for (; k < kq; k += 32) {  // dim is a multiple of 128: the quarter's remaining 32-wide steps
+    const bf16x8 a = tr < L.n ? *reinterpret_cast<const bf16x8*>(hrow + k) : zero;
+#pragma unroll
+    for (int bb = 0; bb < 4; ++bb)
+      acc[bb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, *reinterpret_cast<const bf16x8*>(wrow + bb * wstep + k),
+                                                        acc[bb], 0, 0, 0);
+  }
+#pragma unroll
+  for (int bb = 0; bb < 4; ++bb) red[wave][bb][lane] = acc[bb];
+  __syncthreads();
+  if (wave != 0) return;
+  float y[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int bb = 0; bb < 4; ++bb) {
+    const f32x4 z = red[0][bb][lane] + red[1][bb][lane] + red[2][bb][lane] + red[3][bb][lane];
+    const int u = h0 + 16 * bb + j;
+    const float bias = L.b1[u], wt = L.w2[u];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) y[e] = fmaf(wt, mlp_act(z[e] + bias, L.act), y[e]);
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) y[e] += __shfl_xor(y[e], off);  // over the 16 units of the lane group
+  if (j == 0) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int t = t0 + 4 * q + e;
+      if (t < L.n) L.parts[(size_t)blockIdx.y * L.n + t] = y[e];
+    }
+  }
+}
+
+// One workgroup: logit = b2 + the tiles' partials in tile order; sigmoid;
+// optionally the top `keep` ids by (score descending, id ascending).
+__global__ __launch_bounds__(kProbeThreads) void mlp_finish_kernel(MlpLaunch L) {
+  const int nt = L.hidden / kMlpTileH;
+  for (int t = threadIdx.x; t < L.n; t += kProbeThreads) {
+    float z = L.b2;
+    for (int i = 0; i < nt; ++i) z += L.parts[(size_t)i * L.n + t];
+    L.scores_out[t] = 1.f / (1.f + expf(-z));
+  }
+  if (L.keep <= 0) return;
+  __syncthreads();  // the scores written above are visible to the whole workgroup
+  rank_and_plan(L.n, L.ids, L.scores_out, false, L.keep, 0, L.keep_out, nullptr, nullptr);
+}
+
+__global__ void record_scores_kernel(DevPool P, const int32_t* list, const float* f, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int t = list[i];
+  const int c = P.nscore[t] + 1;
+  P.sbar[t] += (f[i] - P.sbar[t]) / (float)c;
+  P.nscore[t] = c;
+}
+
 }  // namespace
+
+hipError_t launch_mlp_score(const MlpLaunch& L, hipStream_t s) {
+  hipLaunchKernelGGL(mlp_tile_kernel, dim3((L.n + kMlpTileT - 1) / kMlpTileT, L.hidden / kMlpTileH), dim3(256),
+                     0, s, L);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(mlp_finish_kernel, dim3(1), dim3(kProbeThreads), 0, s, L);
+  return hipGetLastError();
+}
+
+hipError_t launch_record_scores(const DevPool& P, const int32_t* list, const float* f, int32_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(record_scores_kernel, dim3((n + 255) / 256), dim3(256), 0, s, P, list, f, n);
+  return hipGetLastError();
+}
 
 hipError_t launch_score_update(const DevPool& P, const ScoreLaunch& L, hipStream_t s) {
   if (L.n <= 0) return hipSuccess;

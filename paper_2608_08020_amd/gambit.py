@@ -51,6 +51,15 @@ class Round(ctypes.Structure):
                 ("n_pruned", ctypes.c_int32), ("n_children", ctypes.c_int32)]
 
 
+class Mlp(ctypes.Structure):
+    _fields_ = [("dim", ctypes.c_int32), ("hidden", ctypes.c_int32), ("activation", ctypes.c_int32),
+                ("w1", ctypes.c_void_p), ("b1", ctypes.c_void_p), ("w2", ctypes.c_void_p),
+                ("b2", ctypes.c_float)]
+
+
+ACT_RELU, ACT_GELU = 0, 1
+
+
 class Stats(ctypes.Structure):
     _fields_ = [("total_tokens", ctypes.c_int64), ("unique_tokens", ctypes.c_int64),
                 ("unique_blocks", ctypes.c_int64), ("table_entries", ctypes.c_int64),
@@ -64,7 +73,8 @@ EXPORTS = ["gambit_workspace_size", "gambit_pool_create", "gambit_pool_destroy",
            "gambit_score_prune_branch", "gambit_rank_topk", "gambit_pool_check",
            "gambit_plan_stats", "gambit_seq_len", "gambit_free_blocks", "gambit_status_str",
            "gambit_last_error", "gambit_profile_begin", "gambit_profile_end", "gambit_score_update",
-           "gambit_evict", "gambit_tournament", "gambit_trace_state"]
+           "gambit_evict", "gambit_tournament", "gambit_trace_state", "gambit_record_scores",
+           "gambit_mlp_workspace_size", "gambit_mlp_score"]
 
 
 def lib() -> ctypes.CDLL:
@@ -98,6 +108,9 @@ def lib() -> ctypes.CDLL:
         "gambit_evict": (i32, [vp, i32, vp, vp, vp]),
         "gambit_tournament": (i32, [vp, i32, i32, i32, ctypes.POINTER(Round), vp, vp, vp, vp]),
         "gambit_trace_state": (i32, [vp, i32, vp, vp, vp, vp, vp, vp]),
+        "gambit_record_scores": (i32, [vp, i32, vp, vp, vp]),
+        "gambit_mlp_workspace_size": (ctypes.c_size_t, [i32, i32]),
+        "gambit_mlp_score": (i32, [i32, vp, ctypes.POINTER(Mlp), vp, vp, i32, vp, vp, ctypes.c_size_t, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -142,6 +155,25 @@ def rank_topk(ids: torch.Tensor, scores: torch.Tensor, keep: int, stream=None) -
     if st != OK:
         raise GambitError(st, "rank_topk")
     return out
+
+
+def mlp_score(h: torch.Tensor, w1: torch.Tensor, b1: torch.Tensor, w2: torch.Tensor, b2: float,
+              activation: str = "relu", ids: torch.Tensor | None = None, keep: int = 0, stream=None):
+    """gambit_mlp_score: (scores [n] fp32, top-`keep` ids or None), on the device."""
+    n, dim = h.shape
+    hidden = w1.shape[0]
+    m = Mlp(dim, hidden, ACT_RELU if activation == "relu" else ACT_GELU, _dev(w1, torch.bfloat16).value,
+            _dev(b1, torch.float32).value, _dev(w2, torch.float32).value, float(b2))
+    ws_bytes = int(lib().gambit_mlp_workspace_size(n, hidden))
+    ws = torch.empty(max(ws_bytes, 4), dtype=torch.uint8, device=h.device)
+    scores = torch.empty(n, dtype=torch.float32, device=h.device)
+    keep_out = torch.empty(max(keep, 1), dtype=torch.int32, device=h.device)
+    st = lib().gambit_mlp_score(n, _dev(h, torch.bfloat16), ctypes.byref(m), _dev(scores),
+                                None if ids is None else _dev(ids, torch.int32), keep, _dev(keep_out), _dev(ws),
+                                ws_bytes, _stream(stream))
+    if st != OK:
+        raise GambitError(st, "mlp_score")
+    return scores, (keep_out[:keep] if keep > 0 else None)
 
 
 class Pool:
@@ -287,6 +319,12 @@ class Pool:
         pl = [(int(c), int(p)) for c, p in pairs[:r.n_children]]
         rk = ranked[:r.n_active].cpu().numpy().tolist() if ranked is not None else None
         return r.case_taken, r.n_active, pruned[:r.n_pruned].tolist(), pl, rk
+
+    def record_scores(self, ids, f: torch.Tensor, stream=None):
+        """gambit_record_scores: running means from device thought scores f [n]."""
+        ids = _host_i32(ids)
+        self._check(lib().gambit_record_scores(self._h, ids.size, _ptr(ids), _dev(f, torch.float32),
+                                               _stream(stream)), "record_scores")
 
     def trace_state(self, ids, stream=None):
         """gambit_trace_state: (s_bar fp32, scored thoughts, GenLen, ghost) per listed slot."""
