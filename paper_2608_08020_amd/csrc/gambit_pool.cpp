@@ -125,7 +125,7 @@ struct gambit_pool {
   int n_units = 0;
   bool queues_dirty = false;       // an attention launch was not followed by its merge
   int max_splits_used = 0;
-  std::vector<int32_t> cnt, first, csr_off, csr_fill, csr;  // per-block planner scratch
+  std::vector<int32_t> cnt, first;  // per-block planner scratch, zero / -1 between calls
   gambit_stats stats{};            // of plan_list, kept current by decode steps
 
   // attention-kernel event timing
@@ -278,28 +278,29 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
   const int Hkv = p->d.num_kv_heads;
   const int kmax = p->L.kmax;
   const int nb_total = p->d.num_blocks;
-  if ((int)p->first.size() != nb_total) {
-    p->first.assign(nb_total, -1);
-    p->csr_off.assign(nb_total, 0);
-    p->csr_fill.assign(nb_total, 0);
-  }
+  if ((int)p->first.size() != nb_total) p->first.assign(nb_total, -1);
   std::vector<int> nb(n);
+  for (int pos = 0; pos < n; ++pos) nb[pos] = cdiv(p->seq_len[ids[pos]], 16);
+  // Sharers per block among the listed traces.  When the list holds every
+  // running trace that is the block's refcount (ghosts hold no blocks);
+  // otherwise it is counted.
+  int running = 0, listed_running = 0;
+  for (int t = 0; t < p->d.max_traces; ++t) running += p->seq_len[t] > 0;
+  for (int pos = 0; pos < n; ++pos) listed_running += p->seq_len[ids[pos]] > 0;
+  const bool all = n == running && listed_running == n;  // ids are distinct
+  const int32_t* cnt = all ? p->refcount.data() : p->cnt.data();
   std::vector<int32_t> touched;
-  for (int pos = 0; pos < n; ++pos) {
-    const auto& row = p->table[ids[pos]];
-    nb[pos] = cdiv(p->seq_len[ids[pos]], 16);
-    for (int j = 0; j < nb[pos]; ++j) {
-      const int b = row[j];
-      if (p->cnt[b]++ == 0) {
-        p->first[b] = pos;
-        touched.push_back(b);
-      }
+  if (!all) {
+    for (int pos = 0; pos < n; ++pos) {
+      const auto& row = p->table[ids[pos]];
+      for (int j = 0; j < nb[pos]; ++j)
+        if (p->cnt[row[j]]++ == 0) touched.push_back(row[j]);
     }
   }
   {
     gambit_stats& st = p->stats;
     st = gambit_stats{};
-    st.unique_blocks = (int64_t)touched.size();
+    st.unique_blocks = all ? (int64_t)(nb_total - p->nfree) : (int64_t)touched.size();
     for (int pos = 0; pos < n; ++pos) {
       const int L = p->seq_len[ids[pos]];
       st.total_tokens += L;
@@ -307,23 +308,48 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
       // every block is full except a trace's partial last block, which only that trace holds
       st.unique_tokens += L % 16 ? L % 16 - 16 : 0;
     }
-    st.unique_tokens += 16 * (int64_t)touched.size();
+    st.unique_tokens += 16 * st.unique_blocks;
   }
-  // member lists of shared blocks (positions ascending)
-  size_t total = 0;
-  for (int b : touched) {
-    p->csr_off[b] = (int)total;
-    p->csr_fill[b] = 0;
-    if (p->cnt[b] > 1) total += p->cnt[b];
-  }
-  p->csr.resize(total);
+  // The runs of every listed trace: [j0, j1) with c sharers; c == 1 is the
+  // private rest of the trace.  A shared run starts at the same block in all
+  // its sharers (they hold the same prefix blocks), so its member list is
+  // keyed by that block; positions are visited in ascending order, so the
+  // first one to reach it is the lowest (the run's owner) and the list is
+  // ascending.  first[b] holds the run's index while the plan is built.
+  struct Run {
+    int32_t j0, j1, c, rid;
+  };
+  std::vector<int> run_off(n + 1, 0);
+  std::vector<Run> runs;
+  std::vector<std::vector<int32_t>> mem;
+  std::vector<int32_t> starts;
   for (int pos = 0; pos < n; ++pos) {
     const auto& row = p->table[ids[pos]];
-    for (int j = 0; j < nb[pos]; ++j) {
-      const int b = row[j];
-      if (p->cnt[b] > 1) p->csr[p->csr_off[b] + p->csr_fill[b]++] = pos;
+    run_off[pos] = (int)runs.size();
+    int j = 0;
+    while (j < nb[pos]) {
+      const int c = cnt[row[j]];
+      if (c == 1) {
+        runs.push_back(Run{j, nb[pos], 1, -1});
+        break;
+      }
+      int j1 = j + 1;
+      while (j1 < nb[pos] && cnt[row[j1]] == c) ++j1;
+      const int b0 = row[j];
+      if (p->first[b0] < 0) {
+        p->first[b0] = (int)mem.size();
+        mem.emplace_back();
+        mem.back().reserve(c);
+        starts.push_back(b0);
+      }
+      mem[p->first[b0]].push_back(pos);
+      runs.push_back(Run{j, j1, c, p->first[b0]});
+      j = j1;
     }
   }
+  run_off[n] = (int)runs.size();
+  for (int b : starts) p->first[b] = -1;
+  for (int b : touched) p->cnt[b] = 0;
 
   std::vector<Group> groups;
   std::vector<int32_t> members;
@@ -335,10 +361,10 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
     int worst = 0;
     // One group per (chunk, KV head): a chunk with <= 16 rows is one narrow
     // unit; a wider chunk becomes cooperative items of up to 128 rows.
-    auto emit = [&](int owner_pos, int jb0, int nblk, int ntok_est, const int32_t* mem, int mcnt,
+    auto emit = [&](int owner_pos, int jb0, int nblk, int ntok_est, const int32_t* mem_ids, int mcnt,
                     int kidx) {
       const int moff = (int)members.size();
-      members.insert(members.end(), mem, mem + mcnt);
+      members.insert(members.end(), mem_ids, mem_ids + mcnt);
       const double tok = std::max(ntok_est, 1);
       if (mcnt * p->g <= gambit::kRowsPerUnit) {
         for (int h = 0; h < Hkv; ++h) {
@@ -362,43 +388,36 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
       }
     };
     for (int pos = 0; pos < n; ++pos) {
-      const int t = ids[pos];
-      const auto& row = p->table[t];
-      int kidx = 0, j = 0;
-      while (j < nb[pos]) {
-        const int c = p->cnt[row[j]];
-        if (c == 1) {  // private run: through the trace's last block, chunks of 4 chunk_blocks
-          const int len = nb[pos] - j;
+      int kidx = 0;
+      for (int r = run_off[pos]; r < run_off[pos + 1]; ++r) {
+        const Run& R = runs[r];
+        const int len = R.j1 - R.j0;
+        if (R.c == 1) {  // private run: through the trace's last block, chunks of 4 chunk_blocks
           const int nch = std::max(1, cdiv(len, 4 * chunk_blocks));
-          for (int k = 0, jb = j; k < nch; ++k) {
+          for (int k = 0, jb = R.j0; k < nch; ++k) {
             const int sz = len / nch + (k < len % nch ? 1 : 0);
             const bool last = k == nch - 1;
             emit(pos, jb, last ? -1 : sz, sz * 16, &pos, 1, kidx++);
             jb += sz;
           }
-          j = nb[pos];
           break;
         }
-        int j1 = j + 1;
-        while (j1 < nb[pos] && p->cnt[row[j1]] == c) ++j1;
-        const int len = j1 - j;
         // Chunk lengths (in units of chunk_blocks, 64 at first): 4 for runs of
         // one row block (narrow units), the row-block count up to 8 for wider
         // runs (cooperative items re-read their chunk per item, so longer
         // chunks mean fewer partials for the same bytes per row block).
         // Measured on the 512-trace workload; shorter chunks lose more to
         // per-unit start-up and merging than they gain at the launch's tail.
-        const int nrb = cdiv(c * p->g, gambit::kRowsPerUnit);
+        const int nrb = cdiv(R.c * p->g, gambit::kRowsPerUnit);
         const int nch = cdiv(len, chunk_blocks * (nrb == 1 ? 4 : std::min(nrb, 8)));
-        const int b0 = row[j];
-        for (int k = 0, jb = j; k < nch; ++k) {
+        const auto& ml = mem[R.rid];
+        for (int k = 0, jb = R.j0; k < nch; ++k) {
           const int sz = len / nch + (k < len % nch ? 1 : 0);
-          if (p->first[b0] == pos) emit(pos, jb, sz, sz * 16, &p->csr[p->csr_off[b0]], c, kidx);
+          if (ml[0] == pos) emit(pos, jb, sz, sz * 16, ml.data(), R.c, kidx);
           ++kidx;
           jb += sz;
         }
-        j = j1;
-        if (j == nb[pos]) emit(pos, j, -1, 16, &pos, 1, kidx++);  // appends go past the shared prefix
+        if (R.j1 == nb[pos]) emit(pos, R.j1, -1, 16, &pos, 1, kidx++);  // appends go past the shared prefix
       }
       nk[pos] = kidx;
       worst = std::max(worst, kidx);
@@ -412,10 +431,6 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
                 worst, kmax);
       break;
     }
-  }
-  for (int b : touched) {
-    p->cnt[b] = 0;
-    p->first[b] = -1;
   }
   if (st != GAMBIT_OK) return st;
 
