@@ -271,19 +271,29 @@ struct BlockIds {
   const DevPool& P;
   const int32_t* brow;
   int nblk, lane, win;
+  int fresh_j, fresh_id;  // a block this launch opened (its table entry is not read back)
+  float fresh_scale;
   int cur_id, nxt_id;
   float cur_ks, cur_vs, nxt_ks, nxt_vs;
 
-  __device__ BlockIds(const DevPool& P_, const int32_t* brow_, int nblk_, int lane_)
-      : P(P_), brow(brow_), nblk(nblk_), lane(lane_), win(0) {
+  __device__ BlockIds(const DevPool& P_, const int32_t* brow_, int nblk_, int lane_, int fresh_j_ = -1,
+                      int fresh_id_ = 0, float fresh_scale_ = 1.f)
+      : P(P_), brow(brow_), nblk(nblk_), lane(lane_), win(0), fresh_j(fresh_j_), fresh_id(fresh_id_),
+        fresh_scale(fresh_scale_) {
     fetch(0, cur_id, cur_ks, cur_vs);
     fetch(1, nxt_id, nxt_ks, nxt_vs);
   }
   // Lanes past the unit's last block re-read its last entry (never used);
   // the unconditional load lets the id land in place without a copy.
   __device__ void fetch(int w, int& id, float& ks, float& vs) {
-    id = brow[min(64 * w + lane, nblk - 1)];
+    const int j = min(64 * w + lane, nblk - 1);
+    id = brow[j];
     ks = vs = 1.f;
+    if (j == fresh_j) {
+      id = fresh_id;
+      ks = vs = fresh_scale;
+      return;
+    }
     if constexpr (FP8) {
       if ((unsigned)id >= (unsigned)P.num_blocks) {
         atomicOr(P.err, kErrBadBlock);
@@ -451,20 +461,50 @@ __device__ inline void pv_direct(Tile<FP8>& t, f32x4 s0, f32x4 s1, int t0, int n
 // refilled with tile j + 2 right after QK(j) and its V half right after
 // P.V(j), so two tiles are always in flight.
 // The decode step's append, for one KV head: the unit whose end is read at
-// run time covers its trace's last block (the allocator has already
-// advanced the length), so it writes the new token there; the unit waits
-// for the stores before its first tile load.  Only this wave touches this
-// (block, head) tile in the launch.
+// run time covers its trace's last block, so it writes the new token there;
+// the unit waits for the stores before its first tile load.  Only this wave
+// touches this (block, head) tile in the launch.  len is the trace's length
+// including the new token.  When the token opens a block, the block comes
+// from the launch's list (the host took it by the allocation rule); the KV
+// head 0 unit enters it in the table, refcount, free set (and fp8 scales),
+// and every head's unit uses the id directly.  Returns that block, or -1.
+__device__ inline int fresh_block(const AttnLaunch& A, int pos) {
+  int lo = 0, hi = A.n_new;  // new_pos is ascending
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (A.new_pos[mid] < pos)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  return lo < A.n_new && A.new_pos[lo] == pos ? A.new_blk[lo] : -1;
+}
+
 template <bool FP8>
-__device__ inline void append_token(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int lane) {
+__device__ inline int append_token(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int lane, int len) {
   constexpr int es = FP8 ? 1 : 2;
-  const int tpos = P.seq_len[U.owner] - 1;
-  const int b = P.table[(size_t)U.owner * P.max_blocks + (tpos >> 4)];
+  const int tpos = len - 1;
+  const int pos = A.members[U.mem_off];
+  int b, fresh = -1;
+  if (A.len_bias && (tpos & 15) == 0) {
+    b = fresh = fresh_block(A, pos);
+    if ((unsigned)b < (unsigned)P.num_blocks && U.kvh == 0 && lane == 0) {
+      P.table[(size_t)U.owner * P.max_blocks + (tpos >> 4)] = b;
+      P.refcount[b] = 1;
+      atomicAnd(&P.freebits[b >> 5], ~(1u << (b & 31)));
+      if (P.kv_scale) {
+        P.kv_scale[2 * b] = A.new_scale;
+        P.kv_scale[2 * b + 1] = A.new_scale;
+      }
+    }
+  } else {
+    b = P.table[(size_t)U.owner * P.max_blocks + (tpos >> 4)];
+  }
   if ((unsigned)b >= (unsigned)P.num_blocks) {
     if (lane == 0) atomicOr(P.err, kErrBadBlock);
-    return;
+    return -1;
   }
-  const int row = tpos & 15, pos = A.members[U.mem_off];
+  const int row = tpos & 15;
   const size_t src = ((size_t)pos * P.Hkv + U.kvh) * kHeadDim * es;
   const size_t tile = head_off<FP8>(b, P.Hkv, U.kvh);
   if (lane < kHeadDim * es / 16)  // K: 16-byte d-chunks at token row k_phys(row)
@@ -479,19 +519,21 @@ __device__ inline void append_token(const DevPool& P, const AttnLaunch& A, const
       *reinterpret_cast<uint16_t*>(P.v_cache + tile + ((size_t)d * kBlock + row) * 2) =
           reinterpret_cast<const uint16_t*>(A.v_new + src)[d];
   }
+  return fresh;
 }
 
 template <bool FP8>
 __device__ void narrow_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int lane) {
   const int32_t* brow = P.table + (size_t)U.owner * P.max_blocks + U.jb0;
-  const int ntok = U.nblk >= 0 ? U.nblk * kBlock : P.seq_len[U.owner] - U.jb0 * kBlock;
+  const int len = U.nblk >= 0 ? 0 : P.seq_len[U.owner] + A.len_bias;
+  const int ntok = U.nblk >= 0 ? U.nblk * kBlock : len - U.jb0 * kBlock;
   if (ntok <= 0) return;
-  if (U.nblk < 0) append_token<FP8>(P, A, U, lane);
+  const int fresh = U.nblk < 0 ? append_token<FP8>(P, A, U, lane, len) : -1;
   const int R = U.mem_cnt * P.g;  // <= 16
   const LaneGeom g = lane_geom(lane);
   const int nblk = (ntok + kBlock - 1) / kBlock;
   const int ntile = (ntok + 31) / 32;
-  BlockIds<FP8> ids(P, brow, nblk, lane);
+  BlockIds<FP8> ids(P, brow, nblk, lane, fresh >= 0 ? nblk - 1 : -1, fresh, A.new_scale);
   bf16x8 qf[4];
   load_q(P, A, U, 0, R, FP8, g.q, g.lr, qf);
   RowState st;
@@ -673,7 +715,8 @@ template <bool FP8, int RB>
 __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int wave, int lane,
                           uint8_t* lds) {
   const int32_t* brow = P.table + (size_t)U.owner * P.max_blocks + U.jb0;
-  const int ntok = U.nblk >= 0 ? U.nblk * kBlock : P.seq_len[U.owner] - U.jb0 * kBlock;
+  // a cooperative item is a shared run: its end is in the plan
+  const int ntok = U.nblk >= 0 ? U.nblk * kBlock : P.seq_len[U.owner] + A.len_bias - U.jb0 * kBlock;
   if (ntok <= 0) return;  // uniform over the workgroup
   const int R = U.mem_cnt * P.g;  // <= 64 RB
   const LaneGeom g = lane_geom(lane);
@@ -893,6 +936,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(DevPool P, Attn
 // over the partials with the weights broadcast from their lanes.
 __global__ __launch_bounds__(256) void merge_kernel(DevPool P, AttnLaunch A) {
   if (blockIdx.x == 0 && threadIdx.x < 8) A.queues[threadIdx.x] = 0;  // for the next attention launch
+  if (A.len_bias) {  // the step's token is in: advance the lengths (and GenLen, Alg. 1)
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < A.n) {
+      const int t = A.list[i];
+      P.seq_len[t] += 1;
+      P.gen[t] += 1;
+    }
+  }
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= A.n * P.Hq) return;
   const int lane = threadIdx.x & 63;

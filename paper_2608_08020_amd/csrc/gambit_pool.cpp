@@ -767,8 +767,26 @@ gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, 
     if (st) return st;
   }
   const int32_t* dlist = ws_ptr<int32_t>(p, p->L.list);
-  HIP_TRY(p, gambit::launch_alloc(p->dev, dlist, nullptr, 1, n, p->append_scale, true, s), "append alloc");
   gambit::AttnLaunch A{};
+  // The blocks this step opens: the mirror takes them by the allocation
+  // rule (lowest free ids, in list order) and, when they fit in the launch
+  // arguments, the attention launch enters them and the merge advances the
+  // lengths; otherwise the allocator kernel runs first.
+  const bool in_args = need <= gambit::kMaxArgBlocks;
+  if (!in_args)
+    HIP_TRY(p, gambit::launch_alloc(p->dev, dlist, nullptr, 1, n, p->append_scale, true, s), "append alloc");
+  A.list = dlist;
+  A.len_bias = in_args ? 1 : 0;
+  A.new_scale = p->append_scale;
+  for (int i = 0; i < n; ++i) {
+    const bool opens = p->seq_len[ids[i]] % 16 == 0;
+    mirror_grow(p, ids[i], 1);
+    ++p->gen[ids[i]];
+    if (opens && in_args) {
+      A.new_pos[A.n_new] = i;
+      A.new_blk[A.n_new++] = p->table[ids[i]].back();
+    }
+  }
   A.q = static_cast<const uint16_t*>(q);
   A.k_new = static_cast<const uint8_t*>(k_new);  // appended by the attention launch
   A.v_new = static_cast<const uint8_t*>(v_new);
@@ -799,10 +817,6 @@ gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, 
   }
   HIP_TRY(p, gambit::launch_attention_merge(p->dev, A, s), "attention merge");
   p->queues_dirty = false;
-  for (int i = 0; i < n; ++i) {
-    mirror_grow(p, ids[i], 1);
-    ++p->gen[ids[i]];
-  }
   p->stats.total_tokens += n;
   p->stats.unique_tokens += n;
   p->stats.unique_blocks += need;

@@ -71,6 +71,8 @@ enum : int32_t {
   kErrBadBlock = 4,         // a table entry outside [0, num_blocks)
 };
 
+constexpr int kMaxArgBlocks = 256;  // new blocks one decode step can hand to its launch
+
 struct AttnLaunch {
   const uint16_t* q;        // [n][Hq][128] bf16
   const uint8_t* k_new;     // [n][Hkv][128] cache elements: this step's token, written by the
@@ -89,6 +91,17 @@ struct AttnLaunch {
   float scale_log2;         // sm_scale * log2(e)
   void* out;
   int32_t out_f32;
+  // The decode step's new blocks.  len_bias = 1: the lengths still exclude
+  // this step's token; the blocks it opens (the lowest free ids, in list
+  // order, as the host mirror took them) are listed here and claimed by the
+  // appending units, and the merge kernel advances the lengths.  len_bias =
+  // 0: the allocator kernel has already run.
+  const int32_t* list;      // [n] trace ids in list order
+  int32_t len_bias;
+  int32_t n_new;            // entries of new_pos / new_blk, positions ascending
+  float new_scale;          // fp8 scale of a block a decode step opens
+  int32_t new_pos[kMaxArgBlocks];
+  int32_t new_blk[kMaxArgBlocks];
 };
 
 hipError_t launch_pool_init(const DevPool& P, hipStream_t s);

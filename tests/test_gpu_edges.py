@@ -12,6 +12,7 @@ from oracle.formats import bf16_to_f64, e4m3fn_to_f64
 from oracle.probe import rank
 from paper_2608_08020_amd import gambit
 from paper_2608_08020_amd.gambit import GambitError, Pool
+from workload.generate import to_bf16_bits
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -191,3 +192,74 @@ def test_empty_calls_are_no_ops():
     p.decode_attn([], z, z[:, :1], z[:, :1])
     p.pool_check()
     assert p.free_blocks() == 4
+
+
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8_e4m3"])
+def test_many_blocks_opened_in_one_step(kv_dtype):
+    """A decode step whose appends open more blocks than its launch carries
+    (the allocator kernel runs first) and steps that open fewer (the attention
+    launch claims them), with the trace list out of id order and freed blocks
+    interleaved with used ones: tables, refcounts, lengths, scales and
+    attention as the pool model gives them."""
+    from oracle.pool import PoolModel
+
+    fp8 = kv_dtype == "fp8_e4m3"
+    T, Hq, Hkv = 300, 4, 1
+    rng = np.random.default_rng(11)
+    p = Pool(num_blocks=1200, num_q_heads=Hq, num_kv_heads=Hkv, max_traces=T, max_blocks_per_trace=4,
+             kv_dtype=kv_dtype)
+    om = PoolModel(num_blocks=1200, n_kv_heads=Hkv, head_dim=128, kv_dtype=kv_dtype, max_traces=T,
+                   max_blocks_per_trace=4)
+
+    def codes(n):
+        if fp8:
+            c = rng.integers(0, 256, size=(n, Hkv, 128)).astype(np.uint8)
+            c[(c & 0x7F) == 0x7F] = 0x38  # no NaN codes
+            return c
+        return to_bf16_bits(rng.standard_normal((n, Hkv, 128)).astype(np.float32))
+
+    def bf16_dev(c):
+        return torch.from_numpy(c.view(np.int16)).view(torch.bfloat16).to(DEV)
+
+    def dev(c):
+        return torch.from_numpy(c).to(DEV) if fp8 else bf16_dev(c)
+
+    def fill(t, L):
+        p.kv_alloc([t], [L])
+        om.alloc([t], [L])
+        k, v = codes(L), codes(L)
+        sc = np.full(((L + 15) // 16, 2), 0.5 + t / T, np.float32) if fp8 else None
+        p.kv_write(t, 0, dev(k), dev(v), sc)
+        om.write(t, 0, k, v, sc)
+
+    for t in range(T):
+        fill(t, 16 if t < 270 else 7)
+
+    def step(ids):
+        n = len(ids)
+        q = to_bf16_bits(rng.standard_normal((n, Hq, 128)).astype(np.float32))
+        kn, vn = codes(n), codes(n)
+        out = p.decode_attn(ids, bf16_dev(q), dev(kn), dev(vn), out_dtype=torch.float32).cpu().numpy()
+        om.append(ids, kn, vn)
+        for i in list(range(0, n, 37)) + [n - 1]:
+            K, V = om.materialise(int(ids[i]))
+            ref = decode_attention(bf16_to_f64(q[i]), K, V, 1 / math.sqrt(128))
+            assert np.abs(out[i] - ref).max() <= 1e-3 + 2e-3 * np.abs(ref).max(), (ids[i], i)
+        assert p.seq_len.cpu().numpy().tolist() == om.seq_len
+        assert np.array_equal(p.block_table.cpu().numpy(), om.table_array())
+        assert p.refcount.cpu().numpy().tolist() == om.refcount
+        if fp8:
+            sc = p.kv_scale.cpu().numpy()
+            for t in ids:
+                assert [tuple(sc[b]) for b in om.table[t]] == om.bscale[t], t
+        p.pool_check()
+
+    step(rng.permutation(T))        # 270 blocks opened: more than one launch carries
+    step(rng.permutation(T))        # none opened
+    for t in range(0, 200, 2):      # frees 100 traces' blocks between used ones
+        p.kv_free([t])
+        om.free_traces([t])
+    for t in range(0, 200, 2):
+        fill(t, 32)
+    step(rng.permutation(T))        # 100 opened, claimed by the attention launch
+    step(rng.permutation(T)[:150])  # a partial list
