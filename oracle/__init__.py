@@ -11,7 +11,9 @@ Contents and the passages each part follows:
 
 * ``formats``   - bf16 and OCP E4M3FN decoding to fp64 (storage formats of
                   the KV cache; the fp8 per-block scale follows the workload
-                  definition of the fp8 configuration).
+                  definition of the fp8 configuration), and the E4M3FN
+                  encoding of quantise-on-append (nearest value, ties to the
+                  even code, saturating; the quotient x / scale in fp32).
 * ``attention`` - decode-step attention of one trace over its whole context,
                   the plain softmax(q K^T * s) V definition with grouped KV
                   heads.  The method's saving is that children inherit the
@@ -27,7 +29,9 @@ Contents and the passages each part follows:
                   lowest-free-first block allocation, fork = share full
                   blocks + copy the partial tail, free = drop references
                   (Sec. 4.1 Case 2: pruning frees the non-shared blocks, the
-                  child inherits the parent's KV through prefix caching).
+                  child inherits the parent's KV through prefix caching);
+                  a decode step's bf16 K/V quantised into fp8 blocks with the
+                  landing block's scale.
 * ``tournament`` - the full tournament of Alg. 1 over the pool model:
                   running-mean scores, GenLen eligibility, Case 1 fill
                   (Eq. 2), Case 2 swap (Eq. 3), scheduler eviction of the

@@ -6,6 +6,13 @@ float32 whose upper 16 bits are the pattern.
 OCP 8-bit floating point E4M3FN (the fp8 KV format): sign, 4 exponent bits
 (bias 7), 3 mantissa bits; no infinities; S.1111.111 is NaN; exponent field
 0 encodes subnormals m * 2^-9.  Largest finite magnitude 1.75 * 2^8 = 448.
+
+Encoding (quantise-on-append of a decode step's K/V into an fp8 block): the
+code of a finite value y is the E4M3FN value nearest to |y|, ties to the code
+with an even mantissa, magnitudes beyond 448 saturating to 448, with y's
+sign (so -0 gives 0x80).  The value quantised is y = x / s rounded to fp32 (x
+the bf16 element, s the block's fp32 scale): a rounding decides an integer
+here, so the oracle takes it in the precision the kernel computes in.
 """
 from __future__ import annotations
 
@@ -35,3 +42,48 @@ def decode(codes: np.ndarray, kv_dtype: str) -> np.ndarray:
     if kv_dtype == "fp8_e4m3":
         return e4m3fn_to_f64(codes)
     raise ValueError(kv_dtype)
+
+
+# The 127 non-negative finite E4M3FN values, indexed by code 0x00 .. 0x7E.
+_E4M3_POS = None
+
+
+def _e4m3_table() -> np.ndarray:
+    global _E4M3_POS
+    if _E4M3_POS is None:
+        _E4M3_POS = e4m3fn_to_f64(np.arange(0x7F, dtype=np.uint8))
+    return _E4M3_POS
+
+
+def f64_to_e4m3fn(y: np.ndarray) -> np.ndarray:
+    """Codes of finite values y: nearest value, ties to the even code, saturating."""
+    y = np.asarray(y, dtype=np.float64)
+    if not np.isfinite(y).all():
+        raise ValueError("E4M3FN encoding of a non-finite value")
+    vals = _e4m3_table()
+    a = np.abs(y).reshape(-1)
+    out = np.empty(a.shape, np.uint8)
+    for i, x in enumerate(a):
+        if x >= vals[-1]:
+            out[i] = 0x7E
+            continue
+        hi = int(np.searchsorted(vals, x, side="left"))  # vals[hi] >= x
+        if vals[hi] == x:
+            out[i] = hi
+            continue
+        lo = hi - 1
+        dlo, dhi = x - vals[lo], vals[hi] - x
+        if dlo < dhi:
+            out[i] = lo
+        elif dhi < dlo:
+            out[i] = hi
+        else:  # a tie: the even mantissa
+            out[i] = lo if lo % 2 == 0 else hi
+    out |= np.where(np.signbit(y).reshape(-1), 0x80, 0).astype(np.uint8)
+    return out.reshape(y.shape)
+
+
+def quantise_e4m3fn(x: np.ndarray, scale: float) -> np.ndarray:
+    """Codes of x / scale, the quotient rounded to fp32 first (x: fp64 values of bf16)."""
+    q = np.asarray(x, dtype=np.float32) / np.float32(scale)
+    return f64_to_e4m3fn(q.astype(np.float64))

@@ -32,7 +32,7 @@ import heapq
 
 import numpy as np
 
-from .formats import decode
+from .formats import bf16_to_f64, decode, quantise_e4m3fn
 
 
 class PoolError(ValueError):
@@ -226,6 +226,25 @@ class PoolModel:
             L = self.seq_len[t]
             self._grow(t, 1, (self.append_scale, self.append_scale))
             self.runs[t].append([L, L + 1, k_new, v_new, i])
+
+    def append_quantised(self, ids, k_bf16, v_bf16):
+        """A decode step's append from bf16 K/V (bit patterns [n][Hkv][D], list
+        order).  A bf16 pool stores them as they are.  An fp8 pool quantises
+        each token with the scale of the block it lands in: the block's own
+        (K, V) scales, or append_scale for a block the step opens."""
+        if not self.fp8:
+            return self.append(ids, k_bf16, v_bf16)
+        ids = [int(t) for t in ids]
+        kx, vx = bf16_to_f64(k_bf16), bf16_to_f64(v_bf16)
+        kc = np.empty(kx.shape, np.uint8)
+        vc = np.empty(vx.shape, np.uint8)
+        for i, t in enumerate(ids):
+            L = self.seq_len[t]
+            sk, sv = (self.append_scale, self.append_scale) if L % self.BS == 0 else self.bscale[t][L // self.BS]
+            kc[i] = quantise_e4m3fn(kx[i], sk)
+            vc[i] = quantise_e4m3fn(vx[i], sv)
+        self.append(ids, kc, vc)
+        return kc, vc
 
     # -------------------------------------------------------- materialise --
     def materialise(self, t: int):

@@ -180,3 +180,36 @@ def test_fp8_scales_follow_blocks():
         p.append([0], np.full((1, 1, 2), 0x38, np.uint8), np.full((1, 1, 2), 0x38, np.uint8))
     K, V = p.materialise(0)
     assert K[32, 0, 0] == 0.5 and V[32, 0, 0] == 0.5  # block allocated by a decode step
+
+
+def test_quantised_append_uses_the_scale_of_the_landing_block():
+    """fp8: a token landing in an existing block is quantised with that
+    block's (K, V) scales; one that opens a block, with append_scale.  Values
+    that are code * scale come back exactly; others within half a code step."""
+    p = _pool(kv="fp8_e4m3")
+    p.alloc([0], [3])
+    p.write(0, 0, np.full((3, Hkv, D), 0x38, np.uint8), np.full((3, Hkv, D), 0x38, np.uint8),
+            scales=[[0.5, 0.25]])
+    bits = lambda a: (np.asarray(a, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    # K = 1.5 * 0.5 = 0.75, V = 3 * 0.25 = 0.75 exactly; the codes are 1.5 and 3
+    kc, vc = p.append_quantised([0], bits(np.full((1, Hkv, D), 0.75)), bits(np.full((1, Hkv, D), 0.75)))
+    assert (kc == 0x3C).all() and (vc == 0x44).all()
+    K, V = p.materialise(0)
+    assert (K[3] == 0.75).all() and (V[3] == 0.75).all()
+    # a token that opens a block takes append_scale (2^-6): 0.1 is not a code
+    # multiple; the stored value is the nearest multiple of a code
+    p.alloc([1], [16])
+    p.write(1, 0, np.zeros((16, Hkv, D), np.uint8), np.zeros((16, Hkv, D), np.uint8), scales=[[1.0, 1.0]])
+    x = bits(np.full((1, Hkv, D), 0.1))
+    p.append_quantised([1], x, x)
+    K, V = p.materialise(1)
+    assert p.bscale[1][1] == (2.0 ** -6, 2.0 ** -6)
+    xv = float(bf16_to_f64(x[0, 0, 0]))
+    # 0.1 * 64 = 6.4 lies between the codes 6 and 6.5: 6.5 (step 0.5) is nearer
+    assert K[16, 0, 0] == 6.5 * 2.0 ** -6 and abs(K[16, 0, 0] - xv) <= 0.25 * 2.0 ** -6
+    # a bf16 pool stores the bits as they are
+    q = _pool()
+    q.alloc([0], [5])
+    q.write(0, 0, np.zeros((5, Hkv, D), np.uint16), np.zeros((5, Hkv, D), np.uint16))
+    q.append_quantised([0], x, x)
+    assert (q.materialise(0)[0][5] == xv).all()
