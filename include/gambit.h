@@ -69,7 +69,9 @@ typedef struct gambit_pool gambit_pool;
 
 /*
  * Pool description.  Layouts (all device memory, caller-owned):
- *   k_cache, v_cache  num_blocks x num_kv_heads tiles of block_size x
+ *   k_cache, v_cache  per layer (num_layers of them, one after another; a
+ *                     block id names the same slot in every layer)
+ *                     num_blocks x num_kv_heads tiles of block_size x
  *                     head_dim elements, bf16 or OCP E4M3FN bytes for
  *                     GAMBIT_KV_FP8_E4M3 (tile bytes = 16 * 128 * element
  *                     size).  Inside a tile, with C = 16 / element size:
@@ -78,8 +80,9 @@ typedef struct gambit_pool gambit_pool;
  *                         p(t) = t with its bits 2 and 3 swapped;
  *                       V element (t, d) at element index d * 16 + t.
  *                     Only the library's kernels write the caches.
- *   kv_scale          [num_blocks][2] fp32 (K scale, V scale); fp8 only,
- *                     NULL for bf16.  A stored fp8 value means code * scale.
+ *   kv_scale          [num_layers][num_blocks][2] fp32 (K scale, V scale);
+ *                     fp8 only, NULL for bf16.  A stored fp8 value means
+ *                     code * scale.
  *   block_table       [max_traces][max_blocks_per_trace] int32, -1 = none
  *   seq_len           [max_traces] int32
  *   refcount          [num_blocks] int32
@@ -97,6 +100,7 @@ typedef struct {
   int32_t max_blocks_per_trace;
   int32_t max_splits;            /* attention partials per (trace, head), <= 64; 0 = 64 */
   float fp8_append_scale;        /* scale of blocks a decode step allocates; 0 = 2^-6 */
+  int32_t num_layers;            /* layers sharing the block table; 0 = 1   */
   void* k_cache;
   void* v_cache;
   float* kv_scale;
@@ -132,12 +136,13 @@ gambit_status gambit_pool_destroy(gambit_pool* pool);
 gambit_status gambit_kv_alloc(gambit_pool* pool, int32_t n, const int32_t* trace_ids,
                               const int32_t* n_tokens, void* stream);
 
-/* Write n tokens of K and V at positions pos0 .. pos0+n-1 of a trace.
- * k, v: device [n][num_kv_heads][head_dim] in the cache dtype.  Every touched
- * block must be held by this trace alone (else GAMBIT_ERR_SHARED_WRITE).
- * fp8: scales is host [m][2] for the m blocks whose first position lies in
- * [pos0, pos0+n), ascending; the codes of tokens in other blocks must
- * already be quantised with those blocks' scales.  bf16: scales is NULL. */
+/* Write n tokens of K and V at positions pos0 .. pos0+n-1 of a trace, in
+ * every layer.  k, v: device [num_layers][n][num_kv_heads][head_dim] in the
+ * cache dtype.  Every touched block must be held by this trace alone (else
+ * GAMBIT_ERR_SHARED_WRITE).  fp8: scales is host [num_layers][m][2] for the
+ * m blocks whose first position lies in [pos0, pos0+n), ascending; the codes
+ * of tokens in other blocks must already be quantised with those blocks'
+ * scales.  bf16: scales is NULL. */
 gambit_status gambit_kv_write(gambit_pool* pool, int32_t trace_id, int32_t pos0, int32_t n,
                               const void* k, const void* v, const float* scales, void* stream);
 
@@ -156,7 +161,8 @@ gambit_status gambit_kv_fork(gambit_pool* pool, int32_t n, const int32_t* parent
  * becomes 0.  trace_ids: host [n]; freeing an empty trace is an error. */
 gambit_status gambit_kv_free(gambit_pool* pool, int32_t n, const int32_t* trace_ids, void* stream);
 
-/* One decode step for the listed traces (Alg. 1 Generate, attention part):
+/* One decode step of a one-layer pool (num_layers 1) for the listed traces
+ * (Alg. 1 Generate, attention part):
  * append k_new/v_new at position seq_len (taking a new block when seq_len is
  * a multiple of 16; fp8 blocks taken here get fp8_append_scale), then for
  * every trace t and query head h, with G = h / (Hq / Hkv),
@@ -171,6 +177,28 @@ gambit_status gambit_kv_free(gambit_pool* pool, int32_t n, const int32_t* trace_
 gambit_status gambit_decode_attn(gambit_pool* pool, int32_t n, const int32_t* trace_ids,
                                  const void* q, const void* k_new, const void* v_new,
                                  void* out, int32_t out_dtype, float sm_scale, void* stream);
+
+enum { GAMBIT_NEW_CACHE = 0, GAMBIT_NEW_BF16 = 1 };
+
+/* One layer of a decode step: the operation of gambit_decode_attn on layer
+ * `layer`'s caches.  A step is the calls for layers 0, 1, ..., num_layers - 1
+ * in order, with the same trace list: the blocks the step opens are taken at
+ * layer 0 (one allocation for all layers), the token lands at the same
+ * position in every layer, and the lengths (and GenLen) advance after the
+ * last layer.  While a step is open, calls that change or check the pool
+ * (kv_*, evict, tournament, score_prune_branch, pool_check) fail with
+ * GAMBIT_ERR_INVALID and change nothing.
+ *   new_dtype  GAMBIT_NEW_CACHE: k_new/v_new in the cache dtype, as for
+ *              gambit_decode_attn.  GAMBIT_NEW_BF16: bf16 [n][Hkv][head_dim];
+ *              an fp8 pool quantises each element on append: code = the
+ *              E4M3FN value nearest to x / s (the quotient rounded to fp32;
+ *              ties to the even code; beyond 448 saturating, no NaN), s the
+ *              landing block's K or V scale (fp8_append_scale for a block the
+ *              step opens).  A bf16 pool stores them as they are.
+ * The other arguments are those of gambit_decode_attn. */
+gambit_status gambit_decode_attn_layer(gambit_pool* pool, int32_t layer, int32_t n, const int32_t* trace_ids,
+                                       const void* q, const void* k_new, const void* v_new, int32_t new_dtype,
+                                       void* out, int32_t out_dtype, float sm_scale, void* stream);
 
 /* A thought boundary (Alg. 1 Tournament; Eqs. 2-3; Sec. 4.1):
  *   score[i] = 1 / (1 + exp(-(h[i] . w + b)))   (linear sigmoid probe, the

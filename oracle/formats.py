@@ -62,23 +62,13 @@ def f64_to_e4m3fn(y: np.ndarray) -> np.ndarray:
         raise ValueError("E4M3FN encoding of a non-finite value")
     vals = _e4m3_table()
     a = np.abs(y).reshape(-1)
-    out = np.empty(a.shape, np.uint8)
-    for i, x in enumerate(a):
-        if x >= vals[-1]:
-            out[i] = 0x7E
-            continue
-        hi = int(np.searchsorted(vals, x, side="left"))  # vals[hi] >= x
-        if vals[hi] == x:
-            out[i] = hi
-            continue
-        lo = hi - 1
-        dlo, dhi = x - vals[lo], vals[hi] - x
-        if dlo < dhi:
-            out[i] = lo
-        elif dhi < dlo:
-            out[i] = hi
-        else:  # a tie: the even mantissa
-            out[i] = lo if lo % 2 == 0 else hi
+    hi = np.minimum(np.searchsorted(vals, a, side="left"), len(vals) - 1)  # vals[hi] >= a below 448
+    lo = np.maximum(hi - 1, 0)
+    dlo, dhi = a - vals[lo], vals[hi] - a
+    tie_even = np.where(lo % 2 == 0, lo, hi)
+    out = np.where(dlo < dhi, lo, np.where(dhi < dlo, hi, tie_even))
+    out = np.where(vals[hi] == a, hi, out)
+    out = np.where(a >= vals[-1], 0x7E, out).astype(np.uint8)
     out |= np.where(np.signbit(y).reshape(-1), 0x80, 0).astype(np.uint8)
     return out.reshape(y.shape)
 

@@ -126,10 +126,12 @@ __global__ __launch_bounds__(kAllocThreads) void alloc_kernel(DevPool P, const i
       const int b = P.alloc_list[off++];
       row[j] = b;
       P.refcount[b] = 1;
-      if (P.kv_scale) {
-        P.kv_scale[2 * b] = new_scale;
-        P.kv_scale[2 * b + 1] = new_scale;
-      }
+      if (P.kv_scale)
+        for (int l = 0; l < P.num_layers; ++l) {
+          float* sc = P.kv_scale + (size_t)l * 2 * P.num_blocks;
+          sc[2 * b] = new_scale;
+          sc[2 * b + 1] = new_scale;
+        }
     }
     P.seq_len[tr] = L + nt;
     if (generated) P.gen[tr] += nt;
@@ -161,9 +163,12 @@ __device__ inline void copy_token(const DevPool& P, int blk, int row, const uint
   }
 }
 
-__global__ void write_kernel(DevPool P, int32_t trace, int32_t pos0, const uint8_t* k,
-                             const uint8_t* v, const float* started_scales) {
-  const int i = blockIdx.x;
+// One workgroup per (token, layer); k, v: [layers][n][Hkv][128], started
+// scales: [layers][started][2].
+__global__ void write_kernel(DevPool P0, int32_t trace, int32_t pos0, int32_t n, const uint8_t* k,
+                             const uint8_t* v, const float* started_scales, int32_t started) {
+  const int i = blockIdx.x, l = blockIdx.y;
+  const DevPool P = P0.layer(l);
   const int pos = pos0 + i;
   const int blk = P.table[(size_t)trace * P.max_blocks + pos / kBlock];
   if ((unsigned)blk >= (unsigned)P.num_blocks) {
@@ -171,10 +176,11 @@ __global__ void write_kernel(DevPool P, int32_t trace, int32_t pos0, const uint8
     return;
   }
   const size_t tok_bytes = (size_t)P.Hkv * kHeadDim * P.esize;
-  copy_token(P, blk, pos % kBlock, k + i * tok_bytes, v + i * tok_bytes);
+  const size_t src = ((size_t)l * n + i) * tok_bytes;
+  copy_token(P, blk, pos % kBlock, k + src, v + src);
   if (started_scales && threadIdx.x == 0 && pos % kBlock == 0) {
     const int first = (pos0 + kBlock - 1) / kBlock * kBlock;
-    const int k2 = (pos - first) / kBlock;
+    const int k2 = l * started + (pos - first) / kBlock;
     P.kv_scale[2 * blk] = started_scales[2 * k2];
     P.kv_scale[2 * blk + 1] = started_scales[2 * k2 + 1];
   }
@@ -244,8 +250,9 @@ __global__ void fork_share_kernel(DevPool P, const int32_t* pairs, int32_t* req_
 
 // Branch, part 2: copy the partial tail block (every KV head; whole tiles,
 // the slots past the tail are never read unmasked) and its fp8 scales into
-// the child's new block.
-__global__ void fork_tail_kernel(DevPool P, const int32_t* pairs) {
+// the child's new block; one workgroup per (pair, layer).
+__global__ void fork_tail_kernel(DevPool P0, const int32_t* pairs) {
+  const DevPool P = P0.layer(blockIdx.y);
   const int child = pairs[2 * blockIdx.x], parent = pairs[2 * blockIdx.x + 1];
   const int L = P.seq_len[parent];
   if (L % kBlock == 0) return;
@@ -289,8 +296,10 @@ hipError_t launch_alloc(const DevPool& P, const int32_t* req_trace, const int32_
 hipError_t launch_write(const DevPool& P, int32_t trace, int32_t pos0, int32_t n, const void* k,
                         const void* v, const float* started_scales, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(write_kernel, dim3(n), dim3(128), 0, s, P, trace, pos0,
-                     static_cast<const uint8_t*>(k), static_cast<const uint8_t*>(v), started_scales);
+  const int first = (pos0 + kBlock - 1) / kBlock, last = (pos0 + n - 1) / kBlock;
+  hipLaunchKernelGGL(write_kernel, dim3(n, P.num_layers), dim3(128), 0, s, P, trace, pos0, n,
+                     static_cast<const uint8_t*>(k), static_cast<const uint8_t*>(v), started_scales,
+                     last >= first ? last - first + 1 : 0);
   return hipGetLastError();
 }
 
@@ -308,7 +317,7 @@ hipError_t launch_fork(const DevPool& P, const int32_t* pairs, int32_t n, int32_
   if (e != hipSuccess) return e;
   e = launch_alloc(P, req_trace, req_ntok, -1, n, 1.0f, false, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(fork_tail_kernel, dim3(n), dim3(256), 0, s, P, pairs);
+  hipLaunchKernelGGL(fork_tail_kernel, dim3(n, P.num_layers), dim3(256), 0, s, P, pairs);
   return hipGetLastError();
 }
 

@@ -468,6 +468,29 @@ __device__ inline void pv_direct(Tile<FP8>& t, f32x4 s0, f32x4 s1, int t0, int n
 // from the launch's list (the host took it by the allocation rule); the KV
 // head 0 unit enters it in the table, refcount, free set (and fp8 scales),
 // and every head's unit uses the id directly.  Returns that block, or -1.
+// OCP E4M3FN code of a finite fp32 value: the nearest of the format's values
+// (ties to an even mantissa), magnitudes from 448 up saturating to 448.
+// Normal results: round the fp32 significand to 3 bits at bit 20 (round to
+// nearest even), then move the exponent bias from 127 to 7; a carry out of
+// the mantissa steps the exponent, which is the correct next value.  Below
+// 2^-6 the codes are the multiples of 2^-9, so the code is |y| * 512 rounded
+// to the nearest even integer (8 becomes the smallest normal, code 8).
+__device__ inline uint32_t e4m3fn_code(float y) {
+  const uint32_t u = __float_as_uint(y);
+  const uint32_t sign = (u >> 24) & 0x80u;
+  const float a = fabsf(y);
+  uint32_t c;
+  if (a >= 448.f) {
+    c = 0x7Eu;
+  } else if (a < 0.015625f) {
+    c = (uint32_t)__builtin_rintf(a * 512.f);
+  } else {
+    const uint32_t m = u & 0x7FFFFFFFu;
+    c = ((m + 0x7FFFFu + ((m >> 20) & 1u)) >> 20) - ((127u - 7u) << 3);
+  }
+  return sign | c;
+}
+
 __device__ inline int fresh_block(const AttnLaunch& A, int pos) {
   int lo = 0, hi = A.n_new;  // new_pos is ascending
   while (lo < hi) {
@@ -489,9 +512,11 @@ __device__ inline int append_token(const DevPool& P, const AttnLaunch& A, const 
   if (A.len_bias && (tpos & 15) == 0) {
     b = fresh = fresh_block(A, pos);
     if ((unsigned)b < (unsigned)P.num_blocks && U.kvh == 0 && lane == 0) {
-      P.table[(size_t)U.owner * P.max_blocks + (tpos >> 4)] = b;
-      P.refcount[b] = 1;
-      atomicAnd(&P.freebits[b >> 5], ~(1u << (b & 31)));
+      if (A.claim) {
+        P.table[(size_t)U.owner * P.max_blocks + (tpos >> 4)] = b;
+        P.refcount[b] = 1;
+        atomicAnd(&P.freebits[b >> 5], ~(1u << (b & 31)));
+      }
       if (P.kv_scale) {
         P.kv_scale[2 * b] = A.new_scale;
         P.kv_scale[2 * b + 1] = A.new_scale;
@@ -505,8 +530,27 @@ __device__ inline int append_token(const DevPool& P, const AttnLaunch& A, const 
     return -1;
   }
   const int row = tpos & 15;
-  const size_t src = ((size_t)pos * P.Hkv + U.kvh) * kHeadDim * es;
   const size_t tile = head_off<FP8>(b, P.Hkv, U.kvh);
+  if constexpr (FP8) {
+    if (A.new_bf16) {  // quantise on append with the landing block's scales
+      const float sk = fresh >= 0 ? A.new_scale : P.kv_scale[2 * b];
+      const float sv = fresh >= 0 ? A.new_scale : P.kv_scale[2 * b + 1];
+      const size_t src = ((size_t)pos * P.Hkv + U.kvh) * kHeadDim + 2 * lane;  // bf16 elements
+      const uint32_t kk = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint16_t*>(A.k_new) + src);
+      const uint32_t vv = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint16_t*>(A.v_new) + src);
+      const uint32_t k0 = e4m3fn_code(__uint_as_float(kk << 16) / sk);
+      const uint32_t k1 = e4m3fn_code(__uint_as_float(kk & 0xFFFF0000u) / sk);
+      const uint32_t v0 = e4m3fn_code(__uint_as_float(vv << 16) / sv);
+      const uint32_t v1 = e4m3fn_code(__uint_as_float(vv & 0xFFFF0000u) / sv);
+      const int d = 2 * lane;  // elements d, d + 1 of one 16-byte K chunk
+      *reinterpret_cast<uint16_t*>(P.k_cache + tile + ((size_t)(d >> 4) * kBlock + k_phys(row)) * 16 + (d & 15)) =
+          (uint16_t)(k0 | (k1 << 8));
+      P.v_cache[tile + (size_t)d * kBlock + row] = (uint8_t)v0;
+      P.v_cache[tile + (size_t)(d + 1) * kBlock + row] = (uint8_t)v1;
+      return fresh;
+    }
+  }
+  const size_t src = ((size_t)pos * P.Hkv + U.kvh) * kHeadDim * es;
   if (lane < kHeadDim * es / 16)  // K: 16-byte d-chunks at token row k_phys(row)
     *reinterpret_cast<uint4*>(P.k_cache + tile + ((size_t)lane * kBlock + k_phys(row)) * 16) =
         *reinterpret_cast<const uint4*>(A.k_new + src + lane * 16);
@@ -936,7 +980,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(DevPool P, Attn
 // over the partials with the weights broadcast from their lanes.
 __global__ __launch_bounds__(256) void merge_kernel(DevPool P, AttnLaunch A) {
   if (blockIdx.x == 0 && threadIdx.x < 8) A.queues[threadIdx.x] = 0;  // for the next attention launch
-  if (A.len_bias) {  // the step's token is in: advance the lengths (and GenLen, Alg. 1)
+  if (A.len_bias && A.advance) {  // the step's token is in: advance the lengths (and GenLen, Alg. 1)
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i < A.n) {
       const int t = A.list[i];

@@ -29,6 +29,7 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int kDefaultSplits = 64;
+constexpr int kMaxLayers = 1024;
 constexpr int kDefaultChunkBlocks = 64;  // blocks per attention chunk before balancing
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -50,6 +51,8 @@ bool layout_of(const gambit_pool_desc* d, Layout* L) {
   if (g != 1 && g != 2 && g != 4 && g != 8 && g != 16) return false;
   if (d->kv_dtype != GAMBIT_KV_BF16 && d->kv_dtype != GAMBIT_KV_FP8_E4M3) return false;
   if (d->max_traces <= 0 || d->max_blocks_per_trace <= 0 || d->max_splits < 0 || d->max_splits > 64) return false;
+  if (d->num_layers < 0 || d->num_layers > kMaxLayers) return false;
+  const size_t layers = d->num_layers ? d->num_layers : 1;
   const int T = d->max_traces;
   const int kmax = d->max_splits ? d->max_splits : kDefaultSplits;
   size_t o = 0;
@@ -72,7 +75,7 @@ bool layout_of(const gambit_pool_desc* d, Layout* L) {
   L->ticket = take(64);
   L->queues = take(64);
   L->err = take(64);
-  L->scales = take(8 * ((size_t)d->max_blocks_per_trace + 1));
+  L->scales = take(8 * ((size_t)d->max_blocks_per_trace + 1) * layers);
   L->freebits = take(4 * (size_t)L->nwords);
   L->alloc_list = take(4 * (size_t)d->num_blocks);
   L->units = take(sizeof(AttnUnit) * (size_t)L->max_units);
@@ -125,6 +128,8 @@ struct gambit_pool {
   int n_units = 0;
   bool queues_dirty = false;       // an attention launch was not followed by its merge
   int max_splits_used = 0;
+  int step_next = 0;               // the layer the open decode step expects next (0: none open)
+  gambit::AttnLaunch step{};       // the open step's launch arguments
   std::vector<int32_t> cnt, first;  // per-block planner scratch, zero / -1 between calls
   gambit_stats stats{};            // of plan_list, kept current by decode steps
 
@@ -513,6 +518,16 @@ void invalidate_plan(gambit_pool* p) { p->plan_valid = false; }
 }  // namespace
 
 // =============================================================================
+namespace {
+
+// Calls that change or check the pool wait for an open decode step to end.
+gambit_status step_open(gambit_pool* p) {
+  return fail(p, GAMBIT_ERR_INVALID, "a decode step is open: layer %d of %d is next", p->step_next,
+              p->dev.num_layers);
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* gambit_status_str(gambit_status s) {
@@ -576,6 +591,8 @@ gambit_status gambit_pool_create(const gambit_pool_desc* desc, void* stream, gam
   D.Hkv = desc->num_kv_heads;
   D.g = p->g;
   D.esize = desc->kv_dtype == GAMBIT_KV_FP8_E4M3 ? 1 : 2;
+  D.num_layers = desc->num_layers ? desc->num_layers : 1;
+  D.layer_bytes = (size_t)desc->num_blocks * desc->num_kv_heads * 16 * 128 * D.esize;
 
   p->table.assign(desc->max_traces, {});
   p->seq_len.assign(desc->max_traces, 0);
@@ -588,7 +605,7 @@ gambit_status gambit_pool_create(const gambit_pool_desc* desc, void* stream, gam
   if (desc->num_blocks % 64) p->freebits.back() = (1ull << (desc->num_blocks % 64)) - 1;
   p->nfree = desc->num_blocks;
 
-  p->stage_ints = 8 * (size_t)desc->max_traces + 2 * ((size_t)desc->max_blocks_per_trace + 1);
+  p->stage_ints = 8 * (size_t)desc->max_traces + 2 * ((size_t)desc->max_blocks_per_trace + 1) * D.num_layers;
   p->plan_stage_bytes = 4 * align_up(4 * (size_t)desc->max_traces) + sizeof(AttnUnit) * (size_t)L.max_units +
                         4 * (size_t)L.max_members + 4 * kAlign;
   hipError_t e = hipHostMalloc(reinterpret_cast<void**>(&p->stage), p->stage_ints * 4, hipHostMallocDefault);
@@ -632,6 +649,7 @@ int32_t gambit_free_blocks(const gambit_pool* p) { return p ? p->nfree : -1; }
 gambit_status gambit_kv_alloc(gambit_pool* p, int32_t n, const int32_t* ids, const int32_t* ntok,
                               void* stream) {
   if (!p) return GAMBIT_ERR_INVALID;
+  if (p->step_next) return step_open(p);
   gambit_status st = check_ids(p, n, ids, "trace");
   if (st) return st;
   if (n > 0 && !ntok) return fail(p, GAMBIT_ERR_INVALID, "token counts are NULL");
@@ -664,6 +682,7 @@ gambit_status gambit_kv_alloc(gambit_pool* p, int32_t n, const int32_t* ids, con
 gambit_status gambit_kv_write(gambit_pool* p, int32_t t, int32_t pos0, int32_t n, const void* k,
                               const void* v, const float* scales, void* stream) {
   if (!p) return GAMBIT_ERR_INVALID;
+  if (p->step_next) return step_open(p);
   if (t < 0 || t >= p->d.max_traces) return fail(p, GAMBIT_ERR_INVALID, "trace id %d out of range", t);
   if (pos0 < 0 || n < 0 || (long)pos0 + n > p->seq_len[t])
     return fail(p, GAMBIT_ERR_INVALID, "write [%d, %d) outside trace %d's %d positions", pos0, pos0 + n, t,
@@ -682,7 +701,8 @@ gambit_status gambit_kv_write(gambit_pool* p, int32_t t, int32_t pos0, int32_t n
   if (fp8 && started > 0) {
     dsc = ws_ptr<float>(p, p->L.scales);
     gambit_status st = upload_ints(p, reinterpret_cast<int32_t*>(dsc),
-                                   reinterpret_cast<const int32_t*>(scales), 2 * (size_t)started, S(stream));
+                                   reinterpret_cast<const int32_t*>(scales),
+                                   2 * (size_t)started * p->dev.num_layers, S(stream));
     if (st) return st;
   }
   HIP_TRY(p, gambit::launch_write(p->dev, t, pos0, n, k, v, dsc, S(stream)), "write kernel");
@@ -692,6 +712,7 @@ gambit_status gambit_kv_write(gambit_pool* p, int32_t t, int32_t pos0, int32_t n
 gambit_status gambit_kv_fork(gambit_pool* p, int32_t n, const int32_t* parents, const int32_t* children,
                              void* stream) {
   if (!p) return GAMBIT_ERR_INVALID;
+  if (p->step_next) return step_open(p);
   std::vector<char> is_child;
   gambit_status st = check_ids(p, n, children, "child", &is_child);
   if (st) return st;
@@ -725,6 +746,7 @@ gambit_status gambit_kv_fork(gambit_pool* p, int32_t n, const int32_t* parents, 
 
 gambit_status gambit_kv_free(gambit_pool* p, int32_t n, const int32_t* ids, void* stream) {
   if (!p) return GAMBIT_ERR_INVALID;
+  if (p->step_next) return step_open(p);
   gambit_status st = check_ids(p, n, ids, "trace");
   if (st) return st;
   for (int i = 0; i < n; ++i)
@@ -740,69 +762,90 @@ gambit_status gambit_kv_free(gambit_pool* p, int32_t n, const int32_t* ids, void
   return GAMBIT_OK;
 }
 
-gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, const void* q,
-                                 const void* k_new, const void* v_new, void* out, int32_t out_dtype,
-                                 float sm_scale, void* stream) {
+// One layer of a decode step.  Layer 0 opens the step: it validates the
+// list, plans the launch, and takes the blocks the step opens.  The mirror
+// takes them by the allocation rule (lowest free ids, in list order); when
+// they fit in the launch arguments the layer-0 attention launch enters them
+// and the last layer's merge advances the lengths, otherwise the allocator
+// kernel enters them (and advances the lengths) before layer 0.
+static gambit_status decode_layer(gambit_pool* p, int32_t layer, int32_t n, const int32_t* ids, const void* q,
+                           const void* k_new, const void* v_new, int32_t new_dtype, void* out,
+                           int32_t out_dtype, float sm_scale, void* stream) {
   if (!p) return GAMBIT_ERR_INVALID;
+  const int nl = p->dev.num_layers;
+  if (layer != p->step_next)
+    return fail(p, GAMBIT_ERR_INVALID, "decode layer %d called, layer %d of %d is next", layer, p->step_next, nl);
   gambit_status st = check_ids(p, n, ids, "trace");
   if (st) return st;
   if (n == 0) return GAMBIT_OK;
   if (!q || !k_new || !v_new || !out) return fail(p, GAMBIT_ERR_INVALID, "NULL buffer");
   if (out_dtype != GAMBIT_OUT_BF16 && out_dtype != GAMBIT_OUT_F32)
     return fail(p, GAMBIT_ERR_INVALID, "bad output dtype");
+  if (new_dtype != GAMBIT_NEW_CACHE && new_dtype != GAMBIT_NEW_BF16)
+    return fail(p, GAMBIT_ERR_INVALID, "bad dtype of the new K/V");
   if (!std::isfinite(sm_scale)) return fail(p, GAMBIT_ERR_INVALID, "softmax scale is not finite");
-  int need = 0;
-  for (int i = 0; i < n; ++i) {
-    const int L = p->seq_len[ids[i]];
-    if (L == 0) return fail(p, GAMBIT_ERR_INVALID, "trace %d is empty", ids[i]);
-    if (cdiv(L + 1, 16) > p->d.max_blocks_per_trace)
-      return fail(p, GAMBIT_ERR_INVALID, "trace %d is full", ids[i]);
-    need += L % 16 == 0;
-  }
-  if (need > p->nfree) return fail(p, GAMBIT_ERR_OUT_OF_BLOCKS, "need %d blocks, %d free", need, p->nfree);
   hipStream_t s = S(stream);
-  if (!p->plan_valid || (int)p->plan_list.size() != n ||
-      !std::equal(p->plan_list.begin(), p->plan_list.end(), ids)) {
-    st = build_plan(p, n, ids, s);
-    if (st) return st;
-  }
-  const int32_t* dlist = ws_ptr<int32_t>(p, p->L.list);
-  gambit::AttnLaunch A{};
-  // The blocks this step opens: the mirror takes them by the allocation
-  // rule (lowest free ids, in list order) and, when they fit in the launch
-  // arguments, the attention launch enters them and the merge advances the
-  // lengths; otherwise the allocator kernel runs first.
-  const bool in_args = need <= gambit::kMaxArgBlocks;
-  if (!in_args)
-    HIP_TRY(p, gambit::launch_alloc(p->dev, dlist, nullptr, 1, n, p->append_scale, true, s), "append alloc");
-  A.list = dlist;
-  A.len_bias = in_args ? 1 : 0;
-  A.new_scale = p->append_scale;
-  for (int i = 0; i < n; ++i) {
-    const bool opens = p->seq_len[ids[i]] % 16 == 0;
-    mirror_grow(p, ids[i], 1);
-    ++p->gen[ids[i]];
-    if (opens && in_args) {
-      A.new_pos[A.n_new] = i;
-      A.new_blk[A.n_new++] = p->table[ids[i]].back();
+  gambit::AttnLaunch& A = p->step;
+  if (layer == 0) {
+    int need = 0;
+    for (int i = 0; i < n; ++i) {
+      const int L = p->seq_len[ids[i]];
+      if (L == 0) return fail(p, GAMBIT_ERR_INVALID, "trace %d is empty", ids[i]);
+      if (cdiv(L + 1, 16) > p->d.max_blocks_per_trace)
+        return fail(p, GAMBIT_ERR_INVALID, "trace %d is full", ids[i]);
+      need += L % 16 == 0;
     }
+    if (need > p->nfree) return fail(p, GAMBIT_ERR_OUT_OF_BLOCKS, "need %d blocks, %d free", need, p->nfree);
+    if (!p->plan_valid || (int)p->plan_list.size() != n ||
+        !std::equal(p->plan_list.begin(), p->plan_list.end(), ids)) {
+      st = build_plan(p, n, ids, s);
+      if (st) return st;
+    }
+    const int32_t* dlist = ws_ptr<int32_t>(p, p->L.list);
+    A = gambit::AttnLaunch{};
+    const bool in_args = need <= gambit::kMaxArgBlocks;
+    if (!in_args)
+      HIP_TRY(p, gambit::launch_alloc(p->dev, dlist, nullptr, 1, n, p->append_scale, true, s), "append alloc");
+    A.list = dlist;
+    A.len_bias = in_args ? 1 : 0;
+    A.new_scale = p->append_scale;
+    for (int i = 0; i < n; ++i) {
+      const bool opens = p->seq_len[ids[i]] % 16 == 0;
+      mirror_grow(p, ids[i], 1);
+      ++p->gen[ids[i]];
+      if (opens && in_args) {
+        A.new_pos[A.n_new] = i;
+        A.new_blk[A.n_new++] = p->table[ids[i]].back();
+      }
+    }
+    A.units = ws_ptr<AttnUnit>(p, p->L.units);
+    std::memcpy(A.xcd_off, p->xcd_off, sizeof A.xcd_off);
+    A.grid = p->grid;
+    A.queues = ws_ptr<int32_t>(p, p->L.queues);
+    A.members = ws_ptr<int32_t>(p, p->L.members);
+    A.nk = ws_ptr<int32_t>(p, p->L.nk);
+    A.part_acc = ws_ptr<float>(p, p->L.part_acc);
+    A.part_ml = ws_ptr<float2>(p, p->L.part_ml);
+    A.kmax = p->L.kmax;
+    A.n = n;
+    p->stats.total_tokens += n;
+    p->stats.unique_tokens += n;
+    p->stats.unique_blocks += need;
+    p->stats.table_entries += need;
+  } else if (n != A.n || !std::equal(p->plan_list.begin(), p->plan_list.end(), ids)) {
+    return fail(p, GAMBIT_ERR_INVALID, "layer %d of a step lists other traces than layer 0", layer);
   }
   A.q = static_cast<const uint16_t*>(q);
   A.k_new = static_cast<const uint8_t*>(k_new);  // appended by the attention launch
   A.v_new = static_cast<const uint8_t*>(v_new);
-  A.units = ws_ptr<AttnUnit>(p, p->L.units);
-  std::memcpy(A.xcd_off, p->xcd_off, sizeof A.xcd_off);
-  A.grid = p->grid;
-  A.queues = ws_ptr<int32_t>(p, p->L.queues);
-  A.members = ws_ptr<int32_t>(p, p->L.members);
-  A.nk = ws_ptr<int32_t>(p, p->L.nk);
-  A.part_acc = ws_ptr<float>(p, p->L.part_acc);
-  A.part_ml = ws_ptr<float2>(p, p->L.part_ml);
-  A.kmax = p->L.kmax;
-  A.n = n;
   A.scale_log2 = sm_scale * 1.4426950408889634f;
   A.out = out;
   A.out_f32 = out_dtype == GAMBIT_OUT_F32;
+  A.claim = layer == 0;
+  A.advance = layer == nl - 1;
+  A.new_bf16 = new_dtype == GAMBIT_NEW_BF16 && p->d.kv_dtype == GAMBIT_KV_FP8_E4M3;
+  p->step_next = layer + 1 == nl ? 0 : layer + 1;
+  const gambit::DevPool D = p->dev.layer(layer);
   // The merge kernel leaves the slot counters at zero for the next launch;
   // only after a launch that was not followed by its merge are they
   // cleared here.
@@ -810,18 +853,30 @@ gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, 
   p->queues_dirty = true;
   const bool timed = p->prof_on && p->prof_used + 2 <= (int)p->prof_ev.size();
   if (timed) HIP_TRY(p, hipEventRecord(p->prof_ev[p->prof_used], s), "profile event");
-  HIP_TRY(p, gambit::launch_attention_units(p->dev, A, s), "attention");
+  HIP_TRY(p, gambit::launch_attention_units(D, A, s), "attention");
   if (timed) {
     HIP_TRY(p, hipEventRecord(p->prof_ev[p->prof_used + 1], s), "profile event");
     p->prof_used += 2;
   }
-  HIP_TRY(p, gambit::launch_attention_merge(p->dev, A, s), "attention merge");
+  HIP_TRY(p, gambit::launch_attention_merge(D, A, s), "attention merge");
   p->queues_dirty = false;
-  p->stats.total_tokens += n;
-  p->stats.unique_tokens += n;
-  p->stats.unique_blocks += need;
-  p->stats.table_entries += need;
   return GAMBIT_OK;
+}
+
+gambit_status gambit_decode_attn(gambit_pool* p, int32_t n, const int32_t* ids, const void* q,
+                                 const void* k_new, const void* v_new, void* out, int32_t out_dtype,
+                                 float sm_scale, void* stream) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  if (p->dev.num_layers != 1)
+    return fail(p, GAMBIT_ERR_INVALID, "the pool has %d layers: decode with gambit_decode_attn_layer",
+                p->dev.num_layers);
+  return decode_layer(p, 0, n, ids, q, k_new, v_new, GAMBIT_NEW_CACHE, out, out_dtype, sm_scale, stream);
+}
+
+gambit_status gambit_decode_attn_layer(gambit_pool* p, int32_t layer, int32_t n, const int32_t* ids,
+                                       const void* q, const void* k_new, const void* v_new, int32_t new_dtype,
+                                       void* out, int32_t out_dtype, float sm_scale, void* stream) {
+  return decode_layer(p, layer, n, ids, q, k_new, v_new, new_dtype, out, out_dtype, sm_scale, stream);
 }
 
 gambit_status gambit_score_prune_branch(gambit_pool* p, int32_t n, const int32_t* ids, const void* h,
@@ -829,6 +884,7 @@ gambit_status gambit_score_prune_branch(gambit_pool* p, int32_t n, const int32_t
                                         int32_t n_parents, float* scores_out, int32_t* keep_out,
                                         int32_t* child_parent_out, void* stream) {
   if (!p) return GAMBIT_ERR_INVALID;
+  if (p->step_next) return step_open(p);
   gambit_status st = check_ids(p, n, ids, "trace");
   if (st) return st;
   if (n == 0 || n > gambit::kMaxRank) return fail(p, GAMBIT_ERR_UNSUPPORTED, "population size %d", n);
@@ -949,6 +1005,7 @@ gambit_status gambit_score_update(gambit_pool* p, int32_t n, const int32_t* ids,
 
 gambit_status gambit_evict(gambit_pool* p, int32_t n, const int32_t* ids, int32_t* victim_out, void* stream) {
   if (!p) return GAMBIT_ERR_INVALID;
+  if (p->step_next) return step_open(p);
   gambit_status st = check_running(p, n, ids);
   if (st) return st;
   if (n == 0 || !victim_out) return fail(p, GAMBIT_ERR_INVALID, "no eviction candidates");
@@ -974,6 +1031,7 @@ gambit_status gambit_tournament(gambit_pool* p, int32_t capacity, int32_t swap_k
                                 gambit_round* round_out, int32_t* pruned_out, int32_t* child_parent_out,
                                 int32_t* ranked_out, void* stream) {
   if (!p) return GAMBIT_ERR_INVALID;
+  if (p->step_next) return step_open(p);
   const int T = p->d.max_traces;
   if (T > gambit::kMaxRank) return fail(p, GAMBIT_ERR_UNSUPPORTED, "%d trace slots", T);
   if (capacity < 1 || capacity > T || swap_k < 0 || warmup < 0)
@@ -1119,6 +1177,7 @@ gambit_status gambit_trace_state(gambit_pool* p, int32_t n, const int32_t* ids, 
 
 gambit_status gambit_pool_check(gambit_pool* p, void* stream) {
   if (!p) return GAMBIT_ERR_INVALID;
+  if (p->step_next) return step_open(p);
   hipStream_t s = S(stream);
   HIP_TRY(p, hipStreamSynchronize(s), "sync");
   const int T = p->d.max_traces, MB = p->d.max_blocks_per_trace, NB = p->d.num_blocks;

@@ -44,9 +44,9 @@ constexpr int kTailSlots = 96;     // last workgroup slots of an XCD, claimed at
 
 // Device view of a pool.
 struct DevPool {
-  uint8_t* k_cache;
+  uint8_t* k_cache;       // layer 0; layer l at + l * layer_bytes
   uint8_t* v_cache;
-  float* kv_scale;        // [num_blocks][2], fp8 only
+  float* kv_scale;        // [num_layers][num_blocks][2], fp8 only
   int32_t* table;         // [max_traces][max_blocks]
   int32_t* seq_len;       // [max_traces]
   int32_t* refcount;      // [num_blocks]
@@ -63,6 +63,17 @@ struct DevPool {
   int32_t num_blocks, nwords, max_traces, max_blocks;
   int32_t Hq, Hkv, g;
   int32_t esize;          // bytes per cache element (2 bf16, 1 fp8)
+  int32_t num_layers;
+  size_t layer_bytes;     // bytes of one layer of k_cache (and of v_cache)
+
+  // The same pool seen through layer l's caches.
+  __host__ __device__ DevPool layer(int l) const {
+    DevPool q = *this;
+    q.k_cache += (size_t)l * layer_bytes;
+    q.v_cache += (size_t)l * layer_bytes;
+    if (q.kv_scale) q.kv_scale += (size_t)l * 2 * num_blocks;
+    return q;
+  }
 };
 
 enum : int32_t {
@@ -100,6 +111,10 @@ struct AttnLaunch {
   int32_t len_bias;
   int32_t n_new;            // entries of new_pos / new_blk, positions ascending
   float new_scale;          // fp8 scale of a block a decode step opens
+  int32_t claim;            // enter the new blocks in table, refcounts and free set (the
+                            //   step's first layer; every layer sets its own fp8 scales)
+  int32_t advance;          // the merge advances lengths and GenLen (the step's last layer)
+  int32_t new_bf16;         // fp8 pool: k_new / v_new are bf16, quantised on append
   int32_t new_pos[kMaxArgBlocks];
   int32_t new_blk[kMaxArgBlocks];
 };

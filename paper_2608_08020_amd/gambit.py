@@ -21,6 +21,7 @@ OK, ERR_INVALID, ERR_OUT_OF_BLOCKS, ERR_SHARED_WRITE, ERR_UNSUPPORTED, ERR_DEVIC
     0, -1, -2, -3, -4, -5, -6)
 KV_BF16, KV_FP8_E4M3 = 0, 1
 OUT_BF16, OUT_F32 = 0, 1
+NEW_CACHE, NEW_BF16 = 0, 1
 CODE_NAMES = {ERR_INVALID: "INVALID", ERR_OUT_OF_BLOCKS: "OUT_OF_BLOCKS",
               ERR_SHARED_WRITE: "SHARED_WRITE", ERR_UNSUPPORTED: "UNSUPPORTED",
               ERR_DEVICE: "DEVICE", ERR_WORKSPACE: "WORKSPACE"}
@@ -40,6 +41,7 @@ class PoolDesc(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("kv_dtype", ctypes.c_int32),
                 ("max_traces", ctypes.c_int32), ("max_blocks_per_trace", ctypes.c_int32),
                 ("max_splits", ctypes.c_int32), ("fp8_append_scale", ctypes.c_float),
+                ("num_layers", ctypes.c_int32),
                 ("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p),
                 ("kv_scale", ctypes.c_void_p), ("block_table", ctypes.c_void_p),
                 ("seq_len", ctypes.c_void_p), ("refcount", ctypes.c_void_p),
@@ -69,7 +71,7 @@ class Stats(ctypes.Structure):
 
 _lib = None
 EXPORTS = ["gambit_workspace_size", "gambit_pool_create", "gambit_pool_destroy", "gambit_kv_alloc",
-           "gambit_kv_write", "gambit_kv_fork", "gambit_kv_free", "gambit_decode_attn",
+           "gambit_kv_write", "gambit_kv_fork", "gambit_kv_free", "gambit_decode_attn", "gambit_decode_attn_layer",
            "gambit_score_prune_branch", "gambit_rank_topk", "gambit_pool_check",
            "gambit_plan_stats", "gambit_seq_len", "gambit_free_blocks", "gambit_status_str",
            "gambit_last_error", "gambit_profile_begin", "gambit_profile_end", "gambit_score_update",
@@ -94,6 +96,7 @@ def lib() -> ctypes.CDLL:
         "gambit_kv_fork": (i32, [vp, i32, vp, vp, vp]),
         "gambit_kv_free": (i32, [vp, i32, vp, vp]),
         "gambit_decode_attn": (i32, [vp, i32, vp, vp, vp, vp, vp, i32, f32, vp]),
+        "gambit_decode_attn_layer": (i32, [vp, i32, i32, vp, vp, vp, vp, i32, vp, i32, f32, vp]),
         "gambit_score_prune_branch": (i32, [vp, i32, vp, vp, i32, vp, f32, i32, i32, vp, vp, vp, vp]),
         "gambit_rank_topk": (i32, [i32, vp, vp, i32, vp, vp]),
         "gambit_pool_check": (i32, [vp, vp]),
@@ -182,24 +185,28 @@ class Pool:
     def __init__(self, *, num_blocks: int, num_q_heads: int, num_kv_heads: int,
                  max_traces: int, max_blocks_per_trace: int, kv_dtype: str = "bf16",
                  head_dim: int = 128, max_splits: int = 0, fp8_append_scale: float = 0.0,
-                 device: str = "cuda", stream=None):
+                 num_layers: int = 1, device: str = "cuda", stream=None):
         fp8 = kv_dtype == "fp8_e4m3"
         if kv_dtype not in ("bf16", "fp8_e4m3"):
             raise ValueError(kv_dtype)
         self.kv_dtype = kv_dtype
         self.Hq, self.Hkv, self.D = num_q_heads, num_kv_heads, head_dim
         self.max_traces, self.max_blocks = max_traces, max_blocks_per_trace
+        self.num_layers = num_layers
         cache_dtype = torch.uint8 if fp8 else torch.bfloat16
-        shape = (num_blocks, num_kv_heads, 16, head_dim)
+        # one layer: [num_blocks][Hkv][16][D]; several: a leading layer axis
+        lead = (num_layers,) if num_layers > 1 else ()
+        shape = lead + (num_blocks, num_kv_heads, 16, head_dim)
         self.k_cache = torch.empty(shape, dtype=cache_dtype, device=device)
         self.v_cache = torch.empty(shape, dtype=cache_dtype, device=device)
-        self.kv_scale = torch.ones((num_blocks, 2), dtype=torch.float32, device=device) if fp8 else None
+        self.kv_scale = torch.ones(lead + (num_blocks, 2), dtype=torch.float32, device=device) if fp8 else None
         self.block_table = torch.empty((max_traces, max_blocks_per_trace), dtype=torch.int32, device=device)
         self.seq_len = torch.empty(max_traces, dtype=torch.int32, device=device)
         self.refcount = torch.empty(num_blocks, dtype=torch.int32, device=device)
         d = PoolDesc(num_blocks, 16, num_q_heads, num_kv_heads, head_dim,
                      KV_FP8_E4M3 if fp8 else KV_BF16, max_traces, max_blocks_per_trace, max_splits,
-                     fp8_append_scale, self.k_cache.data_ptr(), self.v_cache.data_ptr(),
+                     fp8_append_scale,
+                     num_layers, self.k_cache.data_ptr(), self.v_cache.data_ptr(),
                      self.kv_scale.data_ptr() if fp8 else None, self.block_table.data_ptr(),
                      self.seq_len.data_ptr(), self.refcount.data_ptr(), None, 0)
         ws = workspace_size(d)
@@ -240,7 +247,9 @@ class Pool:
                     "kv_alloc")
 
     def kv_write(self, trace: int, pos0: int, k: torch.Tensor, v: torch.Tensor, scales=None, stream=None):
-        n = k.shape[0]
+        """k, v: [n][Hkv][D] (one layer) or [num_layers][n][Hkv][D]; fp8 scales
+        [m][2] or [num_layers][m][2]."""
+        n = k.shape[-3]
         sc = None
         if scales is not None:
             sc = np.ascontiguousarray(np.asarray(scales, np.float32))
@@ -270,6 +279,28 @@ class Pool:
         _dev(q, torch.bfloat16, (n, self.Hq, self.D))
         self._check(lib().gambit_decode_attn(self._h, n, _ptr(ids), _dev(q), _dev(k_new), _dev(v_new),
                                              _dev(out), od, sm, _stream(stream)), "decode_attn")
+        return out
+
+    def decode_attn_layer(self, layer: int, ids, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
+                          new_dtype: str = "cache", out: torch.Tensor | None = None, out_dtype=torch.bfloat16,
+                          sm_scale=None, stream=None) -> torch.Tensor:
+        """gambit_decode_attn_layer: layer `layer` of a decode step; new_dtype
+        "bf16" quantises bf16 k_new / v_new on append (fp8 pools)."""
+        ids = _host_i32(ids)
+        n = ids.size
+        if out is None:
+            out = torch.empty((n, self.Hq, self.D), dtype=out_dtype, device=q.device)
+        if out.dtype not in (torch.float32, torch.bfloat16):
+            raise ValueError("out must be bf16 or fp32")
+        od = OUT_F32 if out.dtype == torch.float32 else OUT_BF16
+        nd = {"cache": NEW_CACHE, "bf16": NEW_BF16}[new_dtype]
+        if nd == NEW_BF16:
+            _dev(k_new, torch.bfloat16, (n, self.Hkv, self.D))
+            _dev(v_new, torch.bfloat16, (n, self.Hkv, self.D))
+        sm = float(self.D ** -0.5 if sm_scale is None else sm_scale)
+        _dev(q, torch.bfloat16, (n, self.Hq, self.D))
+        self._check(lib().gambit_decode_attn_layer(self._h, layer, n, _ptr(ids), _dev(q), _dev(k_new), _dev(v_new),
+                                                   nd, _dev(out), od, sm, _stream(stream)), "decode_attn_layer")
         return out
 
     def score_prune_branch(self, ids, h: torch.Tensor, w: torch.Tensor, b: float, keep: int,
