@@ -20,7 +20,9 @@ its event-timed average duration.  `cpu_baseline` times the CPU oracle on a
 bounded sample of the same workload.  `tournament` times rounds of the full
 tournament of Alg. 1 (C = 256, K = 16: running-mean scoring, an eviction
 into a ghost every other round, rank / prune / branch) and the oracle's
-rounds beside them.
+rounds beside them.  `fp8_layers` times decode steps through all 64
+attention layers of a Qwen3-32B-shaped model on the fp8 workload, with the
+new K/V quantised on append.
 """
 from __future__ import annotations
 
@@ -197,6 +199,84 @@ def mlp_measure(reps: int = 20):
             "note": "includes the finishing launch (partial-logit sums, sigmoid, top-128 rank) and host launch gaps"}
 
 
+def layered_fp8(layers: int = 64, warm: int = 8, steps: int = 24):
+    """Decode steps of every attention layer of a Qwen3-32B-shaped model (64
+    layers; 64 q / 8 KV heads, head dim 128) over the 256-trace, 3-generation
+    fp8 workload: one pool of `layers` layers sharing one block table, each
+    step one allocation and one launch pair per layer, the new K/V arriving
+    in bf16 and quantised to E4M3FN on append.  Every layer holds the same
+    prefix contents (written once per layer from one generated copy); the
+    queries and new K/V are the step's for every layer.  Returns per-step
+    time, per-layer attention time and its algorithmic-bytes rate."""
+    import numpy as np
+    import torch
+
+    from paper_2608_08020_amd.gambit import Pool
+    from paper_2608_08020_amd.runner import estimate_blocks
+    from workload import CONFIGS, Workload
+    from workload.generate import to_bf16_bits
+
+    cfg = CONFIGS[5]
+    wl = Workload(cfg, total_steps=warm + steps)
+    T, Hq, Hkv, D = wl.T, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    pool = Pool(num_blocks=estimate_blocks(wl), num_q_heads=Hq, num_kv_heads=Hkv, max_traces=T,
+                max_blocks_per_trace=cfg.max_blocks_per_trace, kv_dtype="fp8_e4m3", num_layers=layers)
+    for op in wl.setup_ops():
+        if op[0] == "fork":
+            pool.kv_fork(op[1], op[2])
+        elif op[0] == "alloc":
+            pool.kv_alloc(op[1], op[2])
+        else:
+            _, slot, pos0, nid = op
+            k, v, sc = wl.node_kv(nid)
+            kd = torch.from_numpy(k).cuda().expand(layers, *k.shape).contiguous()
+            vd = torch.from_numpy(v).cuda().expand(layers, *v.shape).contiguous()
+            pool.kv_write(slot, pos0, kd, vd, None if sc is None else np.tile(sc, (layers, 1, 1)))
+    torch.cuda.synchronize()
+    log(f"fp8 {layers}-layer pool set up")
+    ids = np.arange(T, dtype=np.int32)
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()  # noqa: E731
+    q, kn, vn = {}, {}, {}
+    for st in range(warm + steps):
+        q[st] = bf(wl.step_q(st))
+        x = to_bf16_bits(wl.step_kv_f32(st))
+        kn[st], vn[st] = bf(x[0]), bf(x[1])
+    out = torch.empty((T, Hq, D), dtype=torch.bfloat16, device="cuda")
+
+    def step(st):
+        for layer in range(layers):
+            pool.decode_attn_layer(layer, ids, q[st], kn[st], vn[st], new_dtype="bf16", out=out)
+
+    for st in range(warm):
+        step(st)
+    torch.cuda.synchronize()
+    pool.profile_begin(steps * layers)
+    alg = []
+    t0 = time.perf_counter()
+    for st in range(warm, warm + steps):
+        step(st)
+        ps = pool.plan_stats(ids)
+        # distinct blocks once (fp8) + their scales, queries, table entries,
+        # the append (bf16 K/V read, fp8 codes written)
+        alg.append(ps.unique_tokens * Hkv * D * 2 + 8 * ps.unique_blocks + T * Hq * D * 2
+                   + 4 * ps.table_entries + T * Hkv * D * (2 * 2 + 2))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    attn_ms, launches = pool.profile_end()
+    pool.pool_check()
+    per_layer_s = attn_ms / 1e3 / launches
+    gbps = sum(alg) / len(alg) / per_layer_s / 1e9
+    pool.close()
+    del pool
+    torch.cuda.empty_cache()
+    return {"workload": cfg.name, "layers": layers, "steps": steps, "warmup": warm,
+            "ms_per_step": round(wall * 1e3 / steps, 3), "trace_steps_per_s": round(T * steps / wall, 1),
+            "attn_us_per_layer": round(per_layer_s * 1e6, 2), "achieved_GBps": round(gbps, 1),
+            "hbm_peak_frac": round(gbps / PEAK_HBM_GBPS, 4), "alg_bytes_per_layer": round(sum(alg) / len(alg)),
+            "append": "bf16 K/V quantised to E4M3FN in the attention launch (landing block's scale)",
+            "note": "every layer holds the same prefix contents; one block allocation per step for all layers"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -206,6 +286,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-tournament", action="store_true")
+    ap.add_argument("--no-layers", action="store_true")
+    ap.add_argument("--layers", type=int, default=64)
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path shards by "
@@ -305,6 +387,11 @@ def main():
         res["tournament"] = tournament_rounds()
         log("timing the MLP scorer")
         res["mlp_scorer"] = mlp_measure()
+    if not args.no_layers:
+        log(f"timing {args.layers}-layer fp8 steps")
+        del run, pool
+        torch.cuda.empty_cache()
+        res["fp8_layers"] = layered_fp8(args.layers)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
         res["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
