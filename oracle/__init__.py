@@ -40,9 +40,14 @@ Contents and the passages each part follows:
 * ``mlp``       - the 2-layer MLP scorer sigmoid(w2 . act(W1 h + b1) + b2)
                   (the paper's main-evaluation scorer family, Sec. 5.1;
                   dimensions, activation and weights are parameters).
+* ``seqscorer`` - the history-aware sequence scorer of App. A.1 (Eqs. 4-6):
+                  input LN, W_in, GELU, pre-norm causal Transformer layers
+                  (RoPE attention, SwiGLU), output LN, w_out, sigmoid; the
+                  whole history recomputed at every boundary.
 
 Parity status: every function is pinned by the ``-m "not gpu"`` tests
 (closed forms, library special cases, invariants, brute force, exhaustive
-code tables, hand-worked block counts).  The paper prints no numeric example
+code tables, hand-worked block counts, torch's LayerNorm / GELU / SiLU /
+causal scaled-dot-product attention).  The paper prints no numeric example
 of attention, scores or block tables, so no pin is a value from the paper.
 """
