@@ -352,6 +352,71 @@ gambit_status gambit_plan_stats(gambit_pool* pool, int32_t n, const int32_t* tra
 gambit_status gambit_profile_begin(gambit_pool* pool, int32_t max_launches);
 gambit_status gambit_profile_end(gambit_pool* pool, double* attn_ms, int32_t* launches);
 
+/*
+ * The history-aware sequence scorer (App. A.1, Eqs. 4-6) with incremental
+ * inference: each trace slot keeps the cached keys and values of its step
+ * states; at a thought boundary a listed trace's new step state h_t is
+ * scored in one pass against them,
+ *     x = GELU(W_in LN_in(h_t))
+ *     per layer:  x += W_o MHA(LN1(x))   causal over the trace's steps
+ *                                        0..t, RoPE at the step index
+ *                 x += W_2 (SiLU(W_1 LN2(x)) * W_3 LN2(x))
+ *     y_t = 1 / (1 + exp(-(w_out . LN_out(x))))
+ * which equals the whole-history forward at its last position.  LN is
+ * LayerNorm with gain and bias, eps 1e-5; GELU the erf form; heads of 64
+ * dims, scale 1/8; RoPE rotates (x_i, x_{i+32}) of each head by
+ * t * 10000^(-i/32); no biases in the linear maps.  Weights (device fp32,
+ * caller-owned, [out][in] row-major; 16-byte aligned):
+ *   ln_in_g, ln_in_b [input_dim];  w_in [d_model][input_dim]
+ *   ln1_g, ln1_b, ln2_g, ln2_b [n_layers][d_model]
+ *   w_qkv [n_layers][3 d_model][d_model]   rows: W_q, then W_k, then W_v
+ *   w_o   [n_layers][d_model][d_model]
+ *   w_13  [n_layers][2 d_ff][d_model]      rows: W_1, then W_3
+ *   w_2   [n_layers][d_model][d_ff]
+ *   ln_out_g, ln_out_b, w_out [d_model]
+ * d_model = 64 n_heads; input_dim and d_ff multiples of 64; max_steps <=
+ * 8192.  The workspace (>= gambit_scorer_workspace_size, 256-B aligned)
+ * holds the per-slot caches (fp32, max_traces * n_layers * n_heads * 2 * 64
+ * * max_steps floats) and the step's activations.
+ */
+typedef struct gambit_scorer gambit_scorer;
+typedef struct {
+  int32_t input_dim, d_model, n_heads, n_layers, d_ff, max_steps, max_traces;
+  const float *ln_in_g, *ln_in_b, *w_in;
+  const float *ln1_g, *ln1_b, *w_qkv, *w_o, *ln2_g, *ln2_b, *w_13, *w_2;
+  const float *ln_out_g, *ln_out_b, *w_out;
+  void* workspace;
+  size_t workspace_bytes;
+} gambit_scorer_desc;
+
+size_t gambit_scorer_workspace_size(const gambit_scorer_desc* desc);
+gambit_status gambit_scorer_create(const gambit_scorer_desc* desc, void* stream, gambit_scorer** out);
+gambit_status gambit_scorer_destroy(gambit_scorer* scorer);
+
+/* One thought boundary: each listed slot appends its step state and gets
+ * its score y_t.  trace_ids host [n], distinct, each holding < max_steps
+ * steps; h device [n][input_dim] bf16 in list order; scores_out device [n]
+ * fp32. */
+gambit_status gambit_scorer_step(gambit_scorer* scorer, int32_t n, const int32_t* trace_ids, const void* h,
+                                 float* scores_out, void* stream);
+
+/* Branch: child_ids[i] takes the step history of parent_ids[i] (its cached
+ * keys and values and its step count).  Children distinct and not parents
+ * in the same call.  Host arrays [n]. */
+gambit_status gambit_scorer_fork(gambit_scorer* scorer, int32_t n, const int32_t* parent_ids,
+                                 const int32_t* child_ids, void* stream);
+
+/* Prune / end: the listed slots forget their histories.  Host [n]. */
+gambit_status gambit_scorer_free(gambit_scorer* scorer, int32_t n, const int32_t* trace_ids, void* stream);
+
+/* Steps a slot holds (host mirror, no sync); -1 for a bad id. */
+int32_t gambit_scorer_steps(const gambit_scorer* scorer, int32_t trace_id);
+
+/* Compare the device step counts with the host mirror and read the device
+ * error word (synchronises the stream).  GAMBIT_OK when they agree. */
+gambit_status gambit_scorer_check(gambit_scorer* scorer, void* stream);
+const char* gambit_scorer_last_error(const gambit_scorer* scorer);
+
 /* Host mirror queries (no sync): length of a trace; free block count. */
 int32_t gambit_seq_len(const gambit_pool* pool, int32_t trace_id);
 int32_t gambit_free_blocks(const gambit_pool* pool);

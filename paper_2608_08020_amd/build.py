@@ -15,7 +15,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libgambit.so")
-SOURCES = ["gambit_pool.cpp", "blocktable.hip", "decode_attn.hip", "probe_topk.hip"]
+SOURCES = ["gambit_pool.cpp", "blocktable.hip", "decode_attn.hip", "probe_topk.hip", "seq_scorer.cpp",
+           "seqscorer.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-mcode-object-version=5",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

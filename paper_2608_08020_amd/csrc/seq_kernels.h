@@ -1,0 +1,37 @@
+// Device side of the sequence scorer: its view of the caller's memory and
+// the kernel launchers (seqscorer.hip).
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace gambit {
+
+constexpr float kSeqLnEps = 1e-5f;
+enum : int { kEpiNone = 0, kEpiGelu = 1, kEpiResid = 2 };
+
+struct SeqDev {
+  const int32_t* ids;     // [n] listed trace slots, this boundary
+  int32_t* lens;          // [max_traces] steps held per slot
+  int32_t* err;           // device error word
+  float* cache;           // [max_traces][n_layers][n_heads][keys^T [64][max_steps], values [max_steps][64]]
+  const float* ln_out_g;
+  const float* ln_out_b;
+  const float* w_out;
+  int32_t d_model, n_heads, n_layers, max_steps;
+};
+
+hipError_t seq_ln_rows(const void* in, bool in_bf16, float* out, int dim, const float* g, const float* b, int n,
+                       hipStream_t s);
+// C = A W^T (+ epilogue); N a multiple of 64, K / splits a multiple of 16;
+// part holds splits * M * N floats when splits > 1.
+hipError_t seq_gemm(const float* A, const float* W, float* C, int M, int N, int K, int splits, int epi,
+                    const float* R, float* part, hipStream_t s);
+hipError_t seq_swiglu(const float* a, float* g, int n, int f, hipStream_t s);
+hipError_t seq_attention(const SeqDev& S, int layer, const float* qkv, float* o, int n, hipStream_t s);
+hipError_t seq_head(const SeqDev& S, const float* x, float* scores, int n, hipStream_t s);
+hipError_t seq_fork(const SeqDev& S, const int32_t* pairs, int n, hipStream_t s);
+hipError_t seq_set_len(const SeqDev& S, const int32_t* ids, int n, int value, hipStream_t s);
+
+}  // namespace gambit

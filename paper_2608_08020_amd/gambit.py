@@ -62,6 +62,15 @@ class Mlp(ctypes.Structure):
 ACT_RELU, ACT_GELU = 0, 1
 
 
+class ScorerDesc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("input_dim", "d_model", "n_heads", "n_layers", "d_ff", "max_steps",
+                                              "max_traces")] + \
+               [(n, ctypes.c_void_p) for n in ("ln_in_g", "ln_in_b", "w_in", "ln1_g", "ln1_b", "w_qkv", "w_o",
+                                               "ln2_g", "ln2_b", "w_13", "w_2", "ln_out_g", "ln_out_b", "w_out",
+                                               "workspace")] + \
+               [("workspace_bytes", ctypes.c_size_t)]
+
+
 class Stats(ctypes.Structure):
     _fields_ = [("total_tokens", ctypes.c_int64), ("unique_tokens", ctypes.c_int64),
                 ("unique_blocks", ctypes.c_int64), ("table_entries", ctypes.c_int64),
@@ -76,7 +85,9 @@ EXPORTS = ["gambit_workspace_size", "gambit_pool_create", "gambit_pool_destroy",
            "gambit_plan_stats", "gambit_seq_len", "gambit_free_blocks", "gambit_status_str",
            "gambit_last_error", "gambit_profile_begin", "gambit_profile_end", "gambit_score_update",
            "gambit_evict", "gambit_tournament", "gambit_trace_state", "gambit_record_scores",
-           "gambit_mlp_workspace_size", "gambit_mlp_score"]
+           "gambit_mlp_workspace_size", "gambit_mlp_score", "gambit_scorer_workspace_size", "gambit_scorer_create",
+           "gambit_scorer_destroy", "gambit_scorer_step", "gambit_scorer_fork", "gambit_scorer_free",
+           "gambit_scorer_steps", "gambit_scorer_check", "gambit_scorer_last_error"]
 
 
 def lib() -> ctypes.CDLL:
@@ -114,6 +125,15 @@ def lib() -> ctypes.CDLL:
         "gambit_record_scores": (i32, [vp, i32, vp, vp, vp]),
         "gambit_mlp_workspace_size": (ctypes.c_size_t, [i32, i32]),
         "gambit_mlp_score": (i32, [i32, vp, ctypes.POINTER(Mlp), vp, vp, i32, vp, vp, ctypes.c_size_t, vp]),
+        "gambit_scorer_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(ScorerDesc)]),
+        "gambit_scorer_create": (i32, [ctypes.POINTER(ScorerDesc), vp, ctypes.POINTER(vp)]),
+        "gambit_scorer_destroy": (i32, [vp]),
+        "gambit_scorer_step": (i32, [vp, i32, vp, vp, vp, vp]),
+        "gambit_scorer_fork": (i32, [vp, i32, vp, vp, vp]),
+        "gambit_scorer_free": (i32, [vp, i32, vp, vp]),
+        "gambit_scorer_steps": (i32, [vp, i32]),
+        "gambit_scorer_check": (i32, [vp, vp]),
+        "gambit_scorer_last_error": (ctypes.c_char_p, [vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -391,3 +411,87 @@ class Pool:
 
     def free_blocks(self) -> int:
         return int(lib().gambit_free_blocks(self._h))
+
+
+class Scorer:
+    """The sequence scorer with per-slot step histories (gambit_scorer_*).
+
+    weights: dict of fp32 arrays - ln_in_g, ln_in_b [D], W_in [d][D],
+    ln_out_g, ln_out_b, w_out [d], and "layers": a list of dicts with ln1_g,
+    ln1_b, Wq, Wk, Wv, Wo, ln2_g, ln2_b, W1, W3 ([d_ff][d]), W2 ([d][d_ff]).
+    The binding only packs them into the library's layout on the device."""
+
+    def __init__(self, weights: dict, *, n_heads: int, max_steps: int, max_traces: int, device: str = "cuda",
+                 stream=None):
+        f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(device)  # noqa: E731
+        L = weights["layers"]
+        d, D = weights["W_in"].shape
+        d_ff = L[0]["W1"].shape[0] if L else 64
+        stack = lambda key: np.stack([x[key] for x in L]) if L else np.zeros((1, 1), np.float32)  # noqa: E731
+        self.t = {"ln_in_g": f32(weights["ln_in_g"]), "ln_in_b": f32(weights["ln_in_b"]),
+                  "w_in": f32(weights["W_in"]), "ln_out_g": f32(weights["ln_out_g"]),
+                  "ln_out_b": f32(weights["ln_out_b"]), "w_out": f32(weights["w_out"]),
+                  "ln1_g": f32(stack("ln1_g")), "ln1_b": f32(stack("ln1_b")),
+                  "ln2_g": f32(stack("ln2_g")), "ln2_b": f32(stack("ln2_b")),
+                  "w_o": f32(stack("Wo")), "w_2": f32(stack("W2")),
+                  "w_qkv": f32(np.stack([np.concatenate([x["Wq"], x["Wk"], x["Wv"]]) for x in L]) if L
+                               else np.zeros((1, 1), np.float32)),
+                  "w_13": f32(np.stack([np.concatenate([x["W1"], x["W3"]]) for x in L]) if L
+                              else np.zeros((1, 1), np.float32))}
+        self.D, self.d = D, d
+        desc = ScorerDesc(D, d, n_heads, len(L), d_ff, max_steps, max_traces,
+                          *[self.t[k].data_ptr() for k in ("ln_in_g", "ln_in_b", "w_in", "ln1_g", "ln1_b", "w_qkv",
+                                                           "w_o", "ln2_g", "ln2_b", "w_13", "w_2", "ln_out_g",
+                                                           "ln_out_b", "w_out")], None, 0)
+        ws = int(lib().gambit_scorer_workspace_size(ctypes.byref(desc)))
+        if ws == 0:
+            raise GambitError(ERR_INVALID, "invalid scorer description")
+        self.workspace = torch.empty(ws + 256, dtype=torch.uint8, device=device)
+        base = self.workspace.data_ptr()
+        desc.workspace = base + (-base) % 256
+        desc.workspace_bytes = ws
+        self.desc = desc
+        h = ctypes.c_void_p()
+        st = lib().gambit_scorer_create(ctypes.byref(desc), _stream(stream), ctypes.byref(h))
+        if st != OK:
+            raise GambitError(st, "scorer_create")
+        self._h = h
+
+    def _check(self, st: int, what: str):
+        if st != OK:
+            raise GambitError(st, f"{what}: {lib().gambit_scorer_last_error(self._h).decode()}")
+
+    def close(self):
+        if getattr(self, "_h", None):
+            torch.cuda.current_stream().synchronize()
+            lib().gambit_scorer_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def step(self, ids, h: torch.Tensor, stream=None) -> torch.Tensor:
+        """Scores [n] (device fp32) of the listed slots' new step states h [n][D] bf16."""
+        ids = _host_i32(ids)
+        n = ids.size
+        out = torch.empty(max(n, 1), dtype=torch.float32, device=h.device)
+        _dev(h, torch.bfloat16, (n, self.D))
+        self._check(lib().gambit_scorer_step(self._h, n, _ptr(ids), _dev(h), _dev(out), _stream(stream)), "step")
+        return out[:n]
+
+    def fork(self, parents, children, stream=None):
+        p, c = _host_i32(parents), _host_i32(children)
+        self._check(lib().gambit_scorer_fork(self._h, c.size, _ptr(p), _ptr(c), _stream(stream)), "fork")
+
+    def free(self, ids, stream=None):
+        ids = _host_i32(ids)
+        self._check(lib().gambit_scorer_free(self._h, ids.size, _ptr(ids), _stream(stream)), "free")
+
+    def steps(self, trace: int) -> int:
+        return int(lib().gambit_scorer_steps(self._h, trace))
+
+    def check(self, stream=None):
+        self._check(lib().gambit_scorer_check(self._h, _stream(stream)), "check")

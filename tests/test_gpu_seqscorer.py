@@ -1,0 +1,118 @@
+"""The sequence scorer's incremental inference (App. A.1, Eqs. 4-6) through
+the C ABI against the oracle's whole-history forward.
+
+Bar: scores within 1e-5 absolute.  The GPU path is fp32 (weights,
+activations, cached keys and values); the oracle fp64.  fp32's unit
+roundoff is 6e-8; the longest dot product is 4096 terms (the input
+projection), so a logit's relative error stays near 1e-6, and the sigmoid's
+slope is at most 1/4.  Step counts bit-exact with the host mirror and the
+oracle's histories.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle.formats import bf16_to_f64
+from oracle.seqscorer import SeqScorerModel, scorer_outputs
+from paper_2608_08020_amd.gambit import GambitError, Scorer
+from workload.seqscorer import SEQ_512, SEQ_SMALL, step_states, weights
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-5
+
+
+def _bf16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def _make(cfg):
+    w = weights(cfg)
+    gpu = Scorer(w, n_heads=cfg.n_heads, max_steps=cfg.max_steps, max_traces=cfg.slots)
+    ref = SeqScorerModel(w, cfg.n_heads, cfg.slots, cfg.max_steps)
+    return w, gpu, ref
+
+
+def test_small_every_round_with_forks_and_frees():
+    cfg = SEQ_SMALL
+    _, gpu, ref = _make(cfg)
+    rng = np.random.default_rng(51)
+    live = list(range(10))
+    worst = 0.0
+    for r in range(36):
+        ids = [int(t) for t in rng.permutation(live)[:max(1, int(len(live) * rng.uniform(0.5, 1.0)))]]
+        ids = [t for t in ids if ref.hist[t].__len__() < cfg.max_steps]
+        H = step_states(cfg, r)[ids]
+        got = gpu.step(ids, _bf16(H)).cpu().numpy()
+        want = ref.step(ids, bf16_to_f64(H))
+        err = float(np.abs(got - want).max())
+        worst = max(worst, err)
+        assert err <= TOL, (r, err)
+        if r % 5 == 4:  # prune two, branch two children from the survivors, into free slots
+            gone = [int(t) for t in rng.choice(live, 2, replace=False)]
+            gpu.free(gone)
+            ref.free(gone)
+            live = [t for t in live if t not in gone]
+            free_slots = [t for t in range(cfg.slots) if t not in live][:3]
+            parents = [int(t) for t in rng.choice(live, len(free_slots))]
+            gpu.fork(parents, free_slots)
+            ref.fork(parents, free_slots)
+            live += free_slots
+        assert [gpu.steps(t) for t in range(cfg.slots)] == [len(h) for h in ref.hist]
+    gpu.check()
+    assert worst > 0  # fp32 against fp64: not bitwise equal, within the bar
+
+
+def test_full_size_512_traces_sampled():
+    cfg = SEQ_512
+    w, gpu, _ = _make(cfg)
+    ids = np.arange(cfg.slots)
+    hist = []
+    sample = [0, 77, 255, 256, 511]
+    for r in range(24):
+        H = step_states(cfg, r)
+        hist.append(H)
+        got = gpu.step(ids, _bf16(H)).cpu().numpy()
+        if r in (0, 1, 7, 23):
+            for t in sample:
+                Ht = np.stack([bf16_to_f64(h[t]) for h in hist])
+                want = scorer_outputs(w, Ht, cfg.n_heads)[-1]
+                assert abs(got[t] - want) <= TOL, (r, t, got[t], want)
+    # a ragged subset (77 rows: two full 64-row tiles would be 128), then one row
+    sub = np.arange(3, 3 + 77)
+    H = step_states(cfg, 24)
+    got = gpu.step(sub, _bf16(H[sub])).cpu().numpy()
+    for i in (0, 40, 76):
+        t = int(sub[i])
+        Ht = np.stack([bf16_to_f64(h[t]) for h in hist] + [bf16_to_f64(H[t])])
+        assert abs(got[i] - scorer_outputs(w, Ht, cfg.n_heads)[-1]) <= TOL
+    got1 = gpu.step([511], _bf16(H[511:512])).cpu().numpy()
+    Ht = np.stack([bf16_to_f64(h[511]) for h in hist] + [bf16_to_f64(H[511])])
+    assert abs(got1[0] - scorer_outputs(w, Ht, cfg.n_heads)[-1]) <= TOL
+    assert gpu.steps(0) == 24 and gpu.steps(3) == 25 and gpu.steps(511) == 25
+    gpu.check()
+
+
+def test_errors_change_nothing():
+    cfg = SEQ_SMALL
+    _, gpu, ref = _make(cfg)
+    H = step_states(cfg, 0)
+    gpu.step([0, 1], _bf16(H[:2]))
+    for bad in ([0, 0], [cfg.slots], [-1]):
+        with pytest.raises(GambitError):
+            gpu.step(bad, _bf16(H[:len(bad)]))
+    with pytest.raises(GambitError):
+        gpu.fork([0], [0])
+    with pytest.raises(GambitError):
+        gpu.fork([2, 1], [1, 3])            # 1 is both child and parent
+    for r in range(cfg.max_steps - 1):      # fill slot 0 to its capacity
+        gpu.step([0], _bf16(step_states(cfg, r + 1)[:1]))
+    assert gpu.steps(0) == cfg.max_steps
+    with pytest.raises(GambitError):
+        gpu.step([0], _bf16(H[:1]))
+    assert gpu.steps(0) == cfg.max_steps and gpu.steps(1) == 1
+    gpu.free([0])
+    assert gpu.steps(0) == 0
+    gpu.check()
+    # a freed slot starts a fresh history
+    got = gpu.step([0], _bf16(H[5:6])).cpu().numpy()[0]
+    assert abs(got - ref.step([0], bf16_to_f64(H[5:6]))[0]) <= TOL
