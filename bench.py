@@ -277,6 +277,54 @@ def layered_fp8(layers: int = 64, warm: int = 8, steps: int = 24):
             "note": "every layer holds the same prefix contents; one block allocation per step for all layers"}
 
 
+def scorer_measure(history: int = 128, reps: int = 10):
+    """The history-aware sequence scorer (App. A.1) at a thought boundary of
+    all 512 traces (Qwen3-8B hidden size 4096; d_model 256, 4 heads, 2
+    layers, SwiGLU 768), each trace holding `history` earlier steps: event-
+    timed microseconds per boundary, its flops and minimum bytes, and the
+    oracle's whole-history forward on the host for a sample of traces."""
+    import numpy as np
+    import torch
+
+    from oracle.formats import bf16_to_f64
+    from oracle.seqscorer import scorer_outputs
+    from paper_2608_08020_amd.gambit import Scorer
+    from workload.seqscorer import SEQ_512, step_states, weights
+
+    c = SEQ_512
+    w = weights(c)
+    sc = Scorer(w, n_heads=c.n_heads, max_steps=c.max_steps, max_traces=c.slots)
+    ids = np.arange(c.slots, dtype=np.int32)
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()  # noqa: E731
+    H = [bf(step_states(c, r)) for r in range(4)]
+    for r in range(history):
+        sc.step(ids, H[r % 4])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for r in range(reps):
+        sc.step(ids, H[r % 4])
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    sc.check()
+    n, D, d, f, L, Hh = c.slots, c.input_dim, c.d_model, c.d_ff, c.n_layers, c.n_heads
+    t_mid = history + reps / 2
+    flops = 2.0 * n * (D * d + L * (4 * d * d + 3 * f * d)) + L * 2.0 * 2 * n * Hh * 64 * (t_mid + 1)
+    nbytes = 2.0 * n * D + 4.0 * (D * d + L * (4 * d * d + 3 * f * d)) + L * 4.0 * n * Hh * 2 * 64 * (t_mid + 1)
+    sc.close()
+    # the oracle: whole-history forward for a few traces
+    hist = np.stack([bf16_to_f64(step_states(c, r % 4)[:4]) for r in range(history + 1)], axis=1)
+    t0 = time.perf_counter()
+    for t in range(4):
+        scorer_outputs(w, hist[t], c.n_heads)
+    cpu_us = (time.perf_counter() - t0) * 1e6 / 4
+    return {"workload": c.name, "traces": n, "history_steps": history, "us_per_boundary": round(us, 1),
+            "tflops": round(flops / us / 1e6, 3), "min_bytes_GB": round(nbytes / 1e9, 4),
+            "gbps": round(nbytes / us / 1e3, 1), "cpu_oracle_us_per_trace": round(cpu_us, 1),
+            "note": "fp32 weights, activations and caches; 19 launches per boundary (2 layers)"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -288,6 +336,7 @@ def main():
     ap.add_argument("--no-tournament", action="store_true")
     ap.add_argument("--no-layers", action="store_true")
     ap.add_argument("--layers", type=int, default=64)
+    ap.add_argument("--scorer-only", action="store_true", help="time only the sequence scorer and print it")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path shards by "
@@ -295,6 +344,10 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.scorer_only:
+        print(json.dumps({"seqscorer": scorer_measure()}), flush=True)
+        return
 
     from paper_2608_08020_amd.runner import PopulationRun
     from workload import CONFIGS, Workload
@@ -387,6 +440,8 @@ def main():
         res["tournament"] = tournament_rounds()
         log("timing the MLP scorer")
         res["mlp_scorer"] = mlp_measure()
+        log("timing the sequence scorer")
+        res["seqscorer"] = scorer_measure()
     if not args.no_layers:
         log(f"timing {args.layers}-layer fp8 steps")
         del run, pool
