@@ -183,10 +183,10 @@ gambit_status gambit_scorer_create(const gambit_scorer_desc* desc, void* stream,
 gambit_status gambit_scorer_destroy(gambit_scorer* q) {
   if (!q) return GAMBIT_ERR_INVALID;
   if (q->stage_ev) {
-    hipEventSynchronize(q->stage_ev);
-    hipEventDestroy(q->stage_ev);
+    (void)hipEventSynchronize(q->stage_ev);
+    (void)hipEventDestroy(q->stage_ev);
   }
-  if (q->stage) hipHostFree(q->stage);
+  if (q->stage) (void)hipHostFree(q->stage);
   delete q;
   return GAMBIT_OK;
 }
