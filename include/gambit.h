@@ -371,7 +371,9 @@ gambit_status gambit_profile_end(gambit_pool* pool, double* attn_ms, int32_t* la
  *   ln1_g, ln1_b, ln2_g, ln2_b [n_layers][d_model]
  *   w_qkv [n_layers][3 d_model][d_model]   rows: W_q, then W_k, then W_v
  *   w_o   [n_layers][d_model][d_model]
- *   w_13  [n_layers][2 d_ff][d_model]      rows: W_1, then W_3
+ *   w_13  [n_layers][2 d_ff][d_model]      rows 32c .. 32c+15: W_1 rows
+ *                                          16c .. 16c+15; rows 32c+16 ..
+ *                                          32c+31: W_3 rows 16c .. 16c+15
  *   w_2   [n_layers][d_model][d_ff]
  *   ln_out_g, ln_out_b, w_out [d_model]
  * d_model = 64 n_heads; input_dim and d_ff multiples of 64; max_steps <=

@@ -9,7 +9,7 @@
 namespace gambit {
 
 constexpr float kSeqLnEps = 1e-5f;
-enum : int { kEpiNone = 0, kEpiGelu = 1, kEpiResid = 2 };
+enum : int { kEpiNone = 0, kEpiGelu = 1, kEpiResid = 2, kEpiSwiGLU = 3 };
 
 struct SeqDev {
   const int32_t* ids;     // [n] listed trace slots, this boundary
@@ -24,11 +24,13 @@ struct SeqDev {
 
 hipError_t seq_ln_rows(const void* in, bool in_bf16, float* out, int dim, const float* g, const float* b, int n,
                        hipStream_t s);
+// Per-row (mean, 1 / sqrt(var + eps)) of bf16 rows.
+hipError_t seq_row_stats(const uint16_t* h, int dim, float2* stats, int n, hipStream_t s);
 // C = A W^T (+ epilogue); N a multiple of 64, K / splits a multiple of 16;
-// part holds splits * M * N floats when splits > 1.
-hipError_t seq_gemm(const float* A, const float* W, float* C, int M, int N, int K, int splits, int epi,
-                    const float* R, float* part, hipStream_t s);
-hipError_t seq_swiglu(const float* a, float* g, int n, int f, hipStream_t s);
+// part holds splits * M * N floats when splits > 1.  With ln_stats, A is
+// bf16 and LayerNorm-ed (stats, gain ln_g, bias ln_b) on the fly; else fp32.
+hipError_t seq_gemm(const void* A, const float2* ln_stats, const float* ln_g, const float* ln_b, const float* W,
+                    float* C, int M, int N, int K, int splits, int epi, const float* R, float* part, hipStream_t s);
 hipError_t seq_attention(const SeqDev& S, int layer, const float* qkv, float* o, int n, hipStream_t s);
 hipError_t seq_head(const SeqDev& S, const float* x, float* scores, int n, hipStream_t s);
 hipError_t seq_fork(const SeqDev& S, const int32_t* pairs, int n, hipStream_t s);

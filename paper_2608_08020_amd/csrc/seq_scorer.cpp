@@ -19,8 +19,9 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct SeqLayout {
-  size_t ids, pairs, lens, err, cache, u0, part, x, u, qkv, o, a13, g, total;
-  int splits;  // of the input projection's K
+  size_t ids, pairs, lens, err, cache, stats, part, x, u, qkv, o, g, total;
+  int splits;      // of the input projection's K
+  int out_splits;  // of the d_model-wide projections (W_o, W_2) over their K
 };
 
 bool seq_layout(const gambit_scorer_desc* d, SeqLayout* L) {
@@ -31,8 +32,13 @@ bool seq_layout(const gambit_scorer_desc* d, SeqLayout* L) {
   if (d->input_dim % 64 || d->d_ff % 64) return false;          // GEMM tiles
   if (d->max_steps > 8192) return false;                        // LDS of the attention step
   const size_t T = d->max_traces, D = d->input_dim, dm = d->d_model, f = d->d_ff;
-  L->splits = (int)std::max<size_t>(1, D / 512);
+  L->splits = (int)std::max<size_t>(1, D / 256);
   while (D % (16 * (size_t)L->splits)) --L->splits;
+  // W_o (K = d_model) and W_2 (K = d_ff) have d_model / 64 column tiles:
+  // split their K four ways (while the parts stay >= 64 deep) to fill the GPU
+  L->out_splits = 4;
+  while (L->out_splits > 1 && (dm % (64 * (size_t)L->out_splits) || f % (64 * (size_t)L->out_splits)))
+    --L->out_splits;
   size_t o = 0;
   auto take = [&](size_t bytes) {
     const size_t at = o;
@@ -44,13 +50,12 @@ bool seq_layout(const gambit_scorer_desc* d, SeqLayout* L) {
   L->lens = take(4 * T);
   L->err = take(64);
   L->cache = take(4 * T * d->n_layers * d->n_heads * 2 * 64 * (size_t)d->max_steps);
-  L->u0 = take(4 * T * D);
-  L->part = take(4 * (size_t)L->splits * T * dm);
+  L->stats = take(8 * T);
+  L->part = take(4 * (size_t)std::max(L->splits, L->out_splits) * T * dm);
   L->x = take(4 * T * dm);
   L->u = take(4 * T * dm);
   L->qkv = take(4 * T * 3 * dm);
   L->o = take(4 * T * dm);
-  L->a13 = take(4 * T * 2 * f);
   L->g = take(4 * T * f);
   L->total = o;
   return true;
@@ -206,28 +211,34 @@ gambit_status gambit_scorer_step(gambit_scorer* q, int32_t n, const int32_t* ids
   if (st) return st;
   const gambit_scorer_desc& d = q->d;
   const int D = d.input_dim, dm = d.d_model, f = d.d_ff;
-  float* u0 = wsp<float>(q, q->L.u0);
+  float2* stats = wsp<float2>(q, q->L.stats);
   float* part = wsp<float>(q, q->L.part);
   float* x = wsp<float>(q, q->L.x);
   float* u = wsp<float>(q, q->L.u);
   float* qkv = wsp<float>(q, q->L.qkv);
   float* o = wsp<float>(q, q->L.o);
-  float* a13 = wsp<float>(q, q->L.a13);
   float* g = wsp<float>(q, q->L.g);
   using namespace gambit;
-  SEQ_TRY(q, seq_ln_rows(h, true, u0, D, d.ln_in_g, d.ln_in_b, n, s), "input LN");
-  SEQ_TRY(q, seq_gemm(u0, d.w_in, x, n, dm, D, q->L.splits, kEpiGelu, nullptr, part, s), "input projection");
+  SEQ_TRY(q, seq_row_stats(static_cast<const uint16_t*>(h), D, stats, n, s), "input LN statistics");
+  SEQ_TRY(q, seq_gemm(h, stats, d.ln_in_g, d.ln_in_b, d.w_in, x, n, dm, D, q->L.splits, kEpiGelu, nullptr, part, s),
+          "input projection");
   for (int l = 0; l < d.n_layers; ++l) {
     const size_t dd = (size_t)dm * dm;
     SEQ_TRY(q, seq_ln_rows(x, false, u, dm, d.ln1_g + (size_t)l * dm, d.ln1_b + (size_t)l * dm, n, s), "LN1");
-    SEQ_TRY(q, seq_gemm(u, d.w_qkv + 3 * dd * l, qkv, n, 3 * dm, dm, 1, kEpiNone, nullptr, nullptr, s), "QKV");
+    SEQ_TRY(q, seq_gemm(u, nullptr, nullptr, nullptr, d.w_qkv + 3 * dd * l, qkv, n, 3 * dm, dm, 1, kEpiNone, nullptr,
+                        nullptr, s),
+            "QKV");
     SEQ_TRY(q, seq_attention(q->dev, l, qkv, o, n, s), "attention step");
-    SEQ_TRY(q, seq_gemm(o, d.w_o + dd * l, x, n, dm, dm, 1, kEpiResid, x, nullptr, s), "output projection");
+    SEQ_TRY(q, seq_gemm(o, nullptr, nullptr, nullptr, d.w_o + dd * l, x, n, dm, dm, q->L.out_splits, kEpiResid, x,
+                        part, s),
+            "output projection");
     SEQ_TRY(q, seq_ln_rows(x, false, u, dm, d.ln2_g + (size_t)l * dm, d.ln2_b + (size_t)l * dm, n, s), "LN2");
-    SEQ_TRY(q, seq_gemm(u, d.w_13 + 2 * (size_t)f * dm * l, a13, n, 2 * f, dm, 1, kEpiNone, nullptr, nullptr, s),
-            "SwiGLU in");
-    SEQ_TRY(q, seq_swiglu(a13, g, n, f, s), "SwiGLU");
-    SEQ_TRY(q, seq_gemm(g, d.w_2 + (size_t)f * dm * l, x, n, dm, f, 1, kEpiResid, x, nullptr, s), "SwiGLU out");
+    SEQ_TRY(q, seq_gemm(u, nullptr, nullptr, nullptr, d.w_13 + 2 * (size_t)f * dm * l, g, n, 2 * f, dm, 1,
+                        kEpiSwiGLU, nullptr, nullptr, s),
+            "SwiGLU");
+    SEQ_TRY(q, seq_gemm(g, nullptr, nullptr, nullptr, d.w_2 + (size_t)f * dm * l, x, n, dm, f, q->L.out_splits,
+                        kEpiResid, x, part, s),
+            "SwiGLU out");
   }
   SEQ_TRY(q, seq_head(q->dev, x, scores_out, n, s), "output head");
   for (int i = 0; i < n; ++i) ++q->lens[ids[i]];

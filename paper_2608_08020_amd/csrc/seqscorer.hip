@@ -58,63 +58,152 @@ __global__ __launch_bounds__(256) void ln_rows_kernel(const void* in, int in_bf1
 
 __device__ inline float gelu_erf(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Row statistics of the step states for the input LayerNorm: one workgroup
+// per row, mean, then the mean squared deviation.
+__global__ __launch_bounds__(256) void row_stats_kernel(const uint16_t* h, int dim, float2* stats, int n) {
+  __shared__ float red[4];
+  const int row = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (row >= n) return;
+  const uint16_t* x = h + (size_t)row * dim;
+  const uint2* x4 = reinterpret_cast<const uint2*>(x);  // four bf16 per load (dim % 64 == 0)
+  auto f4 = [](uint2 u, float* o) {
+    o[0] = __uint_as_float(u.x << 16), o[1] = __uint_as_float(u.x & 0xFFFF0000u);
+    o[2] = __uint_as_float(u.y << 16), o[3] = __uint_as_float(u.y & 0xFFFF0000u);
+  };
+  float s = 0.f;
+  for (int i = threadIdx.x; i < dim / 4; i += 256) {
+    float e[4];
+    f4(x4[i], e);
+    s += (e[0] + e[1]) + (e[2] + e[3]);
+  }
+  s = wave_sum(s);
+  if (lane == 0) red[w] = s;
+  __syncthreads();
+  const float mean = (red[0] + red[1] + red[2] + red[3]) / dim;
+  __syncthreads();
+  float v = 0.f;
+  for (int i = threadIdx.x; i < dim / 4; i += 256) {
+    float e[4];
+    f4(x4[i], e);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v += (e[k] - mean) * (e[k] - mean);
+  }
+  v = wave_sum(v);
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) stats[row] = make_float2(mean, 1.f / sqrtf((red[0] + red[1] + red[2] + red[3]) / dim + kSeqLnEps));
+}
+
 // C[M][N] = A[M][K] . W[N][K]^T over K range [z * ks, (z + 1) * ks) of split
-// z = blockIdx.z.  64 x 64 tiles, 16-deep K steps through LDS, 4 x 4 outputs
-// per thread.  One split: the epilogue is applied and C written; several:
-// the raw sums go to part[z][M][N] for seq_reduce_kernel.
-__global__ __launch_bounds__(256) void gemm_kernel(const float* A, const float* W, float* C, int M, int N, int K,
+// z = blockIdx.z, on the fp32 matrix cores (v_mfma_f32_16x16x4f32).  64 x 64
+// tiles staged through LDS 16 deep, the next tile's loads in flight while
+// the current one is multiplied; each of the 4 waves computes a 32 x 32
+// quarter as 2 x 2 products of 16 x 16.  Operands of one product: lane l
+// holds A[l % 16][k + l / 16] and B[k + l / 16][l % 16] = W[l % 16][k + l / 16];
+// result element (4 (l / 16) + r, l % 16) sits in lane l, register r.
+// LN_A: A is the bf16 step states, normalised while staged:
+// (h - mean) * rstd * g[k] + b[k].  One split: the epilogue is applied and C
+// written; several: the raw sums go to part[z][M][N] for seq_reduce_kernel.
+// kEpiSwiGLU: W holds W_1 and W_3 rows interleaved in groups of 16, so a
+// wave's two column blocks are W_1 and W_3 of the same 16 outputs, and
+// C[m][16 c + i] = SiLU(a1) * a3 with row stride N / 2.
+template <bool LN_A>
+__global__ __launch_bounds__(256) void gemm_kernel(const void* Av, const float2* stats, const float* lg,
+                                                   const float* lb, const float* W, float* C, int M, int N, int K,
                                                    int ks, int epi, const float* R, float* part) {
-  __shared__ float As[kBK][kBM + 4];
-  __shared__ float Ws[kBK][kBN + 4];
-  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  __shared__ float As[kBM][kBK + 1];
+  __shared__ float Ws[kBN][kBK + 1];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int m0 = blockIdx.y * kBM, n0 = blockIdx.x * kBN;
   const int k0 = blockIdx.z * ks, k1 = k0 + ks;
   const int lr = tid >> 2, lk = (tid & 3) * 4;  // loader: row lr of the tile, k offset lk
-  float acc[4][4] = {};
-  for (int kb = k0; kb < k1; kb += kBK) {
-    float4 av = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (m0 + lr < M) av = *reinterpret_cast<const float4*>(A + (size_t)(m0 + lr) * K + kb + lk);
-    const float4 wv = *reinterpret_cast<const float4*>(W + (size_t)(n0 + lr) * K + kb + lk);
-    __syncthreads();  // the previous step's reads are done
-    As[lk + 0][lr] = av.x;
-    As[lk + 1][lr] = av.y;
-    As[lk + 2][lr] = av.z;
-    As[lk + 3][lr] = av.w;
-    Ws[lk + 0][lr] = wv.x;
-    Ws[lk + 1][lr] = wv.y;
-    Ws[lk + 2][lr] = wv.z;
-    Ws[lk + 3][lr] = wv.w;
-    __syncthreads();
+  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 32;
+  const int li = lane & 15, lq = lane >> 4;
+  const bool row_ok = m0 + lr < M;
+  float2 st = make_float2(0.f, 0.f);
+  if (LN_A && row_ok) st = stats[m0 + lr];
+  f32x4 acc[2][2];
 #pragma unroll
-    for (int k = 0; k < kBK; ++k) {
-      const float4 a = *reinterpret_cast<const float4*>(&As[k][ty * 4]);
-      const float4 w = *reinterpret_cast<const float4*>(&Ws[k][tx * 4]);
-      const float ar[4] = {a.x, a.y, a.z, a.w}, wr[4] = {w.x, w.y, w.z, w.w};
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(ar[i], wr[j], acc[i][j]);
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float av[4];
+  float4 wv;
+  auto fetch = [&](int kb) {
+    av[0] = av[1] = av[2] = av[3] = 0.f;
+    if (row_ok) {
+      if constexpr (LN_A) {
+        const uint2 hv =
+            *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(Av) + (size_t)(m0 + lr) * K + kb + lk);
+        const float4 g = *reinterpret_cast<const float4*>(lg + kb + lk);
+        const float4 bb = *reinterpret_cast<const float4*>(lb + kb + lk);
+        av[0] = (__uint_as_float(hv.x << 16) - st.x) * st.y * g.x + bb.x;
+        av[1] = (__uint_as_float(hv.x & 0xFFFF0000u) - st.x) * st.y * g.y + bb.y;
+        av[2] = (__uint_as_float(hv.y << 16) - st.x) * st.y * g.z + bb.z;
+        av[3] = (__uint_as_float(hv.y & 0xFFFF0000u) - st.x) * st.y * g.w + bb.w;
+      } else {
+        const float4 a4 =
+            *reinterpret_cast<const float4*>(static_cast<const float*>(Av) + (size_t)(m0 + lr) * K + kb + lk);
+        av[0] = a4.x, av[1] = a4.y, av[2] = a4.z, av[3] = a4.w;
+      }
     }
+    wv = *reinterpret_cast<const float4*>(W + (size_t)(n0 + lr) * K + kb + lk);
+  };
+  fetch(k0);
+  for (int kb = k0; kb < k1; kb += kBK) {
+    __syncthreads();  // the previous step's reads are done
+#pragma unroll
+    for (int e = 0; e < 4; ++e) As[lr][lk + e] = av[e];
+    Ws[lr][lk + 0] = wv.x;
+    Ws[lr][lk + 1] = wv.y;
+    Ws[lr][lk + 2] = wv.z;
+    Ws[lr][lk + 3] = wv.w;
+    __syncthreads();
+    if (kb + kBK < k1) fetch(kb + kBK);
+#pragma unroll
+    for (int kk = 0; kk < kBK; kk += 4) {
+      const float a0 = As[wm + li][kk + lq], a1 = As[wm + 16 + li][kk + lq];
+      const float b0 = Ws[wn + li][kk + lq], b1 = Ws[wn + 16 + li][kk + lq];
+      acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0, acc[0][0], 0, 0, 0);
+      acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b1, acc[0][1], 0, 0, 0);
+      acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b0, acc[1][0], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b1, acc[1][1], 0, 0, 0);
+    }
+  }
+  if (epi == kEpiSwiGLU) {  // one split, no residual
+    const int f = N / 2, c = (n0 + wn) / 32;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + wm + 16 * i + 4 * lq + r;
+        if (m >= M) continue;
+        const float a = acc[i][0][r], b = acc[i][1][r];
+        C[(size_t)m * f + 16 * c + li] = a / (1.f + expf(-a)) * b;
+      }
+    return;
   }
   const bool split = gridDim.z > 1;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = m0 + ty * 4 + i;
-    if (m >= M) break;
-    const size_t o = (size_t)m * N + n0 + tx * 4;
-    float4 r = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
-    if (split) {
-      *reinterpret_cast<float4*>(part + (size_t)blockIdx.z * M * N + o) = r;
-      continue;
-    }
-    if (epi == kEpiGelu) {
-      r.x = gelu_erf(r.x), r.y = gelu_erf(r.y), r.z = gelu_erf(r.z), r.w = gelu_erf(r.w);
-    } else if (epi == kEpiResid) {
-      const float4 q = *reinterpret_cast<const float4*>(R + o);
-      r.x += q.x, r.y += q.y, r.z += q.z, r.w += q.w;
-    }
-    *reinterpret_cast<float4*>(C + o) = r;
-  }
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + wm + 16 * i + 4 * lq + r, n = n0 + wn + 16 * j + li;
+        if (m >= M) continue;
+        const size_t o = (size_t)m * N + n;
+        float v = acc[i][j][r];
+        if (split) {
+          part[(size_t)blockIdx.z * M * N + o] = v;
+          continue;
+        }
+        if (epi == kEpiGelu) v = gelu_erf(v);
+        else if (epi == kEpiResid) v += R[o];
+        C[o] = v;
+      }
 }
 
 // Sum of the splits in split order, then the epilogue.
@@ -129,74 +218,96 @@ __global__ __launch_bounds__(256) void seq_reduce_kernel(const float* part, int 
   C[i] = s;
 }
 
-// g[m][j] = SiLU(a[m][j]) * a[m][f + j]   (a = u W13^T, W1 rows then W3 rows)
-__global__ __launch_bounds__(256) void swiglu_kernel(const float* a, float* g, int n, int f) {
-  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (size_t)n * f) return;
-  const size_t m = i / f, j = i % f;
-  const float x = a[m * 2 * f + j], y = a[m * 2 * f + f + j];
-  g[i] = x / (1.f + expf(-x)) * y;
-}
-
-// One attention step of one (trace row, head), one wave, head_dim 64 (one
-// element per lane).  The trace's step index t is its count of earlier
-// steps.  RoPE rotates (x_i, x_{i+32}) by t * 10000^(-i/32); the rotated key
-// and the value are appended at t in the trace's cache (keys transposed,
-// [64][max_steps], so the score loop reads consecutive steps across lanes;
-// values [max_steps][64]); then softmax over steps 0..t.  Step t's own score
-// and value come from registers, the earlier ones from the cache.
-__global__ __launch_bounds__(64) void seq_attn_kernel(SeqDev S, int layer, const float* qkv, float* o, int n) {
-  extern __shared__ float lds[];  // p[max_steps], q[64]
+// One attention step of one (trace row, head), head_dim 64, four waves.
+// The trace's step index t is its count of earlier steps.  Wave 0 (one
+// element per lane) applies RoPE - (x_i, x_{i+32}) rotated by
+// t * 10000^(-i/32) - and appends the rotated key and the value at t in the
+// trace's cache (keys transposed, [64][max_steps], so the score loop reads
+// consecutive steps across lanes; values [max_steps][64]).  All 256 threads
+// score the earlier steps, the softmax is taken over steps 0..t, and wave w
+// accumulates the values of steps j = w mod 4; the four partial sums and
+// step t's own term (its key and value in wave 0's registers) are added.
+__global__ __launch_bounds__(256) void seq_attn_kernel(SeqDev S, int layer, const float* qkv, float* o, int n) {
+  extern __shared__ float lds[];  // p[max_steps], q[64], partial outputs [4][64], reductions [8]
   float* p = lds;
-  float* qs = lds + S.max_steps;
-  const int row = blockIdx.x / S.n_heads, h = blockIdx.x % S.n_heads, lane = threadIdx.x;
-  if (row >= n) return;
+  float* qs = p + S.max_steps;
+  float* op = qs + 64;
+  float* red = op + 4 * 64;
+  const int row = blockIdx.x / S.n_heads, h = blockIdx.x % S.n_heads;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (row >= n) return;  // uniform over the workgroup
   const int tr = S.ids[row];
   const int t = S.lens[tr];
   if (t >= S.max_steps) {  // the host bounds step counts; keep the cache in bounds regardless
-    if (lane == 0) atomicOr(S.err, 1);
+    if (tid == 0) atomicOr(S.err, 1);
     return;
   }
   const int d = S.d_model;
-  const float* src = qkv + (size_t)row * 3 * d + h * 64;
-  const float q = src[lane], k = src[d + lane], v = src[2 * d + lane];
-  const int i = lane & 31;
-  const float theta = exp2f(-(float)i * (13.287712379549449f / 32.f));  // 10000^(-i/32)
-  float sn, cs;
-  sincosf((float)t * theta, &sn, &cs);
-  const float qp = __shfl_xor(q, 32, 64), kp = __shfl_xor(k, 32, 64);
-  const float qr = lane < 32 ? q * cs - qp * sn : qp * sn + q * cs;
-  const float kr = lane < 32 ? k * cs - kp * sn : kp * sn + k * cs;
   float* kt = S.cache + (((size_t)tr * S.n_layers + layer) * S.n_heads + h) * (size_t)(2 * 64 * S.max_steps);
   float* vc = kt + (size_t)64 * S.max_steps;
-  kt[(size_t)lane * S.max_steps + t] = kr;
-  vc[(size_t)t * 64 + lane] = v;
-  qs[lane] = qr;
+  float v = 0.f;
+  if (wave == 0) {
+    const float* src = qkv + (size_t)row * 3 * d + h * 64;
+    const float q = src[lane], k = src[d + lane];
+    v = src[2 * d + lane];
+    const int i = lane & 31;
+    const float theta = exp2f(-(float)i * (13.287712379549449f / 32.f));  // 10000^(-i/32)
+    float sn, cs;
+    sincosf((float)t * theta, &sn, &cs);
+    const float qp = __shfl_xor(q, 32, 64), kp = __shfl_xor(k, 32, 64);
+    const float qr = lane < 32 ? q * cs - qp * sn : qp * sn + q * cs;
+    const float kr = lane < 32 ? k * cs - kp * sn : kp * sn + k * cs;
+    kt[(size_t)lane * S.max_steps + t] = kr;
+    vc[(size_t)t * 64 + lane] = v;
+    qs[lane] = qr;
+    const float st = wave_sum(qr * kr) * 0.125f;  // scale 1 / sqrt(64)
+    if (lane == 0) red[0] = st;
+  }
   __syncthreads();
-  const float scale = 0.125f;  // 1 / sqrt(64)
-  float mx = wave_sum(qr * kr) * scale;
-  const float st = mx;
-  for (int j = lane; j < t; j += 64) {
+  const float st = red[0];
+  float mx = st;
+  for (int j = tid; j < t; j += 256) {
     float s = 0.f;
-#pragma unroll 8
+#pragma unroll 16
     for (int e = 0; e < 64; ++e) s = fmaf(qs[e], kt[(size_t)e * S.max_steps + j], s);
-    s *= scale;
+    s *= 0.125f;
     p[j] = s;
     mx = fmaxf(mx, s);
   }
   mx = wave_max(mx);
+  __syncthreads();  // red[0] has been read by every thread
+  if (lane == 0) red[wave] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   float sum = 0.f;
-  for (int j = lane; j < t; j += 64) {
+  for (int j = tid; j < t; j += 256) {
     const float e = expf(p[j] - mx);
     p[j] = e;
     sum += e;
   }
-  const float pt = expf(st - mx);
-  sum = wave_sum(sum) + pt;
+  sum = wave_sum(sum);
+  if (lane == 0) red[4 + wave] = sum;
+  __syncthreads();  // p[] and the partial sums are complete
+  // four steps' values in flight per iteration (independent sums)
+  float acc0 = 0.f, acc1 = 0.f, acc2 = 0.f, acc3 = 0.f;
+  int j = wave;
+  for (; j + 12 < t; j += 16) {
+    const float v0 = vc[(size_t)j * 64 + lane], v1 = vc[(size_t)(j + 4) * 64 + lane];
+    const float v2 = vc[(size_t)(j + 8) * 64 + lane], v3 = vc[(size_t)(j + 12) * 64 + lane];
+    acc0 = fmaf(p[j], v0, acc0);
+    acc1 = fmaf(p[j + 4], v1, acc1);
+    acc2 = fmaf(p[j + 8], v2, acc2);
+    acc3 = fmaf(p[j + 12], v3, acc3);
+  }
+  for (; j < t; j += 4) acc0 = fmaf(p[j], vc[(size_t)j * 64 + lane], acc0);
+  op[wave * 64 + lane] = (acc0 + acc1) + (acc2 + acc3);
   __syncthreads();
-  float acc = pt * v;
-  for (int j = 0; j < t; ++j) acc = fmaf(p[j], vc[(size_t)j * 64 + lane], acc);
-  o[(size_t)row * d + h * 64 + lane] = acc / sum;
+  if (wave == 0) {
+    const float pt = expf(st - mx);
+    const float total = red[4] + red[5] + red[6] + red[7] + pt;
+    o[(size_t)row * d + h * 64 + lane] =
+        (op[lane] + op[64 + lane] + op[128 + lane] + op[192 + lane] + pt * v) / total;
+  }
 }
 
 // y = sigmoid(w_out . LN_out(x_row)); the trace's step count advances.
@@ -244,11 +355,21 @@ hipError_t seq_ln_rows(const void* in, bool in_bf16, float* out, int dim, const 
   return hipGetLastError();
 }
 
-hipError_t seq_gemm(const float* A, const float* W, float* C, int M, int N, int K, int splits, int epi,
-                    const float* R, float* part, hipStream_t s) {
+hipError_t seq_row_stats(const uint16_t* h, int dim, float2* stats, int n, hipStream_t s) {
+  hipLaunchKernelGGL(row_stats_kernel, dim3(n), dim3(256), 0, s, h, dim, stats, n);
+  return hipGetLastError();
+}
+
+hipError_t seq_gemm(const void* A, const float2* ln_stats, const float* ln_g, const float* ln_b, const float* W,
+                    float* C, int M, int N, int K, int splits, int epi, const float* R, float* part, hipStream_t s) {
   const int ks = K / splits;
-  hipLaunchKernelGGL(gemm_kernel, dim3(N / kBN, (M + kBM - 1) / kBM, splits), dim3(256), 0, s, A, W, C, M, N, K,
-                     ks, epi, R, part);
+  const dim3 grid(N / kBN, (M + kBM - 1) / kBM, splits);
+  if (ln_stats)
+    hipLaunchKernelGGL(gemm_kernel<true>, grid, dim3(256), 0, s, A, ln_stats, ln_g, ln_b, W, C, M, N, K, ks, epi, R,
+                       part);
+  else
+    hipLaunchKernelGGL(gemm_kernel<false>, grid, dim3(256), 0, s, A, ln_stats, ln_g, ln_b, W, C, M, N, K, ks, epi,
+                       R, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
   const size_t MN = (size_t)M * N;
@@ -257,15 +378,9 @@ hipError_t seq_gemm(const float* A, const float* W, float* C, int M, int N, int 
   return hipGetLastError();
 }
 
-hipError_t seq_swiglu(const float* a, float* g, int n, int f, hipStream_t s) {
-  const size_t total = (size_t)n * f;
-  hipLaunchKernelGGL(swiglu_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a, g, n, f);
-  return hipGetLastError();
-}
-
 hipError_t seq_attention(const SeqDev& S, int layer, const float* qkv, float* o, int n, hipStream_t s) {
-  const size_t lds = sizeof(float) * ((size_t)S.max_steps + 64);
-  hipLaunchKernelGGL(seq_attn_kernel, dim3(n * S.n_heads), dim3(64), lds, s, S, layer, qkv, o, n);
+  const size_t lds = sizeof(float) * ((size_t)S.max_steps + 64 + 4 * 64 + 8);
+  hipLaunchKernelGGL(seq_attn_kernel, dim3(n * S.n_heads), dim3(256), lds, s, S, layer, qkv, o, n);
   return hipGetLastError();
 }
 

@@ -413,6 +413,12 @@ class Pool:
         return int(lib().gambit_free_blocks(self._h))
 
 
+def _interleave16(w1: np.ndarray, w3: np.ndarray) -> np.ndarray:
+    """Rows 32c .. 32c+15 = w1 rows 16c .. 16c+15, rows 32c+16 .. 32c+31 = w3's."""
+    f, d = w1.shape
+    return np.stack([w1.reshape(f // 16, 16, d), w3.reshape(f // 16, 16, d)], axis=1).reshape(2 * f, d)
+
+
 class Scorer:
     """The sequence scorer with per-slot step histories (gambit_scorer_*).
 
@@ -436,7 +442,7 @@ class Scorer:
                   "w_o": f32(stack("Wo")), "w_2": f32(stack("W2")),
                   "w_qkv": f32(np.stack([np.concatenate([x["Wq"], x["Wk"], x["Wv"]]) for x in L]) if L
                                else np.zeros((1, 1), np.float32)),
-                  "w_13": f32(np.stack([np.concatenate([x["W1"], x["W3"]]) for x in L]) if L
+                  "w_13": f32(np.stack([_interleave16(x["W1"], x["W3"]) for x in L]) if L
                               else np.zeros((1, 1), np.float32))}
         self.D, self.d = D, d
         desc = ScorerDesc(D, d, n_heads, len(L), d_ff, max_steps, max_traces,
