@@ -19,6 +19,7 @@ import torch
 
 from oracle import run as orun
 from oracle.probe import rank
+from workload.generate import to_bf16_bits
 
 ATOL, RTOL = 1e-3, 2e-3
 BF16_OUT_REL = 2.0 ** -8
@@ -69,7 +70,10 @@ def compare_tables(run, model, what):
 
 
 def replay(wl, *, sample_steps=None, sample_traces=None, out_dtype=torch.float32, num_blocks=None,
-           share_nodes=True, check_pool_every_step=False, max_splits=0):
+           share_nodes=True, check_pool_every_step=False, max_splits=0, quantise_on_append=False):
+    """quantise_on_append: the steps' new K/V go in as bf16 and the fp8 pool
+    quantises them (the oracle with its own encoder and the landing blocks'
+    scales) instead of arriving as the generator's codes."""
     from paper_2608_08020_amd.runner import PopulationRun, estimate_blocks
 
     t0 = time.time()
@@ -114,8 +118,15 @@ def replay(wl, *, sample_steps=None, sample_traces=None, out_dtype=torch.float32
         run.load_steps(chunk, keep_host=True)
         for s in chunk:
             q, k, v = run.host[s]
-            out = run.decode(s, out_dtype=out_dtype)
-            model.append(ids, k, v)
+            if quantise_on_append:
+                x = to_bf16_bits(wl.step_kv_f32(s))
+                dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()  # noqa: E731
+                out = run.pool.decode_attn_layer(0, run.ids, run.q[s], dev(x[0]), dev(x[1]), new_dtype="bf16",
+                                                 out_dtype=out_dtype)
+                model.append_quantised(ids, x[0], x[1])
+            else:
+                out = run.decode(s, out_dtype=out_dtype)
+                model.append(ids, k, v)
             if s in sample_steps:
                 got = out[traces].float().cpu().numpy()
                 ref = orun.attend(model, wl, q, traces)

@@ -54,6 +54,16 @@ def test_cfg5_fp8_256_traces_sampled():
     replay(wl, sample_steps=steps, sample_traces=[0, 5, 64, 99, 128, 200, 255])
 
 
+@pytest.mark.timeout(900)
+def test_cfg5_fp8_quantise_on_append_sampled():
+    """The fp8 workload with bf16 new K/V quantised by the pool on append
+    (landing block's scale; decode-opened blocks at the append scale) across
+    the first round."""
+    wl = Workload(CONFIGS[5], total_steps=140)
+    replay(wl, sample_steps=[0, 15, 16, 127, 128, 139], sample_traces=[0, 5, 64, 99, 200, 255],
+           quantise_on_append=True)
+
+
 @pytest.mark.timeout(1200)
 def test_cfg4_512_traces_full_size_sampled():
     """The benchmarked workload at full size, in the bench's launch configuration."""
