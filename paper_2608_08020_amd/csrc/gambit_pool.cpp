@@ -1110,7 +1110,7 @@ gambit_status gambit_tournament(gambit_pool* p, int32_t capacity, int32_t swap_k
 }
 
 size_t gambit_mlp_workspace_size(int32_t n, int32_t hidden) {
-  if (n <= 0 || hidden <= 0 || hidden % gambit::kMlpTileH) return 0;
+  if (n <= 0 || hidden <= 0 || hidden % 64) return 0;  // the documented unit multiple
   return 4 * (size_t)n * (hidden / gambit::kMlpTileH);
 }
 
@@ -1118,7 +1118,7 @@ gambit_status gambit_mlp_score(int32_t n, const void* h, const gambit_mlp* mlp, 
                                const int32_t* trace_ids, int32_t keep, int32_t* keep_out, void* workspace,
                                size_t workspace_bytes, void* stream) {
   if (!mlp || !h || !scores_out || n <= 0 || n > gambit::kMaxRank) return GAMBIT_ERR_INVALID;
-  if (mlp->dim <= 0 || mlp->dim % 128 || mlp->hidden <= 0 || mlp->hidden % gambit::kMlpTileH ||
+  if (mlp->dim <= 0 || mlp->dim % 128 || mlp->hidden <= 0 || mlp->hidden % 64 ||
       (mlp->activation != GAMBIT_ACT_RELU && mlp->activation != GAMBIT_ACT_GELU) || !mlp->w1 || !mlp->b1 || !mlp->w2)
     return GAMBIT_ERR_INVALID;
   if (keep < 0 || keep > n || (keep > 0 && (!trace_ids || !keep_out))) return GAMBIT_ERR_INVALID;

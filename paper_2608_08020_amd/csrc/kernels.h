@@ -191,7 +191,7 @@ constexpr int kMaxRank = 4096;  // largest population the in-LDS ranking handles
 // bias, activation and the w2 product applied in the tile, then one
 // workgroup sums the tiles' partial logits in a fixed order, applies the
 // sigmoid and (keep > 0) ranks the top `keep` ids.
-constexpr int kMlpTileT = 16, kMlpTileH = 64;
+constexpr int kMlpTileT = 32, kMlpTileH = 32;
 struct MlpLaunch {
   int32_t n, dim, hidden, act;   // act: 0 ReLU, 1 GELU (erf)
   const uint16_t* h;             // [n][dim] bf16
@@ -199,7 +199,7 @@ struct MlpLaunch {
   const float* b1;               // [hidden]
   const float* w2;               // [hidden]
   float b2;
-  float* parts;                  // [hidden / 64][n] partial logits
+  float* parts;                  // [hidden / kMlpTileH][n] partial logits
   float* scores_out;             // [n]
   const int32_t* ids;            // [n] or NULL (ranking only)
   int32_t keep;
