@@ -15,11 +15,19 @@
 //    streams its chunk 32 tokens at a time straight from HBM into matrix-core
 //    operand registers, double-buffered, with no LDS and no barrier (this is
 //    where most of the bytes are: chunks that 1-4 traces share).
-//  * cooperative: one chunk with 2-4 row blocks (more rows become several
-//    workgroups).  The workgroup stages each 32-token tile into LDS once
-//    (double-buffered) and each wave applies it to its row block, so a chunk
-//    is read from L2/HBM once per four row blocks instead of once per row
-//    block.
+//  * cooperative: one chunk with 2-8 row blocks (more rows become several
+//    workgroups, placed on one XCD so their re-reads hit its L2).  The
+//    workgroup streams 32-token tiles into a 4-stage LDS ring by direct
+//    global-to-LDS loads, three tiles ahead, and each wave applies a tile to
+//    its one or two row blocks, so a chunk is read once per up to eight row
+//    blocks instead of once per row block.
+//
+// The launch also performs the decode step's append: the unit that covers
+// a trace's last block writes the new token's K and V there (quantising
+// bf16 input to E4M3FN for fp8 pools when asked), and enters a block the
+// token opens - chosen by the host by the allocation rule and passed in the
+// launch arguments - into the block table, refcounts and free set.  The
+// merge kernel then advances the lengths.
 //
 // The contractions run on the bf16 matrix cores (v_mfma_f32_16x16x32_bf16):
 //   S^T[token][row] = K[token][:] . Q[row][:]          (A = K, B = Q^T)
