@@ -53,9 +53,24 @@ __device__ inline float probe_dot(const uint16_t* h, const float* w, int Dh, int
 }
 
 // Sort keys[0..N) descending (N a power of two) with all threads of the block.
+__device__ inline uint64_t shfl_xor64(uint64_t v, int m) {
+  const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m, 64);
+  const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m, 64);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Bitonic sort, descending, of keys[0 .. N) (N a power of two) by the
+// workgroup.  Compare-exchange stages whose partners are 128 or more apart
+// go through LDS with a barrier each; the rest of a merge step stays inside
+// 128-key blocks, which one wave holds in registers (keys base + lane and
+// base + 64 + lane): distance 64 pairs a lane's two keys, shorter distances
+// pair lanes by shuffles - one LDS round trip and one barrier for all of
+// them.  Keys past N (when N < 128) pair only among themselves.
 __device__ void bitonic_desc(uint64_t* keys, int N) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   for (int k = 2; k <= N; k <<= 1) {
-    for (int j = k >> 1; j > 0; j >>= 1) {
+    int j = k >> 1;
+    for (; j >= 128; j >>= 1) {
       for (int i = threadIdx.x; i < N; i += blockDim.x) {
         const int ixj = i ^ j;
         if (ixj > i) {
@@ -69,6 +84,28 @@ __device__ void bitonic_desc(uint64_t* keys, int N) {
       }
       __syncthreads();
     }
+    for (int base = 128 * wave; base < N; base += 128 * nw) {
+      const int ia = base + lane, ib = ia + 64;
+      uint64_t a = keys[ia], b = keys[ib];
+      const bool desc_a = (ia & k) == 0, desc_b = (ib & k) == 0;
+      for (int jj = j; jj > 0; jj >>= 1) {
+        if (jj == 64) {  // a (index ia) is the lower of the pair (ia, ib); k >= 128 here
+          if (desc_a ? (a < b) : (a > b)) {
+            const uint64_t t = a;
+            a = b;
+            b = t;
+          }
+        } else {
+          const uint64_t pa = shfl_xor64(a, jj), pb = shfl_xor64(b, jj);
+          const bool lower = (lane & jj) == 0;
+          a = (lower == desc_a) ? (a > pa ? a : pa) : (a < pa ? a : pa);
+          b = (lower == desc_b) ? (b > pb ? b : pb) : (b < pb ? b : pb);
+        }
+      }
+      keys[ia] = a;
+      keys[ib] = b;
+    }
+    __syncthreads();
   }
 }
 
