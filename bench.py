@@ -338,6 +338,7 @@ def main():
     ap.add_argument("--layers", type=int, default=64)
     ap.add_argument("--scorer-only", action="store_true", help="time only the sequence scorer and print it")
     ap.add_argument("--mlp-only", action="store_true", help="time only the MLP scorer and print it")
+    ap.add_argument("--tournament-only", action="store_true", help="time only the tournament rounds and print them")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path shards by "
@@ -351,6 +352,9 @@ def main():
         return
     if args.mlp_only:
         print(json.dumps({"mlp_scorer": mlp_measure()}), flush=True)
+        return
+    if args.tournament_only:
+        print(json.dumps({"tournament": tournament_rounds()}), flush=True)
         return
 
     from paper_2608_08020_amd.runner import PopulationRun
