@@ -379,11 +379,14 @@ def main():
     out = torch.empty((T, cfg.n_q_heads, cfg.head_dim), dtype=torch.bfloat16, device="cuda")
     round_of = {s: i for i, s in enumerate(rounds)}
 
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
     for s in range(W):
         run.decode(s, out=out)
         if s in round_of:
             run.round(round_of[s])
     torch.cuda.synchronize()
+    warm_wall = time.perf_counter() - w0
     log(f"warm-up {W} steps done")
 
     e = cfg.kv_elem_bytes
@@ -391,6 +394,7 @@ def main():
     pool = run.pool
     pool.profile_begin(K)
     alg_bytes, ctx_tokens = [], 0
+    round_ev = []  # (start, end) events around each probe / rank / prune / branch round
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -404,7 +408,11 @@ def main():
                          + T * Hq * D * 2 + 4 * st.table_entries + 2 * T * Hkv * D * 2 * e)
         ctx_tokens += st.total_tokens
         if s in round_of:
+            r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            r0.record()
             run.round(round_of[s])
+            r1.record()
+            round_ev.append((r0, r1))
     end.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -441,6 +449,12 @@ def main():
                      "alg_bytes_per_launch": round(bytes_per_launch),
                      "avg_launch_us": round(attn_avg_s * 1e6, 2), "launches_timed": launches},
         "step_hbm_GBps": round(sum(alg_bytes) / wall / 1e9, 1),
+        # context: dense per-trace attention would read every trace's whole context
+        "naive_bytes_per_step": round(ctx_tokens / K * Hkv * D * 2 * e),
+        "whole_run": {"steps": W + K, "trace_steps_per_s": round(T * (W + K) / (warm_wall + wall), 1),
+                      "first_interval_ms_per_step": round(warm_wall * 1e3 / max(W, 1), 4),
+                      "note": "includes the first interval (plans for the initial tree, first round)"},
+        "round_us": [round(a.elapsed_time(b) * 1e3, 1) for a, b in round_ev],
         "event_ms_per_step": round(ev_ms / K, 4),
     }
     if not args.no_tournament:

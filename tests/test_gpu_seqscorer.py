@@ -116,3 +116,21 @@ def test_errors_change_nothing():
     # a freed slot starts a fresh history
     got = gpu.step([0], _bf16(H[5:6])).cpu().numpy()[0]
     assert abs(got - ref.step([0], bf16_to_f64(H[5:6]))[0]) <= TOL
+
+
+def test_no_layers_and_single_step_capacity():
+    """The scorer without Transformer layers (input LN, projection, GELU,
+    output head) and a history capacity of one step."""
+    import dataclasses
+    cfg = dataclasses.replace(SEQ_SMALL, n_layers=0, max_steps=1, slots=5)
+    w = weights(cfg)
+    gpu = Scorer(w, n_heads=cfg.n_heads, max_steps=1, max_traces=cfg.slots)
+    H = step_states(cfg, 3)[:5]
+    got = gpu.step(list(range(5)), _bf16(H)).cpu().numpy()
+    for t in range(5):
+        assert abs(got[t] - scorer_outputs(w, bf16_to_f64(H[t:t + 1]), cfg.n_heads)[-1]) <= TOL
+    with pytest.raises(GambitError):  # full
+        gpu.step([0], _bf16(H[:1]))
+    gpu.free([0])
+    assert gpu.steps(0) == 0 and gpu.steps(1) == 1
+    gpu.check()
