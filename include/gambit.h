@@ -4,9 +4,9 @@
  *
  * A population of reasoning traces decodes in lock step.  Their KV caches
  * live in one pool of fixed-size blocks; a trace is a row of block ids.
- * Branching spawns a child from its parent's prefix by sharing the parent's
- * KV blocks (Alg. 1 notation, "Branch"; Sec. 4.1 Case 2: the child inherits
- * the parent's KV-cache through prefix caching), and pruning frees the
+ * Branching starts a child from its parent's prefix by sharing the parent's
+ * KV blocks (Alg. 1 notation, Branch; Sec. 4.1 Case 2: the child reuses its
+ * parent's cached KV, the prefix-caching mechanism), and pruning frees the
  * blocks nobody else references (Sec. 4.1 Case 2).  Every decode step
  * appends one token per trace and attends over the whole context; blocks
  * shared by several traces are read from HBM once per step for all of them.

@@ -29,7 +29,7 @@ Contents and the passages each part follows:
                   lowest-free-first block allocation, fork = share full
                   blocks + copy the partial tail, free = drop references
                   (Sec. 4.1 Case 2: pruning frees the non-shared blocks, the
-                  child inherits the parent's KV through prefix caching);
+                  child reuses its parent's KV by prefix caching);
                   a decode step's bf16 K/V quantised into fp8 blocks with the
                   landing block's scale.
 * ``tournament`` - the full tournament of Alg. 1 over the pool model:

@@ -1,8 +1,8 @@
 """The 2-layer MLP scorer on a thought-boundary hidden state.  Test
 infrastructure only.
 
-The paper's main evaluation scores traces with STEP's off-the-shelf
-2-layer MLP on the last-layer hidden state h at a thought boundary (Sec. 4.1
+The paper's main evaluation scores traces with STEP's ready-made two-layer
+MLP on the last-layer hidden state h at a thought boundary (Sec. 4.1
 and Sec. 5.1: f_theta takes h_{i,j} and returns a score in [0, 1]); it gives
 no dimensions, activation or weights.  This module states the plain form:
 

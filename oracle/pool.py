@@ -5,15 +5,15 @@ Two things are modelled, independently of each other:
 1. The token sequence of every trace (what attention reads).  A trace's
    content is a list of runs over its positions; fork gives the child its
    own copy of the parent's list (the per-trace copy the method avoids on
-   the GPU; Sec. 4.1 Case 2: the child inherits the parent's KV).
+   the GPU; Sec. 4.1 Case 2: the child reuses its parent's KV).
 2. The physical block bookkeeping (what the block tables must say):
 
    * allocation takes the lowest free block id; requests are served in the
      call's list order and, within a trace, in ascending logical index;
    * fork: the child row lists the parent's full blocks (each refcount + 1);
      a partial last block is copied into one newly allocated block; the
-     child's length equals the parent's (Alg. 1 notation: Branch spawns a
-     child from the parent's prefix via KV-cache sharing);
+     child's length equals the parent's (Alg. 1 notation: Branch starts the
+     child from its parent's prefix, whose KV it shares);
    * free: every referenced block loses one reference and becomes free at
      zero; the row empties and the length drops to 0 (Sec. 4.1 Case 2:
      pruning frees the non-shared blocks);
