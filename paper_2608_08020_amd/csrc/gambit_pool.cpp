@@ -12,12 +12,14 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
 #include <numeric>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "../../include/gambit.h"
@@ -172,6 +174,32 @@ T* ws_ptr(gambit_pool* p, size_t off) {
   return reinterpret_cast<T*>(p->ws + off);
 }
 
+// Runs f(0) .. f(n - 1) on up to 8 host threads (the calling one included),
+// in chunks of 16 indices; serially for small n or if no thread can start.
+template <class F>
+void parallel_for(int n, F&& f) {
+  const int nt = (int)std::min(8u, std::max(1u, std::thread::hardware_concurrency()));
+  if (n < 128 || nt == 1) {
+    for (int i = 0; i < n; ++i) f(i);
+    return;
+  }
+  std::atomic<int> next{0};
+  auto body = [&]() {
+    for (int i; (i = next.fetch_add(16, std::memory_order_relaxed)) < n;)
+      for (int k = i, e = std::min(n, i + 16); k < e; ++k) f(k);
+  };
+  std::vector<std::thread> th;
+  for (int t = 1; t < nt; ++t) {
+    try {
+      th.emplace_back(body);
+    } catch (...) {
+      break;
+    }
+  }
+  body();
+  for (auto& x : th) x.join();
+}
+
 // ---- host mirror -----------------------------------------------------------
 int take_lowest(gambit_pool* p) {
   for (size_t w = p->hint; w < p->freebits.size(); ++w) {
@@ -202,17 +230,31 @@ void mirror_grow(gambit_pool* p, int t, int ntok) {
   p->seq_len[t] = L + ntok;
 }
 
-void mirror_fork(gambit_pool* p, int parent, int child) {
-  const int L = p->seq_len[parent];
-  const int full = L / 16;
-  auto& c = p->table[child];
-  c.assign(p->table[parent].begin(), p->table[parent].begin() + full);
-  for (int b : c) ++p->refcount[b];
-  p->seq_len[child] = full * 16;
-  mirror_grow(p, child, L % 16);
-  p->nscore[child] = p->nscore[parent];
-  p->gen[child] = 0;
-  p->ghost[child] = 0;
+// Forks of distinct children (none of them a parent of another), in pair
+// order.  The children's rows copy the parents' full blocks; a parent that
+// several consecutive pairs share adds all their references to each of its
+// blocks in one pass.  The partial tails then follow in pair order, which
+// decides the blocks they get.
+void mirror_fork_many(gambit_pool* p, const int32_t* parents, const int32_t* children, int n) {
+  for (int i = 0; i < n;) {
+    const int par = parents[i];
+    int e = i + 1;
+    while (e < n && parents[e] == par) ++e;
+    const int full = p->seq_len[par] / 16;
+    const auto& prow = p->table[par];
+    for (int k = i; k < e; ++k) p->table[children[k]].assign(prow.begin(), prow.begin() + full);
+    for (int j = 0; j < full; ++j) p->refcount[prow[j]] += e - i;
+    i = e;
+  }
+  for (int i = 0; i < n; ++i) {
+    const int par = parents[i], ch = children[i];
+    const int L = p->seq_len[par];
+    p->seq_len[ch] = L / 16 * 16;
+    mirror_grow(p, ch, L % 16);
+    p->nscore[ch] = p->nscore[par];
+    p->gen[ch] = 0;
+    p->ghost[ch] = 0;
+  }
 }
 
 void mirror_release_rows(gambit_pool* p, int t) {
@@ -223,11 +265,14 @@ void mirror_release_rows(gambit_pool* p, int t) {
   p->gen[t] = 0;
 }
 
-// The trace ends (pruned, completed, or a ghost leaving the tree view).
-void mirror_free(gambit_pool* p, int t) {
-  mirror_release_rows(p, t);
-  p->nscore[t] = 0;
-  p->ghost[t] = 0;
+// Distinct traces end (pruned, completed, or ghosts leaving the tree view).
+void mirror_free_many(gambit_pool* p, const int32_t* ids, int n) {
+  for (int i = 0; i < n; ++i) {
+    const int t = ids[i];
+    mirror_release_rows(p, t);
+    p->nscore[t] = 0;
+    p->ghost[t] = 0;
+  }
 }
 
 // The scheduler evicts the trace: no KV, but it stays in the tree view.
@@ -274,9 +319,9 @@ gambit_status check_ids(gambit_pool* p, int32_t n, const int32_t* ids, const cha
 // ends at the trace's current last block (read by the kernel at run time),
 // so the plan stays valid while decode steps append.
 struct Group {
-  std::vector<AttnUnit> coop;    // cooperative items (one workgroup each)
-  std::vector<AttnUnit> narrow;  // one-row-block units
   double cost;
+  int32_t first, count;  // its units in the plan's unit list
+  bool coop;             // cooperative items (one workgroup each), else one narrow unit
 };
 
 gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t s) {
@@ -328,28 +373,41 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
   std::vector<Run> runs;
   std::vector<std::vector<int32_t>> mem;
   std::vector<int32_t> starts;
-  for (int pos = 0; pos < n; ++pos) {
+  // the scan of every row for its runs, in parallel over positions
+  std::vector<std::vector<Run>> pos_runs(n);
+  parallel_for(n, [&](int pos) {
     const auto& row = p->table[ids[pos]];
-    run_off[pos] = (int)runs.size();
+    auto& out = pos_runs[pos];
     int j = 0;
     while (j < nb[pos]) {
       const int c = cnt[row[j]];
       if (c == 1) {
-        runs.push_back(Run{j, nb[pos], 1, -1});
+        out.push_back(Run{j, nb[pos], 1, -1});
         break;
       }
       int j1 = j + 1;
       while (j1 < nb[pos] && cnt[row[j1]] == c) ++j1;
-      const int b0 = row[j];
-      if (p->first[b0] < 0) {
-        p->first[b0] = (int)mem.size();
-        mem.emplace_back();
-        mem.back().reserve(c);
-        starts.push_back(b0);
-      }
-      mem[p->first[b0]].push_back(pos);
-      runs.push_back(Run{j, j1, c, p->first[b0]});
+      out.push_back(Run{j, j1, c, -1});
       j = j1;
+    }
+  });
+  // member lists of the shared runs, in position order
+  for (int pos = 0; pos < n; ++pos) {
+    const auto& row = p->table[ids[pos]];
+    run_off[pos] = (int)runs.size();
+    for (Run R : pos_runs[pos]) {
+      if (R.c > 1) {
+        const int b0 = row[R.j0];
+        if (p->first[b0] < 0) {
+          p->first[b0] = (int)mem.size();
+          mem.emplace_back();
+          mem.back().reserve(R.c);
+          starts.push_back(b0);
+        }
+        mem[p->first[b0]].push_back(pos);
+        R.rid = p->first[b0];
+      }
+      runs.push_back(R);
     }
   }
   run_off[n] = (int)runs.size();
@@ -357,11 +415,13 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
   for (int b : touched) p->cnt[b] = 0;
 
   std::vector<Group> groups;
+  std::vector<AttnUnit> gunits;  // the groups' units, contiguous per group
   std::vector<int32_t> members;
   std::vector<int32_t> nk(n, 0);
   gambit_status st = GAMBIT_OK;
   for (int chunk_blocks = kDefaultChunkBlocks;; chunk_blocks *= 2) {
     groups.clear();
+    gunits.clear();
     members.clear();
     int worst = 0;
     // One group per (chunk, KV head): a chunk with <= 16 rows is one narrow
@@ -373,23 +433,21 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
       const double tok = std::max(ntok_est, 1);
       if (mcnt * p->g <= gambit::kRowsPerUnit) {
         for (int h = 0; h < Hkv; ++h) {
-          Group gr;
-          gr.cost = tok;
-          gr.narrow.push_back(AttnUnit{ids[owner_pos], jb0, nblk, h, moff, mcnt, kidx, 0});
-          groups.push_back(std::move(gr));
+          groups.push_back(Group{tok, (int32_t)gunits.size(), 1, false});
+          gunits.push_back(AttnUnit{ids[owner_pos], jb0, nblk, h, moff, mcnt, kidx, 0});
         }
         return;
       }
       const int item_members = gambit::kRowsPerCoop / p->g;
       for (int h = 0; h < Hkv; ++h) {
-        Group gr;
-        gr.cost = 0;
+        Group gr{0.0, (int32_t)gunits.size(), 0, true};
         for (int m0 = 0; m0 < mcnt; m0 += item_members) {
           const int mc = std::min(item_members, mcnt - m0);
-          gr.coop.push_back(AttnUnit{ids[owner_pos], jb0, nblk, h, moff + m0, mc, kidx, gambit::kUnitCoop});
+          gunits.push_back(AttnUnit{ids[owner_pos], jb0, nblk, h, moff + m0, mc, kidx, gambit::kUnitCoop});
+          ++gr.count;
           gr.cost += tok * (2.0 + 4.0 * mc * p->g / 64.0);  // staging + compute per row
         }
-        groups.push_back(std::move(gr));
+        groups.push_back(gr);
       }
     };
     for (int pos = 0; pos < n; ++pos) {
@@ -457,13 +515,16 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
   // the long ones, and one that starts late ends the launch late (measured:
   // 853 vs 858 us at 512 traces; 50% starts too few narrow units early).
   std::vector<AttnUnit> units;
+  units.reserve(4 * gunits.size() + 8 * gambit::kUnitsPerWG);  // a cooperative item fills a 4-entry slot
   const AttnUnit empty{0, 0, 0, 0, 0, 0, 0, 0};
+  std::vector<AttnUnit> C, N;
   for (int x = 0; x < 8; ++x) {
     p->xcd_off[x] = (int)units.size();
-    std::vector<AttnUnit> C, N;
+    C.clear();
+    N.clear();
     for (int gi : per[x]) {
-      C.insert(C.end(), groups[gi].coop.begin(), groups[gi].coop.end());
-      N.insert(N.end(), groups[gi].narrow.begin(), groups[gi].narrow.end());
+      const Group& g = groups[gi];
+      (g.coop ? C : N).insert((g.coop ? C : N).end(), gunits.begin() + g.first, gunits.begin() + g.first + g.count);
     }
     const long nC = (long)C.size(), nN = cdiv((int)N.size(), gambit::kUnitsPerWG);
     long ci = 0, ni = 0;
@@ -742,7 +803,7 @@ gambit_status gambit_kv_fork(gambit_pool* p, int32_t n, const int32_t* parents, 
   HIP_TRY(p, gambit::launch_fork(p->dev, dp, n, ws_ptr<int32_t>(p, p->L.req_trace),
                                  ws_ptr<int32_t>(p, p->L.req_ntok), S(stream)),
           "fork kernels");
-  for (int i = 0; i < n; ++i) mirror_fork(p, parents[i], children[i]);
+  mirror_fork_many(p, parents, children, n);
   invalidate_plan(p);
   return GAMBIT_OK;
 }
@@ -760,7 +821,7 @@ gambit_status gambit_kv_free(gambit_pool* p, int32_t n, const int32_t* ids, void
   st = upload_ints(p, d, ids, n, S(stream));
   if (st) return st;
   HIP_TRY(p, gambit::launch_free(p->dev, d, n, gambit::kFreeEnd, S(stream)), "free kernel");
-  for (int i = 0; i < n; ++i) mirror_free(p, ids[i]);
+  mirror_free_many(p, ids, n);
   invalidate_plan(p);
   return GAMBIT_OK;
 }
@@ -962,8 +1023,10 @@ gambit_status gambit_score_prune_branch(gambit_pool* p, int32_t n, const int32_t
   HIP_TRY(p, gambit::launch_fork(p->dev, child_parent_out, nfree_traces, ws_ptr<int32_t>(p, p->L.req_trace),
                                  ws_ptr<int32_t>(p, p->L.req_ntok), s),
           "fork kernels");
-  for (int t : freed) mirror_free(p, t);
-  for (int j = 0; j < nfree_traces; ++j) mirror_fork(p, kept[j / c], freed[j]);
+  std::vector<int32_t> par(nfree_traces);
+  for (int j = 0; j < nfree_traces; ++j) par[j] = kept[j / c];
+  mirror_free_many(p, freed.data(), nfree_traces);
+  mirror_fork_many(p, par.data(), freed.data(), nfree_traces);
   invalidate_plan(p);
   return GAMBIT_OK;
 }
@@ -1097,8 +1160,13 @@ gambit_status gambit_tournament(gambit_pool* p, int32_t capacity, int32_t swap_k
   HIP_TRY(p, gambit::launch_fork(p->dev, out + gambit::kTournHeader + T, m, ws_ptr<int32_t>(p, p->L.req_trace),
                                  ws_ptr<int32_t>(p, p->L.req_ntok), s),
           "fork kernels");
-  for (int i = 0; i < npr; ++i) mirror_free(p, pr[i]);
-  for (int j = 0; j < m; ++j) mirror_fork(p, pairs[2 * j + 1], pairs[2 * j]);
+  mirror_free_many(p, pr, npr);
+  std::vector<int32_t> fork_par(m), fork_ch(m);
+  for (int j = 0; j < m; ++j) {
+    fork_ch[j] = pairs[2 * j];
+    fork_par[j] = pairs[2 * j + 1];
+  }
+  mirror_fork_many(p, fork_par.data(), fork_ch.data(), m);
   invalidate_plan(p);
   round_out->case_taken = kase;
   round_out->n_active = N;
