@@ -263,3 +263,37 @@ def test_many_blocks_opened_in_one_step(kv_dtype):
         fill(t, 32)
     step(rng.permutation(T))        # 100 opened, claimed by the attention launch
     step(rng.permutation(T)[:150])  # a partial list
+
+
+@pytest.mark.parametrize("opening", [256, 257])
+def test_launch_argument_capacity_boundary(opening):
+    """Exactly as many new blocks as one launch carries (256: claimed by the
+    attention launch) and one more (257: the allocator kernel runs first)."""
+    from oracle.pool import PoolModel
+
+    T, Hq, Hkv = 300, 4, 1
+    rng = np.random.default_rng(12 + opening)
+    p = Pool(num_blocks=800, num_q_heads=Hq, num_kv_heads=Hkv, max_traces=T, max_blocks_per_trace=3)
+    om = PoolModel(num_blocks=800, n_kv_heads=Hkv, head_dim=128, kv_dtype="bf16", max_traces=T,
+                   max_blocks_per_trace=3)
+    for t in range(T):
+        L = 16 if t < opening else 9
+        kv = to_bf16_bits(rng.standard_normal((L, Hkv, 128)).astype(np.float32))
+        dev = torch.from_numpy(kv.view(np.int16)).view(torch.bfloat16).to(DEV)
+        p.kv_alloc([t], [L])
+        p.kv_write(t, 0, dev, dev)
+        om.alloc([t], [L])
+        om.write(t, 0, kv, kv)
+    ids = rng.permutation(T)
+    q = to_bf16_bits(rng.standard_normal((T, Hq, 128)).astype(np.float32))
+    kn = to_bf16_bits(rng.standard_normal((T, Hkv, 128)).astype(np.float32))
+    bf = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(DEV)  # noqa: E731
+    out = p.decode_attn(ids, bf(q), bf(kn), bf(kn), out_dtype=torch.float32).cpu().numpy()
+    om.append(ids, kn, kn)
+    assert np.array_equal(p.block_table.cpu().numpy(), om.table_array())
+    assert p.seq_len.cpu().numpy().tolist() == om.seq_len
+    for i in (0, 99, T - 1):
+        K, V = om.materialise(int(ids[i]))
+        ref = decode_attention(bf16_to_f64(q[i]), K, V, 1 / math.sqrt(128))
+        assert np.abs(out[i] - ref).max() <= 1e-3 + 2e-3 * np.abs(ref).max()
+    p.pool_check()
