@@ -1,5 +1,6 @@
 """The C-ABI library loads on a machine without a GPU and exports every
 entry point include/gambit.h declares; host-only queries work."""
+import ctypes
 import os
 import re
 
@@ -34,11 +35,13 @@ def test_workspace_size_validates_descriptions():
     from paper_2608_08020_amd import gambit
     if not os.path.exists(gambit.LIB_PATH):
         pytest.skip("libgambit.so not built")
-    d = gambit.PoolDesc(1000, 16, 32, 8, 128, 0, 64, 100, 0, 0.0, 1, 1, None, 1, 1, 1, None, 0)
+    d = gambit.PoolDesc(num_blocks=1000, block_size=16, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                        kv_dtype=0, max_traces=64, max_blocks_per_trace=100, max_splits=0, fp8_append_scale=0.0,
+                        num_layers=1)
     ok = gambit.workspace_size(d)
     assert ok > 0
     for field, bad in [("head_dim", 64), ("block_size", 32), ("num_q_heads", 12), ("kv_dtype", 7),
-                       ("num_blocks", 0)]:
+                       ("num_blocks", 0), ("num_layers", -1), ("num_layers", 5000)]:
         d2 = gambit.PoolDesc.from_buffer_copy(d)
         setattr(d2, field, bad)
         assert gambit.workspace_size(d2) == 0, field
@@ -50,3 +53,24 @@ def test_workspace_size_validates_descriptions():
     d3.max_splits = 65
     assert gambit.workspace_size(d3) == 0
     assert gambit.lib().gambit_status_str(-2).decode() == "out of KV blocks"
+
+
+def test_scorer_workspace_size_validates_descriptions():
+    from paper_2608_08020_amd import gambit
+    if not os.path.exists(gambit.LIB_PATH):
+        pytest.skip("libgambit.so not built")
+    L = gambit.lib()
+    d = gambit.ScorerDesc(input_dim=4096, d_model=256, n_heads=4, n_layers=2, d_ff=768, max_steps=256,
+                          max_traces=512)
+    ok = int(L.gambit_scorer_workspace_size(ctypes.byref(d)))
+    # the per-slot key / value caches dominate: 512 x 2 layers x 4 heads x 2 x 64 x 256 fp32
+    assert ok >= 512 * 2 * 4 * 2 * 64 * 256 * 4
+    for field, bad in [("d_model", 200), ("n_heads", 3), ("input_dim", 100), ("d_ff", 100), ("max_steps", 0),
+                       ("max_steps", 9000), ("n_layers", -1), ("max_traces", 0)]:
+        d2 = gambit.ScorerDesc.from_buffer_copy(d)
+        setattr(d2, field, bad)
+        assert int(L.gambit_scorer_workspace_size(ctypes.byref(d2))) == 0, field
+    # no layers: no caches
+    d3 = gambit.ScorerDesc.from_buffer_copy(d)
+    d3.n_layers = 0
+    assert 0 < int(L.gambit_scorer_workspace_size(ctypes.byref(d3))) < ok
