@@ -640,32 +640,6 @@ __device__ void narrow_unit(const DevPool& P, const AttnLaunch& A, const AttnUni
 }
 
 // ----------------------------------------------------------- cooperative --
-// Staging registers of one 32-token tile: each of the 256 threads moves two
-// 16-byte chunks of K and two of V (bf16), or one of each (fp8).
-template <bool FP8>
-struct Stage {
-  uint4 k[FP8 ? 1 : 2], v[FP8 ? 1 : 2];
-};
-
-template <bool FP8>
-__device__ inline void stage_load(const DevPool& P, int kvh, const TileMeta& m, Stage<FP8>& s) {
-  const int t = threadIdx.x;
-  if constexpr (!FP8) {
-    // chunk t of each block's K and V tile (4096 bytes = 256 chunks)
-    const size_t o0 = head_off<false>(m.b0, P.Hkv, kvh) + t * 16;
-    const size_t o1 = head_off<false>(m.b1, P.Hkv, kvh) + t * 16;
-    s.k[0] = *reinterpret_cast<const uint4*>(P.k_cache + o0);
-    s.v[0] = *reinterpret_cast<const uint4*>(P.v_cache + o0);
-    s.k[1] = *reinterpret_cast<const uint4*>(P.k_cache + o1);
-    s.v[1] = *reinterpret_cast<const uint4*>(P.v_cache + o1);
-  } else {
-    // chunk t % 128 of block t / 128 (2048-byte fp8 tiles)
-    const size_t o = head_off<true>(t < 128 ? m.b0 : m.b1, P.Hkv, kvh) + (t & 127) * 16;
-    s.k[0] = *reinterpret_cast<const uint4*>(P.k_cache + o);
-    s.v[0] = *reinterpret_cast<const uint4*>(P.v_cache + o);
-  }
-}
-
 __device__ inline int lds_v(int blk, int d, int half) { return kLdsV + blk * kTileBytes + half * 2048 + d * 16; }
 
 // bf16 tiles reach LDS by direct global->LDS loads (no registers): a ring of
@@ -709,6 +683,16 @@ __device__ inline void dma4(const void* g, void* l) {
 
 constexpr int kIdsBytes = 2 * 64 * 4;  // two windows of 64 block ids
 
+// fp8 stage: the raw tiles (K of both blocks, then V^T of both, 2 KiB each,
+// in the cache's own layout) and the tile's block scales (K0, V0, K1, V1,
+// repeated over 256 bytes).  Half the bytes of a bf16 tile, so the ring is
+// deeper for the same bytes in flight.
+constexpr int kMeta8 = 4 * 2048;
+constexpr int kStage8 = kMeta8 + 256;
+constexpr int kRing8 = 7;
+constexpr int kAhead8 = 6;
+static_assert(kAhead8 < kRing8 && kAhead8 <= 6, "ring depth and the waits' range");
+
 // Waits until at most `later` tiles' direct loads of this wave are still in
 // flight (loads retire in issue order).
 __device__ inline void wait_tiles(int later) {
@@ -722,50 +706,40 @@ __device__ inline void wait_tiles(int later) {
     __builtin_amdgcn_s_waitcnt(0x0F70);
 }
 
+// The same for PER direct loads per tile and up to 5 later tiles.
+template <int PER>
+__device__ inline void wait_tiles_per(int later) {
+  static_assert(5 * PER <= 15, "vmcnt immediate");
+  switch (later) {
+    case 0: __builtin_amdgcn_s_waitcnt(0x0F70); break;
+    case 1: __builtin_amdgcn_s_waitcnt(0x0F70 | PER); break;
+    case 2: __builtin_amdgcn_s_waitcnt(0x0F70 | (2 * PER)); break;
+    case 3: __builtin_amdgcn_s_waitcnt(0x0F70 | (3 * PER)); break;
+    case 4: __builtin_amdgcn_s_waitcnt(0x0F70 | (4 * PER)); break;
+    default: __builtin_amdgcn_s_waitcnt(0x0F70 | (5 * PER)); break;
+  }
+}
+
 // Workgroup barrier that keeps the compiler from moving memory accesses
 // across it but adds no wait for outstanding loads (a fenced barrier would
 // wait for every in-flight direct load, emptying the ring).
 __device__ inline void barrier_no_fence() { asm volatile("s_barrier" ::: "memory"); }
 
-// Writes the staged tile into an LDS stage as bf16; with `partial`, tokens
-// at or past nrem (tokens left in the chunk from this tile on) become zeros.
-template <bool FP8>
-__device__ inline void stage_store(uint8_t* stg, const Stage<FP8>& s, bool partial, int nrem) {
-  const int t = threadIdx.x;
-  if constexpr (!FP8) {
-    const int tok = k_phys(t & 15), d = t >> 1, half = t & 1;
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      uint4 k = s.k[b], v = s.v[b];
-      if (partial) {
-        if (16 * b + tok >= nrem) k = make_uint4(0, 0, 0, 0);
-        v = keep_first(v, min(max(nrem - 16 * b - 8 * half, 0), 8));
-      }
-      *reinterpret_cast<uint4*>(stg + (b ? kLdsK1 : 0) + t * 16) = k;
-      *reinterpret_cast<uint4*>(stg + lds_v(b, d, half)) = v;
-    }
-  } else {
-    const int b = t >> 7, ci = t & 127, c16 = ci >> 4, phys = ci & 15;
-    uint4 k = s.k[0], v = s.v[0];
-    if (partial) {
-      if (16 * b + k_phys(phys) >= nrem) k = make_uint4(0, 0, 0, 0);
-      v = keep_first16(v, nrem - 16 * b);
-    }
-    uint8_t* kb = stg + (b ? kLdsK1 : 0);
-    *reinterpret_cast<uint4*>(kb + ((2 * c16) * 16 + phys) * 16) = fp8x8_to_bf16(k.x, k.y);
-    *reinterpret_cast<uint4*>(kb + ((2 * c16 + 1) * 16 + phys) * 16) = fp8x8_to_bf16(k.z, k.w);
-    *reinterpret_cast<uint4*>(stg + lds_v(b, ci, 0)) = fp8x8_to_bf16(v.x, v.y);
-    *reinterpret_cast<uint4*>(stg + lds_v(b, ci, 1)) = fp8x8_to_bf16(v.z, v.w);
-  }
-}
-
 // One workgroup, one chunk, up to 4 x RB row blocks: wave w owns row
 // blocks RB w .. RB w + RB - 1, so each K/V operand a wave reads from LDS
 // feeds RB row blocks (and RB independent chains of products overlap in
 // the wave).  Every wave takes part in every barrier.
+//
+// Tiles reach LDS by direct global-to-LDS loads in a ring of `ring` stages
+// with `ahead` tiles in flight.  bf16 stages hold the layout above; fp8
+// stages hold the raw tiles in the cache's layout, and every wave widens
+// the operands it reads (as the narrow path does from HBM), so an fp8 tile
+// moves half the bytes and the ring is deeper.
 template <bool FP8, int RB>
 __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int wave, int lane,
                           uint8_t* lds) {
+  constexpr int ring = FP8 ? kRing8 : kRing, ahead = FP8 ? kAhead8 : kAhead;
+  constexpr int stage = FP8 ? kStage8 : kStage;
   const int32_t* brow = P.table + (size_t)U.owner * P.max_blocks + U.jb0;
   // a cooperative item is a shared run: its end is in the plan
   const int ntok = U.nblk >= 0 ? U.nblk * kBlock : P.seq_len[U.owner] + A.len_bias - U.jb0 * kBlock;
@@ -780,144 +754,160 @@ __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit&
   RowState st[RB];
 #pragma unroll
   for (int r = 0; r < RB; ++r) {
-    load_q(P, A, U, row0 + 16 * r, R, false, g.q, g.lr, qf[r]);
+    load_q(P, A, U, row0 + 16 * r, R, FP8, g.q, g.lr, qf[r]);
     row_init(st[r]);
   }
   const float sl = A.scale_log2;
-  const int koff = (g.kb1 ? kLdsK1 : 0) + g.q * 256 + (lane & 7) * 16;
-  const int voff = lds_v(g.vb1 ? 1 : 0, g.lr, g.q & 1);
+  // lane's operand offsets in a stage
+  const int koff = FP8 ? (g.kb1 ? 2048 : 0) + g.q * 256 + (lane & 7) * 16
+                       : (g.kb1 ? kLdsK1 : 0) + g.q * 256 + (lane & 7) * 16;
+  const int voff = FP8 ? 2 * 2048 + (g.vb1 ? 2048 : 0) + g.lr * 16 + (g.q & 1) * 8 : lds_v(g.vb1 ? 1 : 0, g.lr, g.q & 1);
 
   // Scores of one tile for every row block (K from the stage holding it).
   auto qk = [&](const uint8_t* stg, f32x4 (&s0)[RB], f32x4 (&s1)[RB]) {
     bf16x8 kf[2][4];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < 2; ++h) {
+      if constexpr (!FP8) {
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) kf[h][kb] = *reinterpret_cast<const bf16x8*>(stg + koff + kb * 1024 + h * 128);
+        for (int kb = 0; kb < 4; ++kb)
+          kf[h][kb] = *reinterpret_cast<const bf16x8*>(stg + koff + kb * 1024 + h * 128);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const uint4 w = *reinterpret_cast<const uint4*>(stg + koff + j * 1024 + h * 128);
+          kf[h][2 * j] = __builtin_bit_cast(bf16x8, fp8x8_to_bf16(w.x, w.y));
+          kf[h][2 * j + 1] = __builtin_bit_cast(bf16x8, fp8x8_to_bf16(w.z, w.w));
+        }
+      }
+    }
 #pragma unroll
     for (int r = 0; r < RB; ++r) qk_mfma(kf, qf[r], s0[r], s1[r]);
   };
-  // Softmax and P.V of tile i from its scores.  mask_v: zero V of tokens
-  // past the end (the stage holds stale bits there).
-  auto pv = [&](const uint8_t* stg, int i, const TileMeta& m, bool mask_v, const f32x4 (&s0)[RB],
-                const f32x4 (&s1)[RB]) {
+  // Softmax and P.V of tile i from its scores.  V of tokens past the end is
+  // zeroed (a missing second block aliases the first; its P is zero, but
+  // the bits need not be finite).
+  auto pv = [&](const uint8_t* stg, int i, const f32x4 (&s0)[RB], const f32x4 (&s1)[RB]) {
     const int t0 = 32 * i;
     const bool partial = t0 + 32 > ntok;
     const int nv = min(max(ntok - t0 - 8 * g.q, 0), 8);
-    uint4 vr[8];
-#pragma unroll
-    for (int r = 0; r < 8; ++r) vr[r] = *reinterpret_cast<const uint4*>(stg + voff + r * 256);
+    TileMeta m{0, 0, 1.f, 1.f, 1.f, 1.f};
+    bf16x8 vf[8];
+    if constexpr (FP8) {
+      const float4 sc = *reinterpret_cast<const float4*>(stg + kMeta8);  // K0, V0, K1, V1
+      m = TileMeta{0, 0, sc.x, sc.z, sc.y, sc.w};
+    }
     float c, vsc;
     lane_scales(g, m, sl, c, vsc);
     bf16x8 ph[RB], pl[RB];
 #pragma unroll
     for (int r = 0; r < RB; ++r) softmax_p<FP8>(s0[r], s1[r], partial, nv, c, vsc, st[r], ph[r], pl[r]);
-    if (mask_v && partial) {
+    if constexpr (!FP8) {
+      uint4 vr[8];
 #pragma unroll
-      for (int r = 0; r < 8; ++r) vr[r] = keep_first(vr[r], nv);
+      for (int r = 0; r < 8; ++r) vr[r] = *reinterpret_cast<const uint4*>(stg + voff + r * 256);
+      if (partial) {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) vr[r] = keep_first(vr[r], nv);
+      }
+#pragma unroll
+      for (int r = 0; r < 8; ++r) vf[r] = __builtin_bit_cast(bf16x8, vr[r]);
+    } else {
+      uint2 vr[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) vr[r] = *reinterpret_cast<const uint2*>(stg + voff + r * 256);
+      if (partial) {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) vr[r] = make_uint2(keep_bytes(vr[r].x, nv), keep_bytes(vr[r].y, nv - 4));
+      }
+#pragma unroll
+      for (int r = 0; r < 8; ++r) vf[r] = __builtin_bit_cast(bf16x8, fp8x8_to_bf16(vr[r].x, vr[r].y));
     }
-    bf16x8 vf[8];
-#pragma unroll
-    for (int r = 0; r < 8; ++r) vf[r] = __builtin_bit_cast(bf16x8, vr[r]);
 #pragma unroll
     for (int r = 0; r < RB; ++r) pv_mfma(vf, ph[r], pl[r], st[r]);
   };
-  auto compute = [&](const uint8_t* stg, int i, const TileMeta& m, bool mask_v) {
-    f32x4 s0[RB], s1[RB];
-    qk(stg, s0, s1);
-    pv(stg, i, m, mask_v, s0, s1);
-  };
 
-  if constexpr (!FP8) {
-    // Lane t of wave w loads a 16-byte chunk of each 4 KB region of a tile
-    // into LDS slot t: K chunk t, and the V^T chunk (d = t % 128, token half
-    // t / 128) that the LDS layout puts in slot t.
-    const int t = threadIdx.x;
-    const int kofs = t * 16;
-    const int vofs = (t & 127) * 32 + 16 * (t >> 7);
-    const int wb = wave * 1024;
-    // Block ids live in LDS, two windows of 64: wave 0 loads window w + 1
-    // when the tiles it issues enter window w.  Its completion is covered
-    // by the per-tile waits (it retires before the tile loads issued after
-    // it), and the tiles of window w - 1, whose slot it reuses, were issued
-    // before the barrier.
-    int32_t* idw = reinterpret_cast<int32_t*>(lds + kRing * kStage);
-    auto fetch_ids = [&](int w) {
-      if (wave == 0) dma4(brow + min(64 * w + lane, nblk - 1), idw + 64 * (w & 1));
-    };
-    auto issue = [&](int i) {
-      const int j0 = 2 * i;
-      if ((j0 & 63) == 0 && j0 > 0) fetch_ids((j0 >> 6) + 1);
-      const int2 pr = *reinterpret_cast<const int2*>(idw + 64 * ((j0 >> 6) & 1) + (j0 & 63));
-      int b0 = __builtin_amdgcn_readfirstlane(pr.x);
-      int b1 = j0 + 1 < nblk ? __builtin_amdgcn_readfirstlane(pr.y) : b0;
-      if ((unsigned)b0 >= (unsigned)P.num_blocks || (unsigned)b1 >= (unsigned)P.num_blocks) {
-        if (t == 0) atomicOr(P.err, kErrBadBlock);
-        b0 = (unsigned)b0 < (unsigned)P.num_blocks ? b0 : 0;
-        b1 = (unsigned)b1 < (unsigned)P.num_blocks ? b1 : 0;
-      }
-      uint8_t* stg = lds + (i % kRing) * kStage + wb;
-      const size_t o0 = head_off<false>(b0, P.Hkv, U.kvh), o1 = head_off<false>(b1, P.Hkv, U.kvh);
-      dma16(P.k_cache + o0 + kofs, stg);
-      dma16(P.k_cache + o1 + kofs, stg + kLdsK1);
-      dma16(P.v_cache + o0 + vofs, stg + kLdsV);
-      dma16(P.v_cache + o1 + vofs, stg + kLdsV + kTileBytes);
-    };
-    const TileMeta unit{0, 0, 1.f, 1.f, 1.f, 1.f};  // bf16: no block scales
-    fetch_ids(0);
-    if (nblk > 64) fetch_ids(1);
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // Q operands and the first id windows are in
-    barrier_no_fence();
-    for (int i = 0; i < kAhead && i < ntile; ++i) issue(i);
-    wait_tiles(min(kAhead - 1, ntile - 1));  // tile 0 is in LDS
-    barrier_no_fence();
-    f32x4 s0[RB], s1[RB];
-    if (active) qk(lds, s0, s1);
-    // Iteration i issues the scores of tile i + 1 before the softmax and
-    // P.V of tile i, so the matrix cores work while the vector ALUs do the
-    // softmax.  Tile i + 1 must be in LDS first; stage (i - 1) % kRing, read
-    // for the last time in iteration i - 1, takes tile i + kAhead.
-    for (int i = 0; i < ntile; ++i) {
-      const bool more = i + 1 < ntile;
-      wait_tiles(i + 2 < ntile ? 1 : 0);  // this wave's loads of tile i + 1 are in LDS
-      barrier_no_fence();                  // ... and every wave's
-      if (i + kAhead < ntile) issue(i + kAhead);
-      if (active) {
-        f32x4 n0[RB], n1[RB];
-        if (more) qk(lds + ((i + 1) % kRing) * kStage, n0, n1);
-        pv(lds + (i % kRing) * kStage, i, unit, true, s0, s1);
-#pragma unroll
-        for (int r = 0; r < RB; ++r) {
-          s0[r] = n0[r];
-          s1[r] = n1[r];
-        }
-      }
+  const int t = threadIdx.x;
+  // Block ids live in LDS, two windows of 64: wave 0 loads window w + 1
+  // when the tiles it issues enter window w.  Its completion is covered by
+  // the per-tile waits (it retires before the tile loads issued after it),
+  // and the tiles of window w - 1, whose slot it reuses, were issued before
+  // the barrier.
+  int32_t* idw = reinterpret_cast<int32_t*>(lds + ring * stage);
+  auto fetch_ids = [&](int w) {
+    if (wave == 0) dma4(brow + min(64 * w + lane, nblk - 1), idw + 64 * (w & 1));
+  };
+  auto issue = [&](int i) {
+    const int j0 = 2 * i;
+    if ((j0 & 63) == 0 && j0 > 0) fetch_ids((j0 >> 6) + 1);
+    const int2 pr = *reinterpret_cast<const int2*>(idw + 64 * ((j0 >> 6) & 1) + (j0 & 63));
+    int b0 = __builtin_amdgcn_readfirstlane(pr.x);
+    int b1 = j0 + 1 < nblk ? __builtin_amdgcn_readfirstlane(pr.y) : b0;
+    if ((unsigned)b0 >= (unsigned)P.num_blocks || (unsigned)b1 >= (unsigned)P.num_blocks) {
+      if (t == 0) atomicOr(P.err, kErrBadBlock);
+      b0 = (unsigned)b0 < (unsigned)P.num_blocks ? b0 : 0;
+      b1 = (unsigned)b1 < (unsigned)P.num_blocks ? b1 : 0;
     }
-  } else {
-    BlockIds<FP8> ids(P, brow, nblk, lane);
-    TileMeta m{}, mn{};
-    ids.tile(0, m.b0, m.b1, m.ks0, m.ks1, m.vs0, m.vs1);
-    Stage<FP8> sg;
-    stage_load<FP8>(P, U.kvh, m, sg);
-    stage_store<FP8>(lds, sg, 32 > ntok, ntok);
-    __syncthreads();
-    auto step = [&](int i, const uint8_t* cur, uint8_t* nxt) {
-      const bool more = i + 1 < ntile;
-      if (more) {
-        ids.tile(i + 1, mn.b0, mn.b1, mn.ks0, mn.ks1, mn.vs0, mn.vs1);
-        stage_load<FP8>(P, U.kvh, mn, sg);
+    uint8_t* stg = lds + (i % ring) * stage;
+    if constexpr (!FP8) {
+      // Lane t of wave w loads a 16-byte chunk of each 4 KB region of a
+      // tile into LDS slot t: K chunk t, and the V^T chunk (d = t % 128,
+      // token half t / 128) that the LDS layout puts in slot t.
+      const int kofs = t * 16;
+      const int vofs = (t & 127) * 32 + 16 * (t >> 7);
+      uint8_t* dst = stg + wave * 1024;
+      const size_t o0 = head_off<false>(b0, P.Hkv, U.kvh), o1 = head_off<false>(b1, P.Hkv, U.kvh);
+      dma16(P.k_cache + o0 + kofs, dst);
+      dma16(P.k_cache + o1 + kofs, dst + kLdsK1);
+      dma16(P.v_cache + o0 + vofs, dst + kLdsV);
+      dma16(P.v_cache + o1 + vofs, dst + kLdsV + kTileBytes);
+    } else {
+      // Waves 0-1 move block b0's K and V^T tiles, waves 2-3 block b1's
+      // (lane t to byte 16 t of each 4 KB half); wave 0 also moves the
+      // scales, lane l the l % 4-th of (K0, V0, K1, V1).
+      if (wave == 0) dma4(P.kv_scale + 2 * ((lane & 2) ? b1 : b0) + (lane & 1), stg + kMeta8);
+      const size_t o = head_off<true>(wave < 2 ? b0 : b1, P.Hkv, U.kvh) + (t & 127) * 16;
+      dma16(P.k_cache + o, stg + wave * 1024);
+      dma16(P.v_cache + o, stg + 2 * 2048 + wave * 1024);
+    }
+  };
+  // Waits until this wave's loads of the tiles before the `later` last
+  // issued ones are in LDS (wave 0 issues one more load per fp8 tile).
+  auto wait = [&](int later) {
+    if constexpr (!FP8)
+      wait_tiles(later);
+    else if (wave == 0)
+      wait_tiles_per<3>(later);
+    else
+      wait_tiles_per<2>(later);
+  };
+  fetch_ids(0);
+  if (nblk > 64) fetch_ids(1);
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // Q operands and the first id windows are in
+  barrier_no_fence();
+  for (int i = 0; i < ahead && i < ntile; ++i) issue(i);
+  wait(min(ahead, ntile) - 1);  // tile 0 is in LDS
+  barrier_no_fence();
+  f32x4 s0[RB], s1[RB];
+  if (active) qk(lds, s0, s1);
+  // Iteration i issues the scores of tile i + 1 before the softmax and P.V
+  // of tile i, so the matrix cores work while the vector ALUs do the
+  // softmax.  Tile i + 1 must be in LDS first; stage (i - 1) % ring, read
+  // for the last time in iteration i - 1, takes tile i + ahead.
+  for (int i = 0; i < ntile; ++i) {
+    const bool more = i + 1 < ntile;
+    wait(max(min(ahead - 2, ntile - 2 - i), 0));  // this wave's loads of tile i + 1 are in LDS
+    barrier_no_fence();                            // ... and every wave's
+    if (i + ahead < ntile) issue(i + ahead);
+    if (active) {
+      f32x4 n0[RB], n1[RB];
+      if (more) qk(lds + ((i + 1) % ring) * stage, n0, n1);
+      pv(lds + (i % ring) * stage, i, s0, s1);
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        s0[r] = n0[r];
+        s1[r] = n1[r];
       }
-      if (active) compute(cur, i, m, false);
-      if (more) {
-        const int t1 = 32 * (i + 1);
-        stage_store<FP8>(nxt, sg, t1 + 32 > ntok, ntok - t1);
-        m = mn;
-      }
-      __syncthreads();
-    };
-    for (int i = 0; i < ntile; i += 2) {
-      step(i, lds, lds + kStage);
-      if (i + 1 < ntile) step(i + 1, lds + kStage, lds);
     }
   }
   if (active) {
@@ -945,7 +935,7 @@ __device__ inline int tail_start(const AttnLaunch& A, int x) {
 
 template <bool FP8>
 __global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(DevPool P, AttnLaunch A) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[FP8 ? 2 * kStage : kRing * kStage + kIdsBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[(FP8 ? kRing8 * kStage8 : kRing * kStage) + kIdsBytes];
   __shared__ int claimed;
   if (threadIdx.x == 0) {
     const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
