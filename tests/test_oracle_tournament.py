@@ -161,12 +161,6 @@ def test_eviction_takes_the_lowest_score_higher_id_on_ties():
     assert m.evict([0, 1, 2, 4]) == 1
 
 
-def test_runtime_example_count_identity():
-    roots, branches, pruned, completed, C = 256, 1339, 1083, 256, 256
-    assert roots + branches - pruned - completed == C
-    assert branches == pruned + completed
-
-
 def test_random_run_conserves_counts():
     rnd = random.Random(7)
     T, C, K = 24, 16, 4
