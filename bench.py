@@ -93,6 +93,35 @@ def cpu_baseline(wl, budget_s: float):
                        f"{spent:.1f} s; {len(os.sched_getaffinity(0))} host cores visible")}
 
 
+def read_ceiling(gib: int = 16, grid: int = 4096, reps: int = 5):
+    """The device's streaming-read rate over a gib-GiB buffer (plain loads and
+    loads with the non-temporal hint; best of reps), measured in this process
+    by the library's stream-read kernel: the practical ceiling beside the
+    published HBM peak."""
+    import torch
+
+    from paper_2608_08020_amd.gambit import stream_read
+
+    buf = torch.empty(gib << 30, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(grid, dtype=torch.int32, device="cuda")
+    out = {"buffer_GiB": gib, "grid": grid, "kernel": "stream_read_kernel (16-byte loads, 64 KiB in flight "
+                                                      "per workgroup, contiguous run per workgroup)"}
+    for nt in (False, True):
+        stream_read(buf, nt, grid, sink)  # warm
+        best = float("inf")
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            stream_read(buf, nt, grid, sink)
+            b.record()
+            b.synchronize()
+            best = min(best, a.elapsed_time(b) / 1e3)
+        out["nontemporal_GBps" if nt else "plain_GBps"] = round(buf.numel() / best / 1e9, 1)
+    del buf
+    torch.cuda.empty_cache()
+    return out
+
+
 def tournament_rounds(rounds: int = 24):
     """The full tournament of Alg. 1 at C = 256, K = 16 (Sec. 5.1), Qwen3-8B
     layer shape: per round every running trace is scored (running means), the
@@ -457,6 +486,10 @@ def main():
         "round_us": [round(a.elapsed_time(b) * 1e3, 1) for a, b in round_ev],
         "event_ms_per_step": round(ev_ms / K, 4),
     }
+    log("measuring the read ceiling")
+    ceil = read_ceiling()
+    ceil["attn_frac_of_nontemporal"] = round(achieved / ceil["nontemporal_GBps"], 4)
+    res["read_ceiling"] = ceil
     if not args.no_tournament:
         log("timing tournament rounds")
         res["tournament"] = tournament_rounds()

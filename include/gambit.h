@@ -419,6 +419,19 @@ int32_t gambit_scorer_steps(const gambit_scorer* scorer, int32_t trace_id);
 gambit_status gambit_scorer_check(gambit_scorer* scorer, void* stream);
 const char* gambit_scorer_last_error(const gambit_scorer* scorer);
 
+/* Measurement, not a step of the method: the device's streaming-read rate,
+ * the practical ceiling beside the published HBM peak for the attention
+ * kernel's achieved bandwidth.  Reads `bytes` of device memory at `buf`
+ * once (workgroup w a contiguous run of 64 KiB chunks; 16-byte loads, with
+ * the non-temporal hint when nontemporal = 1) on `stream`; does not block.
+ * sink: device [grid] uint32, caller-zeroed; each workgroup XORs the dwords
+ * it read into sink[w], so the XOR of sink equals the XOR of the buffer's
+ * dwords.  GAMBIT_ERR_INVALID unless buf is 16-byte aligned, bytes is a
+ * positive multiple of 65536 and 1 <= grid <= min(65535, bytes / 65536);
+ * GAMBIT_ERR_DEVICE if the launch fails. */
+gambit_status gambit_stream_read(const void* buf, size_t bytes, int32_t nontemporal, int32_t grid,
+                                 uint32_t* sink, void* stream);
+
 /* Host mirror queries (no sync): length of a trace; free block count. */
 int32_t gambit_seq_len(const gambit_pool* pool, int32_t trace_id);
 int32_t gambit_free_blocks(const gambit_pool* pool);

@@ -87,7 +87,7 @@ EXPORTS = ["gambit_workspace_size", "gambit_pool_create", "gambit_pool_destroy",
            "gambit_evict", "gambit_tournament", "gambit_trace_state", "gambit_record_scores",
            "gambit_mlp_workspace_size", "gambit_mlp_score", "gambit_scorer_workspace_size", "gambit_scorer_create",
            "gambit_scorer_destroy", "gambit_scorer_step", "gambit_scorer_fork", "gambit_scorer_free",
-           "gambit_scorer_steps", "gambit_scorer_check", "gambit_scorer_last_error"]
+           "gambit_scorer_steps", "gambit_scorer_check", "gambit_scorer_last_error", "gambit_stream_read"]
 
 
 def lib() -> ctypes.CDLL:
@@ -134,6 +134,7 @@ def lib() -> ctypes.CDLL:
         "gambit_scorer_steps": (i32, [vp, i32]),
         "gambit_scorer_check": (i32, [vp, vp]),
         "gambit_scorer_last_error": (ctypes.c_char_p, [vp]),
+        "gambit_stream_read": (i32, [vp, ctypes.c_size_t, i32, i32, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -197,6 +198,18 @@ def mlp_score(h: torch.Tensor, w1: torch.Tensor, b1: torch.Tensor, w2: torch.Ten
     if st != OK:
         raise GambitError(st, "mlp_score")
     return scores, (keep_out[:keep] if keep > 0 else None)
+
+
+def stream_read(buf: torch.Tensor, nontemporal: bool, grid: int, sink: torch.Tensor, stream=None) -> None:
+    """gambit_stream_read: read every byte of buf once (timing of the memory
+    system's read rate); sink (int32, zeroed, >= grid entries) receives each
+    workgroup's XOR of the dwords it read."""
+    if not buf.is_contiguous() or sink.dtype != torch.int32 or sink.numel() < grid:
+        raise ValueError("buf must be contiguous; sink int32 with >= grid entries")
+    st = lib().gambit_stream_read(buf.data_ptr(), buf.numel() * buf.element_size(), int(bool(nontemporal)),
+                                  int(grid), sink.data_ptr(), _stream(stream))
+    if st != OK:
+        raise GambitError(st, "stream_read")
 
 
 class Pool:

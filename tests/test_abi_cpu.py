@@ -74,3 +74,17 @@ def test_scorer_workspace_size_validates_descriptions():
     d3 = gambit.ScorerDesc.from_buffer_copy(d)
     d3.n_layers = 0
     assert 0 < int(L.gambit_scorer_workspace_size(ctypes.byref(d3))) < ok
+
+
+def test_stream_read_rejects_bad_arguments_without_a_device():
+    from paper_2608_08020_amd import gambit
+    if not os.path.exists(gambit.LIB_PATH):
+        pytest.skip("libgambit.so not built")
+    L = gambit.lib()
+    fake = ctypes.c_void_p(1 << 20)  # never dereferenced: every call below fails validation
+    sink = ctypes.c_void_p(1 << 21)
+    bad = [(None, 65536, 0, 1, sink), (fake, 0, 0, 1, sink), (fake, 65536 + 16, 0, 1, sink),
+           (fake, 65536, 0, 0, sink), (fake, 65536, 0, 2, sink), (fake, 65536 * 70000, 0, 65536, sink),
+           (fake, 65536, 2, 1, sink), (fake, 65536, 0, 1, None), (ctypes.c_void_p((1 << 20) + 4), 65536, 0, 1, sink)]
+    for buf, nbytes, nt, grid, snk in bad:
+        assert L.gambit_stream_read(buf, nbytes, nt, grid, snk, None) == gambit.ERR_INVALID
