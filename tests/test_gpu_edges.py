@@ -101,7 +101,10 @@ def test_errors_leave_pool_unchanged():
 
 def test_rank_topk_ties_bit_exact():
     rng = np.random.default_rng(1)
-    for n, keep in [(7, 3), (512, 128), (1000, 999), (4096, 17), (33, 33)]:
+    # sizes on both sides of the run-merge sort's limits (runs of 128, at most
+    # 1024 keys; the bitonic network beyond), crafted ties
+    for n, keep in [(7, 3), (512, 128), (1000, 999), (4096, 17), (33, 33), (1, 1), (64, 10), (128, 64),
+                    (129, 1), (256, 256), (1024, 1024), (1025, 500), (2048, 2000)]:
         ids = rng.permutation(n * 3)[:n].astype(np.int32)
         scores = rng.choice(np.array([0.1, 0.5, 0.5000001, 0.9, -2.0], np.float32), size=n)
         got = gambit.rank_topk(torch.from_numpy(ids).to(DEV), torch.from_numpy(scores).to(DEV), keep)
