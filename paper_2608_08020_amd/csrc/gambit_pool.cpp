@@ -101,6 +101,7 @@ struct gambit_pool {
   gambit::DevPool dev{};
   uint8_t* ws = nullptr;
   int g = 1;
+  int n_cu = 256;  // compute units of the pool's device (two attention workgroups each)
   float append_scale = 1.f / 64.f;
 
   // host mirror
@@ -414,6 +415,36 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
   for (int b : starts) p->first[b] = -1;
   for (int b : touched) p->cnt[b] = 0;
 
+  // Chunk caps from the launch's own length.  A chunk is one unit's work, and
+  // a unit that runs longer than the launch would take with its work spread
+  // evenly sets the launch's length.  The estimate uses per-token times
+  // measured on MI355X with bf16 pools (fp8 tiles move half the bytes): a
+  // narrow unit streams ~0.16 us per token on one wave, four units to a
+  // workgroup slot; a cooperative item ~0.042 us per token on a whole slot;
+  // two slots per compute unit.  Narrow chunks are capped at the estimated
+  // launch length, cooperative ones (which start early) at half of it; on the
+  // 512-trace workload (~0.85 ms launches) neither cap binds.
+  double cap_n = 1e9, cap_c = 1e9;  // blocks
+  {
+    const double e = p->d.kv_dtype == GAMBIT_KV_FP8_E4M3 ? 0.5 : 1.0;
+    const double a_n = 0.16 * e, a_c = 0.042 * e;
+    double slot_us = 0.0;
+    for (int pos = 0; pos < n; ++pos)
+      for (int r = run_off[pos]; r < run_off[pos + 1]; ++r) {
+        const Run& R = runs[r];
+        const double tok = 16.0 * (R.j1 - R.j0);
+        if (R.c == 1) {
+          slot_us += tok * a_n / 4;
+        } else if (mem[R.rid][0] == pos) {
+          const int rows = R.c * p->g;
+          slot_us += rows <= gambit::kRowsPerUnit ? tok * a_n / 4 : tok * a_c * cdiv(rows, gambit::kRowsPerCoop);
+        }
+      }
+    const double launch_us = slot_us * Hkv / (2.0 * p->n_cu);
+    cap_n = std::max(16.0, launch_us / a_n / 16.0);
+    cap_c = std::max(16.0, 0.5 * launch_us / a_c / 16.0);
+  }
+
   std::vector<Group> groups;
   std::vector<AttnUnit> gunits;  // the groups' units, contiguous per group
   std::vector<int32_t> members;
@@ -455,8 +486,12 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
       for (int r = run_off[pos]; r < run_off[pos + 1]; ++r) {
         const Run& R = runs[r];
         const int len = R.j1 - R.j0;
+        // the caps apply to the first pass only: when the partial limit needs
+        // longer chunks, the chunk lengths no longer depend on them
+        const double grow = chunk_blocks == kDefaultChunkBlocks ? 1.0 : 1e9;
         if (R.c == 1) {  // private run: through the trace's last block, chunks of 4 chunk_blocks
-          const int nch = std::max(1, cdiv(len, 4 * chunk_blocks));
+          const int clen = (int)std::max(1.0, std::min(4.0 * chunk_blocks, cap_n * grow));
+          const int nch = std::max(1, cdiv(len, clen));
           for (int k = 0, jb = R.j0; k < nch; ++k) {
             const int sz = len / nch + (k < len % nch ? 1 : 0);
             const bool last = k == nch - 1;
@@ -472,7 +507,9 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
         // Measured on the 512-trace workload; shorter chunks lose more to
         // per-unit start-up and merging than they gain at the launch's tail.
         const int nrb = cdiv(R.c * p->g, gambit::kRowsPerUnit);
-        const int nch = cdiv(len, chunk_blocks * (nrb == 1 ? 4 : std::min(nrb, 8)));
+        const int clen = (int)std::max(1.0, std::min((double)chunk_blocks * (nrb == 1 ? 4 : std::min(nrb, 8)),
+                                                     (nrb == 1 ? cap_n : cap_c) * grow));
+        const int nch = cdiv(len, clen);
         const auto& ml = mem[R.rid];
         for (int k = 0, jb = R.j0; k < nch; ++k) {
           const int sz = len / nch + (k < len % nch ? 1 : 0);
@@ -677,6 +714,12 @@ gambit_status gambit_pool_create(const gambit_pool_desc* desc, void* stream, gam
   if (e == hipSuccess) e = hipEventCreateWithFlags(&p->stage_ev, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&p->plan_ev, hipEventDisableTiming);
 
+  if (e == hipSuccess) {
+    int dev = 0, ncu = 0;
+    e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess && ncu > 0) p->n_cu = ncu;
+  }
   if (e == hipSuccess) e = hipEventRecord(p->stage_ev, S(stream));
   if (e == hipSuccess) e = hipEventRecord(p->plan_ev, S(stream));
   if (e == hipSuccess) e = hipMemsetAsync(p->ws + L.ticket, 0, 64, S(stream));
