@@ -735,10 +735,13 @@ __device__ inline void barrier_no_fence() { asm volatile("s_barrier" ::: "memory
 // stages hold the raw tiles in the cache's layout, and every wave widens
 // the operands it reads (as the narrow path does from HBM), so an fp8 tile
 // moves half the bytes and the ring is deeper.
-template <bool FP8, int RB>
+template <bool FP8, int RB, bool PAIR = false>
 __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int wave, int lane,
                           uint8_t* lds) {
-  constexpr int ring = FP8 ? kRing8 : kRing, ahead = FP8 ? kAhead8 : kAhead;
+  static_assert(!PAIR || (FP8 && RB == 1), "tile pairs: fp8 items of at most two row blocks");
+  // Tile pairs keep four tiles in use (two being applied, two being scored),
+  // so they run two fewer tiles ahead.
+  constexpr int ring = FP8 ? kRing8 : kRing, ahead = FP8 ? (PAIR ? kRing8 - 2 : kAhead8) : kAhead;
   constexpr int stage = FP8 ? kStage8 : kStage;
   const int32_t* brow = P.table + (size_t)U.owner * P.max_blocks + U.jb0;
   // a cooperative item is a shared run: its end is in the plan
@@ -748,7 +751,10 @@ __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit&
   const LaneGeom g = lane_geom(lane);
   const int nblk = (ntok + kBlock - 1) / kBlock;
   const int ntile = (ntok + 31) / 32;
-  const int row0 = 16 * RB * wave;
+  // tile pairs: waves w and w + 2 share row block w & 1 and take the even
+  // and the odd tiles
+  const int row0 = PAIR ? 16 * (wave & 1) : 16 * RB * wave;
+  const int par = PAIR ? wave >> 1 : 0;
   const bool active = row0 < R;
   bf16x8 qf[RB][4];
   RowState st[RB];
@@ -886,6 +892,65 @@ __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit&
   __builtin_amdgcn_s_waitcnt(0x0F70);  // Q operands and the first id windows are in
   barrier_no_fence();
   for (int i = 0; i < ahead && i < ntile; ++i) issue(i);
+  if constexpr (PAIR) {
+    // Step k applies tiles 2k (waves 0-1) and 2k + 1 (waves 2-3) and scores
+    // each wave's next tile (2k + 2 or 2k + 3); tiles up to 2k + ahead + 1
+    // are then issued, into the stages of tiles 2k - 2 and 2k - 1, which
+    // every wave finished with in step k - 1.  Every wave takes part in
+    // every barrier, whatever its tiles.
+    wait(max(min(ahead, ntile) - 2, 0));  // tiles 0 and 1 are in LDS
+    barrier_no_fence();
+    f32x4 s0[1], s1[1];
+    if (active && par < ntile) qk(lds + par * stage, s0, s1);
+    for (int k = 0; 2 * k < ntile; ++k) {
+      const int i = 2 * k + par;
+      // tiles up to 2k + 3 in LDS: of the tiles issued so far, the ones past it may still be in flight
+      wait(max(min(ahead + 2 * k, ntile) - 1 - min(2 * k + 3, ntile - 1), 0));
+      barrier_no_fence();
+      if (2 * k + ahead < ntile) issue(2 * k + ahead);
+      if (2 * k + ahead + 1 < ntile) issue(2 * k + ahead + 1);
+      if (active && i < ntile) {
+        f32x4 n0[1], n1[1];
+        if (i + 2 < ntile) qk(lds + ((i + 2) % ring) * stage, n0, n1);
+        pv(lds + (i % ring) * stage, i, s0, s1);
+        s0[0] = n0[0];
+        s1[0] = n1[0];
+      }
+    }
+    // Waves 2-3 hand their running state to waves 0-1 through LDS (the ring
+    // is idle: every issued tile was waited for), which combine and write.
+    float* xch = reinterpret_cast<float*>(lds) + (wave & 1) * 34 * 64;
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    barrier_no_fence();
+    if (par == 1) {
+      xch[lane] = st[0].m;
+      xch[64 + lane] = st[0].l;
+#pragma unroll
+      for (int r = 0; r < 8; ++r)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) xch[128 + (4 * r + e) * 64 + lane] = st[0].acc[r][e];
+    }
+    __syncthreads();
+    if (par == 0 && active) {
+      const float mb = xch[lane], lb = xch[64 + lane];
+      RowState& a = st[0];
+      if (mb > a.m) {  // the other half moved further; also when this half saw no tile (m = -inf)
+        const float alpha = a.m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(a.m - mb);
+        a.l *= alpha;
+#pragma unroll
+        for (int r = 0; r < 8; ++r) a.acc[r] *= alpha;
+        a.m = mb;
+      }
+      const float beta = mb == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mb - a.m);
+      a.l += beta * lb;
+#pragma unroll
+      for (int r = 0; r < 8; ++r)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) a.acc[r][e] += beta * xch[128 + (4 * r + e) * 64 + lane];
+      write_partial(P, A, U, row0, R, g.q, g.lr, a);
+    }
+    return;
+  }
   wait(min(ahead, ntile) - 1);  // tile 0 is in LDS
   barrier_no_fence();
   f32x4 s0[RB], s1[RB];
@@ -964,6 +1029,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(DevPool P, Attn
     // up to 64 rows: one row block per wave; more: two
     if (U0.mem_cnt * P.g > 4 * kRowsPerUnit)
       coop_unit<FP8, 2>(P, A, U0, wave, lane, lds);
+    else if (FP8 && U0.mem_cnt * P.g <= 2 * kRowsPerUnit && U0.mem_cnt > 0)
+      coop_unit<FP8, 1, FP8>(P, A, U0, wave, lane, lds);  // fp8, at most 32 rows: tile pairs
     else if (U0.mem_cnt > 0)
       coop_unit<FP8, 1>(P, A, U0, wave, lane, lds);
     return;
