@@ -20,7 +20,10 @@
 //    workgroup streams 32-token tiles into a 4-stage LDS ring by direct
 //    global-to-LDS loads, three tiles ahead, and each wave applies a tile to
 //    its one or two row blocks, so a chunk is read once per up to eight row
-//    blocks instead of once per row block.
+//    blocks instead of once per row block.  fp8 items of at most two row
+//    blocks run in tile pairs: waves w and w + 2 take the even and the odd
+//    tiles of row block w & 1, and their running states are combined at the
+//    end, so no wave idles.
 //
 // The launch also performs the decode step's append: the unit that covers
 // a trace's last block writes the new token's K and V there (quantising
