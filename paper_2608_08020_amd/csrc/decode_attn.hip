@@ -122,13 +122,9 @@ __device__ inline uint4 keep_first(uint4 x, int nv) {
   return x;
 }
 
-// Keep the first nv of 16 fp8 codes (four per dword).
+// Keep the first n of the four fp8 codes of a dword.
 __device__ inline uint32_t keep_bytes(uint32_t w, int n) {
   return n >= 4 ? w : (n <= 0 ? 0u : w & ((1u << (8 * n)) - 1u));
-}
-
-__device__ inline uint4 keep_first16(uint4 x, int nv) {
-  return make_uint4(keep_bytes(x.x, nv), keep_bytes(x.y, nv - 4), keep_bytes(x.z, nv - 8), keep_bytes(x.w, nv - 12));
 }
 
 // The narrow path's KV reads are streaming: each byte is read once per
