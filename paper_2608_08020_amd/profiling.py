@@ -85,7 +85,7 @@ def main():
         json.dump(rec, f, indent=1)
     cmds = open(a.cmds).read().strip()
     lines = [f"# {KERNEL} - {a.workload}", "",
-             "Commands (run from the repository root on the GPU box):", "", "```", cmds, "```", "",
+             "Commands (run from the repository root on an MI355X):", "", "```", cmds, "```", "",
              f"## Kernel time (rocprofv3 --kernel-trace --stats)", "",
              "| kernel | calls | avg us | total % |", "|---|---|---|---|"]
     for r in stats[:10]:
