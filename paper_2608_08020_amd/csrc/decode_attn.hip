@@ -1067,21 +1067,24 @@ __global__ __launch_bounds__(256) void merge_kernel(DevPool P, AttnLaunch A) {
   float L = w * mine.y;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) L += __shfl_xor(L, off);
+  // Partials are read once: eight loads in flight, streaming; added in
+  // partial order.
   float o0 = 0.f, o1 = 0.f;
   int k = 0;
-  for (; k + 4 <= nk; k += 4) {
-    float2 a[4];
+  for (; k + 8 <= nk; k += 8) {
+    f32x2 a[8];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) a[j] = *reinterpret_cast<const float2*>(pa + (size_t)(k + j) * kHeadDim + 2 * lane);
+    for (int j = 0; j < 8; ++j)
+      a[j] = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(pa + (size_t)(k + j) * kHeadDim + 2 * lane));
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 8; ++j) {
       const float wk = __shfl(w, k + j);
       o0 += wk * a[j].x;
       o1 += wk * a[j].y;
     }
   }
   for (; k < nk; ++k) {
-    const float2 a = *reinterpret_cast<const float2*>(pa + (size_t)k * kHeadDim + 2 * lane);
+    const f32x2 a = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(pa + (size_t)k * kHeadDim + 2 * lane));
     const float wk = __shfl(w, k);
     o0 += wk * a.x;
     o1 += wk * a.y;
