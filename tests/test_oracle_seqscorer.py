@@ -11,6 +11,11 @@
   -> sigmoid by torch's functions; y_t does not depend on later steps; at one
   step the queries and keys do not matter (attention over one position
   returns its value); the history model's fork equals a copy.
+* The layer stacking (residuals, pre-norm order, attention before the
+  feed-forward, layers in order) against torch's nn.TransformerEncoderLayer
+  with norm_first=True: with zero queries over several steps (uniform causal
+  weights, so the rotary embedding plays no part) and with the full weights
+  at one step.
 """
 import math
 
@@ -132,3 +137,70 @@ def test_history_model_fork_is_a_copy():
     assert a == b
     m.free([1])
     assert m.step([1], H[:1])[0] == scorer_outputs(w, H[:1], 4)[0]
+
+
+def _torch_stack(w, H, n_heads, causal=True):
+    """The scorer's layers run by torch's own pre-norm encoder layers
+    (nn.TransformerEncoderLayer with norm_first=True: x + SA(LN1(x)), then
+    x + FF(LN2(x))).  The gated feed-forward is expressed in torch's
+    Linear -> activation -> Linear form: linear1 stacks W1 over W3, the
+    activation multiplies SiLU of the first half by the second half (padded
+    back with zeros) and linear2 is [W2 | 0]."""
+    t = lambda a: torch.from_numpy(np.asarray(a, np.float64))  # noqa: E731
+    d = w["W_in"].shape[0]
+    f = w["layers"][0]["W1"].shape[0] if w["layers"] else 1
+
+    def gated(z):
+        return torch.cat([F.silu(z[..., :f]) * z[..., f:], torch.zeros_like(z[..., f:])], dim=-1)
+
+    x = F.gelu(F.linear(F.layer_norm(t(H), (H.shape[1],), t(w["ln_in_g"]), t(w["ln_in_b"]), eps=LN_EPS),
+                        t(w["W_in"])))[None]
+    for L in w["layers"]:
+        lay = torch.nn.TransformerEncoderLayer(d, n_heads, dim_feedforward=2 * f, dropout=0.0, activation=gated,
+                                               layer_norm_eps=LN_EPS, batch_first=True, norm_first=True, dtype=torch.float64)
+        with torch.no_grad():
+            for b in (lay.self_attn.in_proj_bias, lay.self_attn.out_proj.bias, lay.linear1.bias, lay.linear2.bias):
+                b.zero_()  # the scorer's linear maps have no biases
+            lay.self_attn.in_proj_weight.copy_(t(np.concatenate([L["Wq"], L["Wk"], L["Wv"]])))
+            lay.self_attn.out_proj.weight.copy_(t(L["Wo"]))
+            lay.linear1.weight.copy_(t(np.concatenate([L["W1"], L["W3"]])))
+            lay.linear2.weight.copy_(t(np.concatenate([L["W2"], np.zeros_like(L["W2"])], axis=1)))
+            lay.norm1.weight.copy_(t(L["ln1_g"]))
+            lay.norm1.bias.copy_(t(L["ln1_b"]))
+            lay.norm2.weight.copy_(t(L["ln2_g"]))
+            lay.norm2.bias.copy_(t(L["ln2_b"]))
+        lay.train()  # the reference (non-fused) code path; dropout is 0
+        T = x.shape[1]
+        mask = torch.nn.Transformer.generate_square_subsequent_mask(T, dtype=torch.float64) if causal else None
+        with torch.no_grad():
+            x = lay(x, src_mask=mask, is_causal=causal)
+    y = torch.sigmoid(F.layer_norm(x[0], (d,), t(w["ln_out_g"]), t(w["ln_out_b"]), eps=LN_EPS) @ t(w["w_out"]))
+    return y.numpy()
+
+
+def test_layer_stacking_matches_torch_pre_norm_encoder():
+    """Residuals and the pre-norm order of each layer (App. A.1's Transformer
+    over the step sequence), pinned by torch's own encoder layer.  Queries are
+    zero, so every causal position averages the values of steps 0..t equally
+    and the rotary embedding (pinned separately) plays no part: what is left
+    is the layer structure - LN1 before attention, LN2 before the gated
+    feed-forward, both added back to the stream, attention before the
+    feed-forward, layers in order.  A dropped residual or a post-norm layer
+    (LN after the addition) fails it."""
+    for n_layers, T in [(1, 1), (1, 2), (2, 5), (3, 7)]:
+        w = _w(cfg_layers=n_layers)
+        for L in w["layers"]:
+            L["Wq"] = np.zeros_like(L["Wq"])
+        H = RNG.standard_normal((T, 24))
+        ref = _torch_stack(w, H, 4)
+        got = scorer_outputs(w, H, 4)
+        assert np.allclose(got, ref, rtol=0, atol=1e-13), (n_layers, T, got, ref)
+
+
+def test_layer_stacking_one_step_full_weights():
+    """At a single step attention returns the step's own value (any queries
+    and keys; the rotation at position 0 is the identity), so torch's
+    pre-norm encoder layer with the full weights gives the scorer's output."""
+    w = _w(cfg_layers=2)
+    H = RNG.standard_normal((1, 24))
+    assert np.allclose(scorer_outputs(w, H, 4), _torch_stack(w, H, 4, causal=False), rtol=0, atol=1e-13)
