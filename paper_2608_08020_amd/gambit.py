@@ -160,22 +160,37 @@ def _ptr(a: np.ndarray):
     return a.ctypes.data_as(ctypes.c_void_p)
 
 
-def _dev(t: torch.Tensor, dtype=None, shape=None):
-    if not t.is_cuda or not t.is_contiguous():
-        raise ValueError("expected a contiguous device tensor")
-    if dtype is not None and t.dtype != dtype:
-        raise ValueError(f"expected {dtype}, got {t.dtype}")
+def _spec(t: torch.Tensor, dtype=None, shape=None, what: str = "tensor"):
+    """Check a tensor argument's dtype(s), shape and contiguity.  The kernels
+    trust these sizes (the C ABI takes bare pointers), so every device
+    argument of an entry point is checked before the library sees any."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{what}: expected a tensor, got {type(t).__name__}")
+    if dtype is not None:
+        ok = t.dtype in dtype if isinstance(dtype, tuple) else t.dtype == dtype
+        if not ok:
+            raise ValueError(f"{what}: expected dtype {dtype}, got {t.dtype}")
     if shape is not None and tuple(t.shape) != tuple(shape):
-        raise ValueError(f"expected shape {tuple(shape)}, got {tuple(t.shape)}")
+        raise ValueError(f"{what}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what}: expected a contiguous tensor")
+
+
+def _dev(t: torch.Tensor, dtype=None, shape=None, what: str = "tensor"):
+    """Pointer of a contiguous device tensor (checked as by _spec)."""
+    _spec(t, dtype, shape, what)
+    if not t.is_cuda:
+        raise ValueError(f"{what}: expected a device tensor")
     return ctypes.c_void_p(t.data_ptr())
 
 
 def rank_topk(ids: torch.Tensor, scores: torch.Tensor, keep: int, stream=None) -> torch.Tensor:
     """gambit_rank_topk: ids of the top `keep` by (score desc, id asc), on the device."""
     n = ids.numel()
+    _spec(ids, torch.int32, (n,), "ids")
+    _spec(scores, torch.float32, (n,), "scores")
     out = torch.empty(keep, dtype=torch.int32, device=ids.device)
-    st = lib().gambit_rank_topk(n, _dev(ids, torch.int32), _dev(scores, torch.float32), keep,
-                                _dev(out), _stream(stream))
+    st = lib().gambit_rank_topk(n, _dev(ids), _dev(scores), keep, _dev(out), _stream(stream))
     if st != OK:
         raise GambitError(st, "rank_topk")
     return out
@@ -184,10 +199,22 @@ def rank_topk(ids: torch.Tensor, scores: torch.Tensor, keep: int, stream=None) -
 def mlp_score(h: torch.Tensor, w1: torch.Tensor, b1: torch.Tensor, w2: torch.Tensor, b2: float,
               activation: str = "relu", ids: torch.Tensor | None = None, keep: int = 0, stream=None):
     """gambit_mlp_score: (scores [n] fp32, top-`keep` ids or None), on the device."""
+    if h.dim() != 2 or w1.dim() != 2:
+        raise ValueError("h: expected [n][dim], w1: expected [hidden][dim]")
     n, dim = h.shape
     hidden = w1.shape[0]
-    m = Mlp(dim, hidden, ACT_RELU if activation == "relu" else ACT_GELU, _dev(w1, torch.bfloat16).value,
-            _dev(b1, torch.float32).value, _dev(w2, torch.float32).value, float(b2))
+    _spec(h, torch.bfloat16, (n, dim), "h")
+    _spec(w1, torch.bfloat16, (hidden, dim), "w1")
+    _spec(b1, torch.float32, (hidden,), "b1")
+    _spec(w2, torch.float32, (hidden,), "w2")
+    if activation not in ("relu", "gelu"):
+        raise ValueError(f"activation: {activation!r}")
+    if keep > 0 and ids is None:
+        raise ValueError("ids: needed when keep > 0")
+    if ids is not None:
+        _spec(ids, torch.int32, (n,), "ids")
+    m = Mlp(dim, hidden, ACT_RELU if activation == "relu" else ACT_GELU, _dev(w1).value, _dev(b1).value,
+            _dev(w2).value, float(b2))
     ws_bytes = int(lib().gambit_mlp_workspace_size(n, hidden))
     ws = torch.empty(max(ws_bytes, 4), dtype=torch.uint8, device=h.device)
     scores = torch.empty(n, dtype=torch.float32, device=h.device)
@@ -227,6 +254,7 @@ class Pool:
         self.max_traces, self.max_blocks = max_traces, max_blocks_per_trace
         self.num_layers = num_layers
         cache_dtype = torch.uint8 if fp8 else torch.bfloat16
+        self.cache_dtype = cache_dtype
         # one layer: [num_blocks][Hkv][16][D]; several: a leading layer axis
         lead = (num_layers,) if num_layers > 1 else ()
         shape = lead + (num_blocks, num_kv_heads, 16, head_dim)
@@ -282,10 +310,22 @@ class Pool:
     def kv_write(self, trace: int, pos0: int, k: torch.Tensor, v: torch.Tensor, scales=None, stream=None):
         """k, v: [n][Hkv][D] (one layer) or [num_layers][n][Hkv][D]; fp8 scales
         [m][2] or [num_layers][m][2]."""
+        if k.dim() not in (3, 4):
+            raise ValueError("k: expected [n][Hkv][D] or [num_layers][n][Hkv][D]")
         n = k.shape[-3]
+        shape = ((self.num_layers,) if self.num_layers > 1 or k.dim() == 4 else ()) + (n, self.Hkv, self.D)
+        _spec(k, self.cache_dtype, shape, "k")
+        _spec(v, self.cache_dtype, shape, "v")
         sc = None
         if scales is not None:
+            if self.kv_dtype != "fp8_e4m3":
+                raise ValueError("scales: only fp8 pools take block scales")
             sc = np.ascontiguousarray(np.asarray(scales, np.float32))
+            # one (K, V) pair per block whose first position lies in [pos0, pos0 + n), per layer
+            m = -(-(pos0 + n) // 16) - -(-pos0 // 16)
+            want = (self.num_layers, m, 2)
+            if not (sc.shape == want or (self.num_layers == 1 and sc.shape == want[1:])):
+                raise ValueError(f"scales: expected shape {want if self.num_layers > 1 else want[1:]}, got {sc.shape}")
         self._check(lib().gambit_kv_write(self._h, trace, pos0, n, _dev(k), _dev(v),
                                           None if sc is None else _ptr(sc), _stream(stream)),
                     "kv_write")
@@ -305,11 +345,12 @@ class Pool:
         n = ids.size
         if out is None:
             out = torch.empty((n, self.Hq, self.D), dtype=out_dtype, device=q.device)
+        _spec(out, (torch.float32, torch.bfloat16), (n, self.Hq, self.D), "out")
         od = OUT_F32 if out.dtype == torch.float32 else OUT_BF16
-        if out.dtype not in (torch.float32, torch.bfloat16):
-            raise ValueError("out must be bf16 or fp32")
         sm = float(self.D ** -0.5 if sm_scale is None else sm_scale)
-        _dev(q, torch.bfloat16, (n, self.Hq, self.D))
+        _spec(q, torch.bfloat16, (n, self.Hq, self.D), "q")
+        _spec(k_new, self.cache_dtype, (n, self.Hkv, self.D), "k_new")
+        _spec(v_new, self.cache_dtype, (n, self.Hkv, self.D), "v_new")
         self._check(lib().gambit_decode_attn(self._h, n, _ptr(ids), _dev(q), _dev(k_new), _dev(v_new),
                                              _dev(out), od, sm, _stream(stream)), "decode_attn")
         return out
@@ -323,15 +364,16 @@ class Pool:
         n = ids.size
         if out is None:
             out = torch.empty((n, self.Hq, self.D), dtype=out_dtype, device=q.device)
-        if out.dtype not in (torch.float32, torch.bfloat16):
-            raise ValueError("out must be bf16 or fp32")
+        _spec(out, (torch.float32, torch.bfloat16), (n, self.Hq, self.D), "out")
         od = OUT_F32 if out.dtype == torch.float32 else OUT_BF16
+        if new_dtype not in ("cache", "bf16"):
+            raise ValueError(f"new_dtype: {new_dtype!r}")
         nd = {"cache": NEW_CACHE, "bf16": NEW_BF16}[new_dtype]
-        if nd == NEW_BF16:
-            _dev(k_new, torch.bfloat16, (n, self.Hkv, self.D))
-            _dev(v_new, torch.bfloat16, (n, self.Hkv, self.D))
+        ndt = torch.bfloat16 if nd == NEW_BF16 else self.cache_dtype
+        _spec(k_new, ndt, (n, self.Hkv, self.D), "k_new")
+        _spec(v_new, ndt, (n, self.Hkv, self.D), "v_new")
         sm = float(self.D ** -0.5 if sm_scale is None else sm_scale)
-        _dev(q, torch.bfloat16, (n, self.Hq, self.D))
+        _spec(q, torch.bfloat16, (n, self.Hq, self.D), "q")
         self._check(lib().gambit_decode_attn_layer(self._h, layer, n, _ptr(ids), _dev(q), _dev(k_new), _dev(v_new),
                                                    nd, _dev(out), od, sm, _stream(stream)), "decode_attn_layer")
         return out
@@ -341,25 +383,35 @@ class Pool:
         """Returns device tensors (scores [n], keep ids [keep], child/parent pairs [n-keep][2])."""
         ids = _host_i32(ids)
         n = ids.size
+        if h.dim() != 2:
+            raise ValueError("h: expected [n][Dh]")
+        Dh = h.shape[1]
+        _spec(h, torch.bfloat16, (n, Dh), "h")
+        _spec(w, torch.float32, (Dh,), "w")
+        if not 0 <= keep <= n:
+            raise ValueError(f"keep: {keep} not in [0, {n}]")
         dev = h.device
         scores = torch.empty(n, dtype=torch.float32, device=dev)
-        keep_out = torch.empty(keep, dtype=torch.int32, device=dev)
+        keep_out = torch.empty(max(keep, 1), dtype=torch.int32, device=dev)
         pairs = torch.empty((max(n - keep, 1), 2), dtype=torch.int32, device=dev)
-        _dev(h, torch.bfloat16)
         self._check(lib().gambit_score_prune_branch(self._h, n, _ptr(ids), _dev(h), h.shape[1],
                                                     _dev(w, torch.float32), float(b), keep, n_parents,
                                                     _dev(scores), _dev(keep_out), _dev(pairs),
                                                     _stream(stream)), "score_prune_branch")
-        return scores, keep_out, pairs[:n - keep]
+        return scores, keep_out[:keep], pairs[:n - keep]
 
     # -- the full tournament of Alg. 1
     def score_update(self, ids, h: torch.Tensor, w: torch.Tensor, b: float, stream=None) -> torch.Tensor:
         """gambit_score_update: thought scores f [n] (device); running means update in the pool."""
         ids = _host_i32(ids)
         n = ids.size
+        if h.dim() != 2 or h.shape[0] < n:
+            raise ValueError("h: expected [>= n][Dh]")
+        Dh = h.shape[1]
+        _spec(h, torch.bfloat16, None, "h")
+        _spec(w, torch.float32, (Dh,), "w")
         scores = torch.empty(max(n, 1), dtype=torch.float32, device=h.device)
-        _dev(h, torch.bfloat16)
-        self._check(lib().gambit_score_update(self._h, n, _ptr(ids), _dev(h), h.shape[1] if n else 8,
+        self._check(lib().gambit_score_update(self._h, n, _ptr(ids), _dev(h), Dh if n else 8,
                                               _dev(w, torch.float32), float(b), _dev(scores),
                                               _stream(stream)), "score_update")
         return scores[:n]
@@ -387,7 +439,9 @@ class Pool:
     def record_scores(self, ids, f: torch.Tensor, stream=None):
         """gambit_record_scores: running means from device thought scores f [n]."""
         ids = _host_i32(ids)
-        self._check(lib().gambit_record_scores(self._h, ids.size, _ptr(ids), _dev(f, torch.float32),
+        if f.dim() != 1 or f.shape[0] < ids.size:
+            raise ValueError("f: expected [>= n] fp32")
+        self._check(lib().gambit_record_scores(self._h, ids.size, _ptr(ids), _dev(f, torch.float32, None, "f"),
                                                _stream(stream)), "record_scores")
 
     def trace_state(self, ids, stream=None):

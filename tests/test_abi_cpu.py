@@ -4,6 +4,8 @@ import ctypes
 import os
 import re
 
+import numpy as np
+
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -88,3 +90,78 @@ def test_stream_read_rejects_bad_arguments_without_a_device():
            (fake, 65536, 2, 1, sink), (fake, 65536, 0, 1, None), (ctypes.c_void_p((1 << 20) + 4), 65536, 0, 1, sink)]
     for buf, nbytes, nt, grid, snk in bad:
         assert L.gambit_stream_read(buf, nbytes, nt, grid, snk, None) == gambit.ERR_INVALID
+
+
+def _fake_pool(kv_dtype="bf16", Hq=32, Hkv=8, num_layers=1):
+    """A Pool object without a device pool behind it: the binding's argument
+    checks run before any library call, so they can be exercised on a
+    machine without a GPU (every call below must fail in them)."""
+    import torch
+
+    from paper_2608_08020_amd import gambit
+    p = gambit.Pool.__new__(gambit.Pool)
+    p.kv_dtype, p.Hq, p.Hkv, p.D, p.num_layers = kv_dtype, Hq, Hkv, 128, num_layers
+    p.cache_dtype = torch.uint8 if kv_dtype == "fp8_e4m3" else torch.bfloat16
+    p.max_traces, p.max_blocks = 16, 8
+    p._h = None
+    return p
+
+
+def _raises(fn, match):
+    with pytest.raises(ValueError, match=match):
+        fn()
+
+
+def test_binding_checks_every_device_argument():
+    """Short or mistyped buffers would be read or written past their end by
+    the kernels (the C ABI takes bare pointers), so the binding checks each
+    one's dtype and shape first."""
+    import torch
+    bf, f32, u8, i32 = torch.bfloat16, torch.float32, torch.uint8, torch.int32
+    z = lambda *s, dt=bf: torch.zeros(s, dtype=dt)  # noqa: E731
+    n = 4
+    for kvd, cdt in [("bf16", bf), ("fp8_e4m3", u8)]:
+        p = _fake_pool(kvd)
+        q, kn, out = z(n, 32, 128), z(n, 8, 128, dt=cdt), z(n, 32, 128, dt=f32)
+        ids = list(range(n))
+        _raises(lambda: p.decode_attn(ids, q, kn, kn, out=z(n - 1, 32, 128, dt=f32)), "out: expected shape")
+        _raises(lambda: p.decode_attn(ids, q, kn, kn, out=z(n, 32, 128, dt=torch.float16)), "out: expected dtype")
+        _raises(lambda: p.decode_attn(ids, z(n, 32, 64), kn, kn, out=out), "q: expected shape")
+        _raises(lambda: p.decode_attn(ids, q, z(n - 1, 8, 128, dt=cdt), kn, out=out), "k_new: expected shape")
+        _raises(lambda: p.decode_attn(ids, q, kn, z(n, 8, 127, dt=cdt), out=out), "v_new: expected shape")
+        other = u8 if cdt == bf else bf
+        _raises(lambda: p.decode_attn(ids, q, z(n, 8, 128, dt=other), kn, out=out), "k_new: expected dtype")
+        _raises(lambda: p.decode_attn(ids, q, kn, kn, out=out), "expected a device tensor")  # all well-formed
+        # one layer of a step: new K/V in the cache dtype or bf16 (quantised on append)
+        _raises(lambda: p.decode_attn_layer(0, ids, q, z(n, 8, 128, dt=other if cdt == u8 else u8), kn, out=out),
+                "k_new: expected dtype")
+        _raises(lambda: p.decode_attn_layer(0, ids, q, z(n, 8, 128), z(n - 1, 8, 128), new_dtype="bf16", out=out),
+                "v_new: expected shape")
+        _raises(lambda: p.decode_attn_layer(0, ids, q, kn, kn, new_dtype="fp16", out=out), "new_dtype")
+        # writes: [n][Hkv][D] in the cache dtype; fp8 scales one (K, V) pair per block started
+        _raises(lambda: p.kv_write(0, 0, z(20, 8, 128, dt=cdt), z(19, 8, 128, dt=cdt)), "v: expected shape")
+        _raises(lambda: p.kv_write(0, 0, z(20, 4, 128, dt=cdt), z(20, 4, 128, dt=cdt)), "k: expected shape")
+    p = _fake_pool("fp8_e4m3")
+    k20 = z(20, 8, 128, dt=u8)
+    _raises(lambda: p.kv_write(0, 0, k20, k20, np.ones((1, 2), np.float32)), "scales: expected shape \\(2, 2\\)")
+    _raises(lambda: p.kv_write(0, 10, k20, k20, np.ones((1, 2), np.float32)), "expected a device tensor")  # one block starts in 10..29
+    _raises(lambda: p.kv_write(0, 10, k20, k20, np.ones((2, 2), np.float32)), "scales: expected shape \\(1, 2\\)")
+    _raises(lambda: _fake_pool("bf16").kv_write(0, 0, z(3, 8, 128), z(3, 8, 128), np.ones((1, 2))), "scales: only fp8")
+    # a thought boundary: h [n][Dh] bf16, w [Dh] fp32
+    p = _fake_pool()
+    _raises(lambda: p.score_prune_branch(range(n), z(n - 1, 64), z(64, dt=f32), 0.0, 2, 2), "h: expected shape")
+    _raises(lambda: p.score_prune_branch(range(n), z(n, 64), z(32, dt=f32), 0.0, 2, 2), "w: expected shape")
+    _raises(lambda: p.score_prune_branch(range(n), z(n, 64, dt=f32), z(64, dt=f32), 0.0, 2, 2), "h: expected dtype")
+    _raises(lambda: p.score_prune_branch(range(n), z(n, 64), z(64, dt=f32), 0.0, 5, 2), "keep")
+    _raises(lambda: p.score_update(range(n), z(n - 1, 64), z(64, dt=f32), 0.0), "h: expected")
+    _raises(lambda: p.score_update(range(n), z(n, 64), z(63, dt=f32), 0.0), "w: expected shape")
+    _raises(lambda: p.record_scores(range(n), z(n - 1, dt=f32)), "f: expected")
+    # the stateless calls
+    from paper_2608_08020_amd.gambit import mlp_score, rank_topk
+    h, w1, b1, w2 = z(n, 256), z(128, 256), z(128, dt=f32), z(128, dt=f32)
+    _raises(lambda: mlp_score(h, z(128, 255), b1, w2, 0.0), "w1: expected shape")
+    _raises(lambda: mlp_score(h, w1, z(127, dt=f32), w2, 0.0), "b1: expected shape")
+    _raises(lambda: mlp_score(h, w1, b1, z(128), 0.0), "w2: expected dtype")
+    _raises(lambda: mlp_score(h, w1, b1, w2, 0.0, keep=2), "ids: needed")
+    _raises(lambda: mlp_score(h, w1, b1, w2, 0.0, ids=z(n - 1, dt=i32), keep=2), "ids: expected shape")
+    _raises(lambda: rank_topk(z(n, dt=i32), z(n - 1, dt=f32), 2), "scores: expected shape")
