@@ -343,6 +343,25 @@ gambit_status gambit_pool_check(gambit_pool* pool, void* stream);
 gambit_status gambit_plan_stats(gambit_pool* pool, int32_t n, const int32_t* trace_ids,
                                 gambit_stats* out);
 
+/* The kinds of attention work that cover each listed trace in the plan the
+ * pool's decode steps of this exact trace list use (host only, no sync; the
+ * plan is made by the first decode step after the list or the pool's block
+ * sharing changed, so call this after such a step).  kinds_out host [n]:
+ * an OR of GAMBIT_UNIT_* bits, one per kind of work unit whose rows include
+ * the trace (narrow one-wave units; cooperative workgroup items with one or
+ * two row blocks per wave, or - fp8 items of at most 32 rows - tile pairs);
+ * GAMBIT_UNIT_TAIL_SLOT when one of them sits in the workgroup slots that
+ * the launch claims at run time.  For test coverage of the kernel's paths.
+ * GAMBIT_ERR_INVALID when the current plan is not for this list. */
+enum {
+  GAMBIT_UNIT_NARROW = 1,
+  GAMBIT_UNIT_COOP_ONE = 2,
+  GAMBIT_UNIT_COOP_TWO = 4,
+  GAMBIT_UNIT_COOP_PAIRS = 8,
+  GAMBIT_UNIT_TAIL_SLOT = 16
+};
+gambit_status gambit_plan_kinds(gambit_pool* pool, int32_t n, const int32_t* trace_ids, int32_t* kinds_out);
+
 /* Event timing of the split-K attention kernel, the dominant kernel of a
  * decode step.  Between gambit_profile_begin and gambit_profile_end every
  * gambit_decode_attn records a HIP event pair on its stream around that

@@ -135,6 +135,7 @@ struct gambit_pool {
   gambit::AttnLaunch step{};       // the open step's launch arguments
   std::vector<int32_t> cnt, first;  // per-block planner scratch, zero / -1 between calls
   gambit_stats stats{};            // of plan_list, kept current by decode steps
+  std::vector<int32_t> plan_kinds;  // per list position: GAMBIT_UNIT_* bits of the units covering it
 
   // attention-kernel event timing
   std::vector<hipEvent_t> prof_ev;
@@ -588,6 +589,30 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
   p->n_units = (int)units.size();
   if ((int)units.size() > p->L.max_units || (int)members.size() > p->L.max_members)
     return fail(p, GAMBIT_ERR_UNSUPPORTED, "plan exceeds workspace bounds");
+  // The kinds of work covering each list position, as the kernel will pick
+  // them (gambit_plan_kinds): a slot in an XCD's last kTailSlots is claimed
+  // at run time.
+  p->plan_kinds.assign(n, 0);
+  for (int x = 0; x < 8; ++x) {
+    const int nslots = (p->xcd_off[x + 1] - p->xcd_off[x]) / gambit::kUnitsPerWG;
+    const int tail0 = std::max(nslots - gambit::kTailSlots, 0);
+    for (int j = 0; j < nslots; ++j) {
+      const int base = p->xcd_off[x] + gambit::kUnitsPerWG * j;
+      const int32_t tail = j >= tail0 ? GAMBIT_UNIT_TAIL_SLOT : 0;
+      auto mark = [&](const AttnUnit& u, int32_t kind) {
+        for (int m = 0; m < u.mem_cnt; ++m) p->plan_kinds[members[u.mem_off + m]] |= kind | tail;
+      };
+      const AttnUnit& u0 = units[base];
+      if (u0.flags & gambit::kUnitCoop) {
+        const int rows = u0.mem_cnt * p->g;
+        mark(u0, rows > 4 * gambit::kRowsPerUnit ? GAMBIT_UNIT_COOP_TWO
+                 : (p->d.kv_dtype == GAMBIT_KV_FP8_E4M3 && rows <= 2 * gambit::kRowsPerUnit) ? GAMBIT_UNIT_COOP_PAIRS
+                                                                                             : GAMBIT_UNIT_COOP_ONE);
+      } else {
+        for (int w = 0; w < gambit::kUnitsPerWG; ++w) mark(units[base + w], GAMBIT_UNIT_NARROW);
+      }
+    }
+  }
 
   // upload: list, nk, members, units through the pinned plan stage
   HIP_TRY(p, hipEventSynchronize(p->plan_ev), "plan fence");
@@ -1071,6 +1096,15 @@ gambit_status gambit_score_prune_branch(gambit_pool* p, int32_t n, const int32_t
   mirror_free_many(p, freed.data(), nfree_traces);
   mirror_fork_many(p, par.data(), freed.data(), nfree_traces);
   invalidate_plan(p);
+  return GAMBIT_OK;
+}
+
+gambit_status gambit_plan_kinds(gambit_pool* p, int32_t n, const int32_t* ids, int32_t* kinds_out) {
+  if (!p) return GAMBIT_ERR_INVALID;
+  if (n < 0 || (n > 0 && (!ids || !kinds_out))) return fail(p, GAMBIT_ERR_INVALID, "bad list or output");
+  if (!p->plan_valid || (int)p->plan_list.size() != n || !std::equal(p->plan_list.begin(), p->plan_list.end(), ids))
+    return fail(p, GAMBIT_ERR_INVALID, "no attention plan for this trace list (run a decode step first)");
+  std::copy(p->plan_kinds.begin(), p->plan_kinds.end(), kinds_out);
   return GAMBIT_OK;
 }
 

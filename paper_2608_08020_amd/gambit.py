@@ -22,6 +22,7 @@ OK, ERR_INVALID, ERR_OUT_OF_BLOCKS, ERR_SHARED_WRITE, ERR_UNSUPPORTED, ERR_DEVIC
 KV_BF16, KV_FP8_E4M3 = 0, 1
 OUT_BF16, OUT_F32 = 0, 1
 NEW_CACHE, NEW_BF16 = 0, 1
+UNIT_NARROW, UNIT_COOP_ONE, UNIT_COOP_TWO, UNIT_COOP_PAIRS, UNIT_TAIL_SLOT = 1, 2, 4, 8, 16
 CODE_NAMES = {ERR_INVALID: "INVALID", ERR_OUT_OF_BLOCKS: "OUT_OF_BLOCKS",
               ERR_SHARED_WRITE: "SHARED_WRITE", ERR_UNSUPPORTED: "UNSUPPORTED",
               ERR_DEVICE: "DEVICE", ERR_WORKSPACE: "WORKSPACE"}
@@ -87,7 +88,8 @@ EXPORTS = ["gambit_workspace_size", "gambit_pool_create", "gambit_pool_destroy",
            "gambit_evict", "gambit_tournament", "gambit_trace_state", "gambit_record_scores",
            "gambit_mlp_workspace_size", "gambit_mlp_score", "gambit_scorer_workspace_size", "gambit_scorer_create",
            "gambit_scorer_destroy", "gambit_scorer_step", "gambit_scorer_fork", "gambit_scorer_free",
-           "gambit_scorer_steps", "gambit_scorer_check", "gambit_scorer_last_error", "gambit_stream_read"]
+           "gambit_scorer_steps", "gambit_scorer_check", "gambit_scorer_last_error", "gambit_stream_read",
+           "gambit_plan_kinds"]
 
 
 def lib() -> ctypes.CDLL:
@@ -135,6 +137,7 @@ def lib() -> ctypes.CDLL:
         "gambit_scorer_check": (i32, [vp, vp]),
         "gambit_scorer_last_error": (ctypes.c_char_p, [vp]),
         "gambit_stream_read": (i32, [vp, ctypes.c_size_t, i32, i32, vp, vp]),
+        "gambit_plan_kinds": (i32, [vp, i32, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -462,6 +465,13 @@ class Pool:
         s = Stats()
         self._check(lib().gambit_plan_stats(self._h, ids.size, _ptr(ids), ctypes.byref(s)), "plan_stats")
         return s
+
+    def plan_kinds(self, ids) -> np.ndarray:
+        """gambit_plan_kinds: UNIT_* bits per listed trace in the current plan."""
+        ids = _host_i32(ids)
+        out = np.zeros(ids.size, np.int32)
+        self._check(lib().gambit_plan_kinds(self._h, ids.size, _ptr(ids), _ptr(out)), "plan_kinds")
+        return out
 
     def profile_begin(self, max_launches: int):
         """gambit_profile_begin: time the split-K attention kernel of each decode step."""

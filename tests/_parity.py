@@ -12,6 +12,7 @@ oracle, with the parity bar:
 """
 from __future__ import annotations
 
+import os
 import time
 
 import numpy as np
@@ -25,6 +26,9 @@ ATOL, RTOL = 1e-3, 2e-3
 BF16_OUT_REL = 2.0 ** -8
 SCORE_TOL = 1e-4
 NEAR_TIE = 1e-6
+
+# worst attention error of each replay, by test (printed in pytest's summary)
+WORST: dict = {}
 
 
 def say(msg):
@@ -73,7 +77,11 @@ def replay(wl, *, sample_steps=None, sample_traces=None, out_dtype=torch.float32
            share_nodes=True, check_pool_every_step=False, max_splits=0, quantise_on_append=False):
     """quantise_on_append: the steps' new K/V go in as bf16 and the fp8 pool
     quantises them (the oracle with its own encoder and the landing blocks'
-    scales) instead of arriving as the generator's codes."""
+    scales) instead of arriving as the generator's codes.
+
+    sample_traces: list positions to compare at the sampled steps (default
+    all), or a callable (run, step) -> positions, called after the step's
+    decode (so it can read the plan that step used)."""
     from paper_2608_08020_amd.runner import PopulationRun, estimate_blocks
 
     t0 = time.time()
@@ -107,7 +115,9 @@ def replay(wl, *, sample_steps=None, sample_traces=None, out_dtype=torch.float32
 
     steps = range(wl.total_steps)
     sample_steps = set(steps) if sample_steps is None else set(sample_steps)
-    traces = list(range(wl.T)) if sample_traces is None else list(sample_traces)
+    pick = sample_traces if callable(sample_traces) else None
+    traces = list(range(wl.T)) if sample_traces is None else (None if pick else list(sample_traces))
+    n_checked = 0
     rounds = {s: i for i, s in enumerate(wl.rounds_after())}
     run.load_rounds(range(len(rounds)))
     ids = list(range(wl.T))
@@ -128,11 +138,13 @@ def replay(wl, *, sample_steps=None, sample_traces=None, out_dtype=torch.float32
                 out = run.decode(s, out_dtype=out_dtype)
                 model.append(ids, k, v)
             if s in sample_steps:
-                got = out[traces].float().cpu().numpy()
-                ref = orun.attend(model, wl, q, traces)
-                for i, t in enumerate(traces):
+                tr = list(pick(run, s)) if pick else traces
+                got = out[tr].float().cpu().numpy()
+                ref = orun.attend(model, wl, q, tr)
+                for i, t in enumerate(tr):
                     worst = max(worst, assert_attn_close(got[i], ref[t], f"step {s} trace {t}",
                                                          bf16_out=out_dtype == torch.bfloat16))
+                n_checked += len(tr)
             if check_pool_every_step:
                 run.pool.pool_check()
             if s in rounds:
@@ -155,5 +167,8 @@ def replay(wl, *, sample_steps=None, sample_traces=None, out_dtype=torch.float32
                 compare_tables(run, model, f"round {r}")
                 say(f"round {r} after step {s}: keep/pairs/tables bit-exact")
             del run.host[s], run.q[s], run.kv[s]
-    say(f"done: worst |err| {worst:.3g}, near ties {near_ties}, {time.time() - t0:.1f}s")
+    say(f"done: worst |err| {worst:.3g} over {n_checked} (trace, step) outputs, near ties {near_ties}, "
+        f"{time.time() - t0:.1f}s")
+    test = os.environ.get("PYTEST_CURRENT_TEST", wl.cfg.name).split(" ")[0]
+    WORST[test] = (worst, n_checked, "bf16" if out_dtype == torch.bfloat16 else "fp32")
     return run, model, worst
