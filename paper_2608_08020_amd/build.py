@@ -10,13 +10,14 @@ from __future__ import annotations
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libgambit.so")
-SOURCES = ["gambit_pool.cpp", "blocktable.hip", "decode_attn.hip", "probe_topk.hip", "seq_scorer.cpp",
-           "seqscorer.hip", "membench.hip"]
+SOURCES = ["gambit_pool.cpp", "blocktable.hip", "decode_attn.hip", "probe_topk.hip",
+           "seq_scorer.cpp", "seqscorer.hip", "membench.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-mcode-object-version=5",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -31,10 +32,10 @@ EXTRA = {"decode_attn.hip": ["-fno-honor-nans", "-mno-amdgpu-ieee"]}
 
 
 def build(verbose: bool = False) -> str:
-    objs = []
     build_dir = os.path.join(HERE, "_build")
     os.makedirs(build_dir, exist_ok=True)
-    for src in SOURCES:
+
+    def compile_one(src):
         obj = os.path.join(build_dir, src + ".o")
         cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
@@ -42,7 +43,11 @@ def build(verbose: bool = False) -> str:
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")
-        objs.append(obj)
+        return obj
+
+    jobs = max(1, min(len(SOURCES), len(os.sched_getaffinity(0)), 8))
+    with ThreadPoolExecutor(jobs) as ex:
+        objs = list(ex.map(compile_one, SOURCES))
     tmp = LIB + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-pthread", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
