@@ -6,10 +6,15 @@ split-K attention + merge) with the thought-boundary round (probe, rank,
 prune, branch) every `interval` steps, exactly as the workload schedules it.
 The default workload is 512 Qwen3-8B-shaped traces (32 q heads, 8 KV heads,
 head dim 128, bf16 KV) in a 5-generation branch tree with contexts up to
-32768 tokens, rounds every 256 steps keeping 128 and forking 4x.  The
-warm-up covers the first round, so the timed steps measure the steady state.
+32768 tokens, rounds every 256 steps keeping 128 and forking 4x, over its
+1024-step schedule.  The first interval (its decode steps and the first
+round) always runs untimed, then W warm-up steps, then K timed steps: the
+timed steps measure the steady state after the first prune/branch round,
+whatever K and W are.  The timing is repeated in R replays, each of which
+replays the op log into a fresh pool; the line reports the median and the
+spread.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 4]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--replays R] [--config 4]
 
 Prints one JSON line.  `value` is trace-steps/s over the timed steps with
 every input already resident in HBM.  `roofline` prices the dominant kernel
@@ -17,7 +22,9 @@ every input already resident in HBM.  `roofline` prices the dominant kernel
 population references read once, plus queries, block-table entries and the
 step's append that the same launch performs (new K/V read and written) - over
 its event-timed average duration.  `cpu_baseline` times the CPU oracle on a
-bounded sample of the same workload.  `tournament` times rounds of the full
+bounded sample of the same workload (the first step, the first step after
+each round, the last step).  `initial_tree` reports the attention launches
+of the first interval (the tree before any round) beside the headline.  `tournament` times rounds of the full
 tournament of Alg. 1 (C = 256, K = 16: running-mean scoring, an eviction
 into a ghost every other round, rank / prune / branch) and the oracle's
 rounds beside them.  `fp8_layers` times decode steps through all 64
@@ -49,48 +56,80 @@ def kernel_sha() -> str:
     return source_sha()
 
 
-def measured_traffic(workload: str):
+def measured_traffic(workload: str, timed_steps):
     """Per-launch HBM bytes from the committed rocprofv3 counter runs, if they
-    were taken on the current kernel and planner sources and this workload."""
+    were taken on the current kernel and planner sources, this workload and
+    exactly these timed steps (the pool state the counters saw)."""
     try:
         with open(TRAFFIC_FILE) as f:
-            rec = json.load(f)
+            recs = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_sha") != kernel_sha() or rec.get("workload") != workload:
-        return None
-    return rec.get("bytes_per_launch")
+    for rec in recs if isinstance(recs, list) else [recs]:
+        if (rec.get("kernel_sha") == kernel_sha() and rec.get("workload") == workload
+                and rec.get("timed_steps") == list(timed_steps)):
+            return rec.get("bytes_per_launch")
+    return None
 
 
 def cpu_baseline(wl, budget_s: float):
-    """Oracle attention for sampled traces at the workload's first decode step."""
+    """The oracle's attention, timed on the host, on a bounded sample of the
+    workload: traces at the first decode step, the first step after each
+    round and the last step (an equal share of the budget each).  The oracle
+    replays the whole schedule (appends and rounds) to reach those steps; only
+    its attention is timed, with every trace's inputs generated beforehand."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
     from oracle import run as orun
 
     T = wl.T
-    model = orun.new_pool(wl, 1 + sum(n.length // 16 + 2 for n in wl.tree.nodes) + 4 * T)
+    ids = list(range(T))
+    rounds = wl.rounds_after()
+    sample = sorted({0, wl.total_steps - 1} | {r + 1 for r in rounds if r + 1 < wl.total_steps})
+    share = budget_s / len(sample)
+    model = orun.new_pool(wl, 1 + sum(n.length // 16 + 2 for n in wl.tree.nodes)
+                          + (len(rounds) + 1) * T * (wl.total_steps // 16 + 2))
     orun.apply_setup(model, wl, lazy=True)
-    k, v = wl.step_kv(0)
-    model.append(list(range(T)), k, v)
-    q = wl.step_q(0)
-    order = [int(t) for t in np.random.default_rng(0).permutation(T)]
-    done, spent, tokens = 0, 0.0, 0
-    for t in order:
-        model.materialise(t)                     # generate the lazily keyed inputs, untimed
-        t0 = time.perf_counter()
-        orun.attend(model, wl, q, [t])
-        spent += time.perf_counter() - t0
-        done += 1
-        tokens += model.seq_len[t]
-        if spent >= budget_s:
-            break
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    return {"value": done / spent, "unit": "trace-steps/s", "cores": threads, "kind": "oracle",
-            "sample": (f"{done} traces (mean context {tokens / done:.0f} tokens) of the first decode "
-                       f"step, fp64 dense attention on materialised per-trace KV, "
-                       f"{spent:.1f} s; {len(os.sched_getaffinity(0))} host cores visible")}
+    cache = {}
+
+    def step_kv(s, i):
+        if s not in cache:
+            cache[s] = wl.step_kv(s)
+        return cache[s][i]
+
+    rng = np.random.default_rng(0)
+    done, spent, tokens, per_step = 0, 0.0, 0, []
+    round_of = {s: i for i, s in enumerate(rounds)}
+    for s in range(wl.total_steps):
+        model.append(ids, lambda s=s: step_kv(s, 0), lambda s=s: step_kv(s, 1))
+        if s in sample:
+            q = wl.step_q(s)
+            n_s, t_s = 0, 0.0
+            for t in rng.permutation(T).tolist():
+                model.materialise(t)              # generate the lazily keyed inputs, untimed
+                t0 = time.perf_counter()
+                orun.attend(model, wl, q, [t])
+                t_s += time.perf_counter() - t0
+                n_s += 1
+                tokens += model.seq_len[t]
+                if t_s >= share:
+                    break
+            per_step.append((s, n_s))
+            done += n_s
+            spent += t_s
+        if s in round_of:
+            orun.run_round(model, wl, round_of[s], ids)
+    info = threadpool_info()
+    blas = [f"{p.get('internal_api', p.get('user_api'))} {p.get('version', '')} ({p.get('num_threads')} threads)"
+            for p in info]
+    threads = max([p.get("num_threads", 1) for p in info] or [1])
+    return {"value": done / spent, "unit": "trace-steps/s", "cores": len(os.sched_getaffinity(0)),
+            "kind": "oracle", "blas": "; ".join(blas) or "none", "blas_threads": threads,
+            "sample": (f"{done} (trace, step) attentions, mean context {tokens / done:.0f} tokens, at steps "
+                       + ", ".join(f"{s} ({n} traces)" for s, n in per_step)
+                       + f"; fp64 dense attention on materialised per-trace KV, {spent:.1f} s of attention; "
+                         f"{len(os.sched_getaffinity(0))} host cores in the process's affinity")}
 
 
 def read_ceiling(gib: int = 16, grid: int = 4096, reps: int = 5):
@@ -354,16 +393,102 @@ def scorer_measure(history: int = 128, reps: int = 10):
             "note": "fp32 weights, activations and caches; 22 launches per boundary (2 layers)"}
 
 
+def alg_bytes(cfg, st, T) -> int:
+    """Algorithmic bytes of one attention launch: every distinct block the
+    listed traces reference (valid tokens), fp8 scales, queries, block-table
+    entries, and the step's append (new K/V read and written into the cache)."""
+    e = cfg.kv_elem_bytes
+    Hkv, D, Hq = cfg.n_kv_heads, cfg.head_dim, cfg.n_q_heads
+    return (st.unique_tokens * Hkv * D * 2 * e + (8 * st.unique_blocks if e == 1 else 0)
+            + T * Hq * D * 2 + 4 * st.table_entries + 2 * T * Hkv * D * 2 * e)
+
+
+def replay(wl, W, K, node_data, inputs_from=None, initial=False):
+    """One timed replay of the schedule into a fresh pool: the op log builds
+    the initial tree; the first interval (its decode steps and the first
+    round) and W warm-up steps run untimed; K steps are timed, rounds
+    included, bracketed by HIP events on the pool's stream and a device
+    synchronisation.  With `initial`, the attention launches of the first
+    interval are also timed (the initial tree, before any round)."""
+    import torch
+
+    from paper_2608_08020_amd.runner import PopulationRun
+
+    cfg = wl.cfg
+    T = wl.T
+    first = wl.rounds_after()[0] + 1          # steps up to and including the first round
+    run = PopulationRun(wl)
+    if inputs_from is not None:
+        run.share_inputs(inputs_from)
+    run.setup(node_data)
+    run.load_steps(range(first + W + K))
+    rounds = wl.rounds_after()
+    run.load_rounds(range(len(rounds)))
+    round_of = {s: i for i, s in enumerate(rounds)}
+    out = torch.empty((T, cfg.n_q_heads, cfg.head_dim), dtype=torch.bfloat16, device="cuda")
+    pool = run.pool
+    res = {}
+    torch.cuda.synchronize()
+    if initial:
+        pool.profile_begin(first)
+        ib = []
+        for s in range(first):
+            run.decode(s, out=out)
+            ib.append(alg_bytes(cfg, pool.plan_stats(run.ids), T))
+        ms, n = pool.profile_end()
+        res["initial"] = (sum(ib) / len(ib), ms / n)
+        run.round(round_of[first - 1])
+    else:
+        for s in range(first):
+            run.decode(s, out=out)
+            if s in round_of:
+                run.round(round_of[s])
+    for s in range(first, first + W):
+        run.decode(s, out=out)
+        if s in round_of:
+            run.round(round_of[s])
+    torch.cuda.synchronize()
+    pool.profile_begin(K)
+    ab, ctx, round_ev = [], 0, []
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record()
+    for s in range(first + W, first + W + K):
+        run.decode(s, out=out)
+        st = pool.plan_stats(run.ids)
+        ab.append(alg_bytes(cfg, st, T))
+        ctx += st.total_tokens
+        if s in round_of:
+            r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            r0.record()
+            run.round(round_of[s])
+            r1.record()
+            round_ev.append((r0, r1))
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    attn_ms, launches = pool.profile_end()
+    pool.pool_check()
+    res.update(wall=wall, event_ms=start.elapsed_time(end), attn_s=attn_ms / 1e3 / launches, launches=launches,
+               alg=sum(ab) / len(ab), ctx=ctx / K / T, rounds=[round(a.elapsed_time(b) * 1e3, 1) for a, b in round_ev],
+               timed=(first + W, first + W + K - 1))
+    return run, res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=None)
-    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--steps", type=int, default=20, help="timed steps K")
+    ap.add_argument("--warmup", type=int, default=5,
+                    help="untimed steps W after the first interval (which always runs untimed)")
+    ap.add_argument("--replays", type=int, default=5, help="timed replays, each into a fresh pool")
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-tournament", action="store_true")
     ap.add_argument("--no-layers", action="store_true")
+    ap.add_argument("--no-ceiling", action="store_true")
     ap.add_argument("--layers", type=int, default=64)
     ap.add_argument("--scorer-only", action="store_true", help="time only the sequence scorer and print it")
     ap.add_argument("--mlp-only", action="store_true", help="time only the MLP scorer and print it")
@@ -386,75 +511,53 @@ def main():
         print(json.dumps({"tournament": tournament_rounds()}), flush=True)
         return
 
-    from paper_2608_08020_amd.runner import PopulationRun
+    from paper_2608_08020_amd.runner import _to_dev
     from workload import CONFIGS, Workload
 
     cfg = CONFIGS[args.config]
-    W = cfg.interval if args.warmup is None else args.warmup
-    K = (cfg.steps - W) if args.steps is None else args.steps
-    if K <= 0:
-        raise SystemExit("need at least one timed step")
-    t_setup = time.time()
-    wl = Workload(cfg, total_steps=W + K)
-    run = PopulationRun(wl)
-    run.setup()
-    log(f"{cfg.name}: setup {time.time() - t_setup:.1f}s")
-    run.load_steps(range(W + K))
-    rounds = wl.rounds_after()
-    run.load_rounds(range(len(rounds)))
-    log(f"inputs resident ({time.time() - t_setup:.1f}s)")
+    W, K = args.warmup, args.steps
+    wl = Workload(cfg)                         # the configuration's own schedule and tree
+    first = wl.rounds_after()[0] + 1
+    if K <= 0 or W < 0 or first + W + K > wl.total_steps:
+        raise SystemExit(f"need K >= 1, W >= 0 and {first} (first interval) + W + K <= {wl.total_steps} steps")
     T = wl.T
-    ids = run.ids
-    out = torch.empty((T, cfg.n_q_heads, cfg.head_dim), dtype=torch.bfloat16, device="cuda")
-    round_of = {s: i for i, s in enumerate(rounds)}
+    cache_dtype = torch.uint8 if wl.fp8 else torch.bfloat16
+    nodes = {}
 
-    torch.cuda.synchronize()
-    w0 = time.perf_counter()
-    for s in range(W):
-        run.decode(s, out=out)
-        if s in round_of:
-            run.round(round_of[s])
-    torch.cuda.synchronize()
-    warm_wall = time.perf_counter() - w0
-    log(f"warm-up {W} steps done")
+    def node_data(nid):                        # generated once, kept resident for later replays
+        if nid not in nodes:
+            k, v, sc = wl.node_kv(nid)
+            nodes[nid] = (_to_dev(k, cache_dtype, "cuda"), _to_dev(v, cache_dtype, "cuda"), sc)
+        return nodes[nid]
 
+    reps, prev = [], None
+    t_setup = time.time()
+    for r in range(args.replays):
+        if prev is not None:               # free the previous replay's pool before the next one's
+            prev.pool.close()
+            prev.pool = None
+        prev, res = replay(wl, W, K, node_data, inputs_from=prev, initial=r == 0)
+        log(f"{cfg.name}: replay {r}: {res['wall'] * 1e3 / K:.4f} ms/step, attention {res['attn_s'] * 1e6:.1f} us "
+            f"({time.time() - t_setup:.1f}s)")
+        reps.append(res)
+    init_bytes, init_ms = reps[0]["initial"]
+    prev.pool.close()
+    del prev
+    nodes.clear()
+    torch.cuda.empty_cache()
+
+    walls = sorted(x["wall"] for x in reps)
+    attn = sorted(x["attn_s"] for x in reps)
+    med = lambda v: v[len(v) // 2] if len(v) % 2 else 0.5 * (v[len(v) // 2 - 1] + v[len(v) // 2])  # noqa: E731
+    wall, attn_s = med(walls), med(attn)
+    bytes_per_launch = reps[0]["alg"]
+    assert all(abs(x["alg"] - bytes_per_launch) < 1 for x in reps), "replays differ in their work"
+    value = T * K / wall
+    achieved = bytes_per_launch / attn_s / 1e9
+    timed = reps[0]["timed"]
+    traffic = measured_traffic(cfg.name, timed)
     e = cfg.kv_elem_bytes
     Hkv, D, Hq = cfg.n_kv_heads, cfg.head_dim, cfg.n_q_heads
-    pool = run.pool
-    pool.profile_begin(K)
-    alg_bytes, ctx_tokens = [], 0
-    round_ev = []  # (start, end) events around each probe / rank / prune / branch round
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    start.record()
-    for s in range(W, W + K):
-        run.decode(s, out=out)
-        st = pool.plan_stats(ids)
-        # every distinct block once (valid tokens), fp8 scales, queries, table
-        # entries, and the step's append (new K/V read, written into the cache)
-        alg_bytes.append(st.unique_tokens * Hkv * D * 2 * e + (8 * st.unique_blocks if e == 1 else 0)
-                         + T * Hq * D * 2 + 4 * st.table_entries + 2 * T * Hkv * D * 2 * e)
-        ctx_tokens += st.total_tokens
-        if s in round_of:
-            r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            r0.record()
-            run.round(round_of[s])
-            r1.record()
-            round_ev.append((r0, r1))
-    end.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ev_ms = start.elapsed_time(end)
-    attn_ms, launches = pool.profile_end()
-    pool.pool_check()
-    timed_rounds = sum(1 for s in range(W, W + K) if s in round_of)
-
-    value = T * K / wall
-    bytes_per_launch = sum(alg_bytes) / len(alg_bytes)
-    attn_avg_s = attn_ms / 1e3 / launches
-    achieved = bytes_per_launch / attn_avg_s / 1e9
-    traffic = measured_traffic(cfg.name)
     res = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -469,27 +572,41 @@ def main():
         "dtype": "bf16" if e == 2 else "fp8_e4m3 KV, bf16 q, fp32 accumulate",
         "data": "synthetic (seeded; shapes from the paper's trace statistics)",
         "config": {"workload": cfg.name, "traces": T, "q_heads": Hq, "kv_heads": Hkv, "head_dim": D,
-                   "kv_dtype": cfg.kv_dtype, "mean_context_tokens": round(ctx_tokens / K / T),
+                   "kv_dtype": cfg.kv_dtype, "schedule_steps": wl.total_steps,
+                   "timed_steps": list(timed), "steady_state": True,
+                   "untimed_before": f"steps 0-{first - 1} and the first round, then {W} warm-up steps",
+                   "mean_context_tokens": round(reps[0]["ctx"]),
                    "round_every_steps": cfg.interval, "keep": cfg.keep, "fanout": cfg.fanout,
-                   "rounds_in_timed_steps": timed_rounds, "parallelism": "single GPU"},
+                   "rounds_in_timed_steps": len(reps[0]["rounds"]), "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": traffic, "kernel": "attn_units_kernel (split-K shared-run attention)",
                      "alg_bytes_per_launch": round(bytes_per_launch),
-                     "avg_launch_us": round(attn_avg_s * 1e6, 2), "launches_timed": launches},
-        "step_hbm_GBps": round(sum(alg_bytes) / wall / 1e9, 1),
+                     "avg_launch_us": round(attn_s * 1e6, 2), "launches_timed": reps[0]["launches"],
+                     "timing": "HIP events around each launch on the pool's stream; median over replays"},
+        "replays": {"n": len(reps), "fresh_pool_each": True,
+                    "ms_per_step": [round(x["wall"] * 1e3 / K, 4) for x in reps],
+                    "attn_launch_us": [round(x["attn_s"] * 1e6, 2) for x in reps],
+                    "spread": {"ms_per_step_min": round(walls[0] * 1e3 / K, 4),
+                               "ms_per_step_max": round(walls[-1] * 1e3 / K, 4),
+                               "rel": round((walls[-1] - walls[0]) / wall, 4),
+                               "attn_us_min": round(attn[0] * 1e6, 2), "attn_us_max": round(attn[-1] * 1e6, 2)}},
+        "step_hbm_GBps": round(bytes_per_launch * K / wall / 1e9, 1),
         # context: dense per-trace attention would read every trace's whole context
-        "naive_bytes_per_step": round(ctx_tokens / K * Hkv * D * 2 * e),
-        "whole_run": {"steps": W + K, "trace_steps_per_s": round(T * (W + K) / (warm_wall + wall), 1),
-                      "first_interval_ms_per_step": round(warm_wall * 1e3 / max(W, 1), 4),
-                      "note": "includes the first interval (plans for the initial tree, first round)"},
-        "round_us": [round(a.elapsed_time(b) * 1e3, 1) for a, b in round_ev],
-        "event_ms_per_step": round(ev_ms / K, 4),
+        "naive_bytes_per_step": round(reps[0]["ctx"] * T * Hkv * D * 2 * e),
+        "initial_tree": {"steps": f"0-{first - 1}", "avg_launch_us": round(init_ms * 1e3, 2),
+                         "alg_bytes_per_launch": round(init_bytes),
+                         "achieved_GBps": round(init_bytes / (init_ms / 1e3) / 1e9, 1),
+                         "frac": round(init_bytes / (init_ms / 1e3) / 1e9 / PEAK_HBM_GBPS, 4),
+                         "note": "the tree before the first round (replay 0); not the headline"},
+        "round_us": reps[0]["rounds"],
+        "event_ms_per_step": round(med(sorted(x["event_ms"] for x in reps)) / K, 4),
     }
-    log("measuring the read ceiling")
-    ceil = read_ceiling()
-    ceil["attn_frac_of_nontemporal"] = round(achieved / ceil["nontemporal_GBps"], 4)
-    res["read_ceiling"] = ceil
+    if not args.no_ceiling:
+        log("measuring the read ceiling")
+        ceil = read_ceiling()
+        ceil["attn_frac_of_nontemporal"] = round(achieved / ceil["nontemporal_GBps"], 4)
+        res["read_ceiling"] = ceil
     if not args.no_tournament:
         log("timing tournament rounds")
         res["tournament"] = tournament_rounds()
@@ -499,7 +616,6 @@ def main():
         res["seqscorer"] = scorer_measure()
     if not args.no_layers:
         log(f"timing {args.layers}-layer fp8 steps")
-        del run, pool
         torch.cuda.empty_cache()
         res["fp8_layers"] = layered_fp8(args.layers)
     if not args.no_cpu_baseline:

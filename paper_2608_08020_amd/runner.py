@@ -18,7 +18,9 @@ from .gambit import Pool
 BS = 16
 
 
-def _to_dev(a: np.ndarray, dtype: torch.dtype, device) -> torch.Tensor:
+def _to_dev(a, dtype: torch.dtype, device) -> torch.Tensor:
+    if isinstance(a, torch.Tensor):  # already resident (e.g. kept from an earlier replay)
+        return a
     t = torch.from_numpy(np.ascontiguousarray(a))
     if dtype == torch.bfloat16:
         t = t.view(torch.int16).view(torch.bfloat16)
@@ -104,6 +106,10 @@ class PopulationRun:
                               _to_dev(v, self.cache_dtype, self.device))
                 if keep_host:
                     self.host[s] = (q, k, v)
+
+    def share_inputs(self, other: "PopulationRun"):
+        """Use another run's resident step and round inputs (same workload)."""
+        self.q, self.kv, self.h = other.q, other.kv, other.h
 
     def load_rounds(self, rounds):
         for r in rounds:
