@@ -328,6 +328,21 @@ gambit_status gambit_mlp_score(int32_t n, const void* h, const gambit_mlp* mlp, 
                                const int32_t* trace_ids, int32_t keep, int32_t* keep_out, void* workspace,
                                size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops or harnesses that forbid allocation): the same
+ * scoring as gambit_mlp_score, with its scratch (the tiles' partial logits)
+ * in a buffer the library holds in device memory, one per device, for the
+ * life of the process, instead of a caller workspace.  It calls no
+ * allocator.  Sizes whose gambit_mlp_workspace_size(n, hidden) exceeds
+ * GAMBIT_MLP_STATIC_SCRATCH_BYTES (8 MiB: n = 4096 with hidden up to 16384)
+ * fail with GAMBIT_ERR_WORKSPACE.  Every call on one device shares that
+ * device's buffer: calls that overlap on one device (other streams, other
+ * threads) race and must be ordered by the caller.  Other arguments and
+ * results as gambit_mlp_score. */
+#define GAMBIT_MLP_STATIC_SCRATCH_BYTES ((size_t)8 << 20)
+gambit_status gambit_mlp_score_static(int32_t n, const void* h, const gambit_mlp* mlp, float* scores_out,
+                                      const int32_t* trace_ids, int32_t keep, int32_t* keep_out, void* stream);
+
 /* Tournament state of the listed slots (host outputs, any may be NULL);
  * synchronises `stream`.  sbar fp32, nscore/gen int32, ghost 0/1. */
 gambit_status gambit_trace_state(gambit_pool* pool, int32_t n, const int32_t* trace_ids, float* sbar_out,

@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libgambit.so")
-SOURCES = ["gambit_pool.cpp", "blocktable.hip", "decode_attn.hip", "probe_topk.hip",
+SOURCES = ["gambit_pool.cpp", "blocktable.hip", "decode_attn.hip", "probe_topk.hip", "mlp_scorer.hip",
            "seq_scorer.cpp", "seqscorer.hip", "membench.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-mcode-object-version=5",

@@ -1254,38 +1254,6 @@ gambit_status gambit_tournament(gambit_pool* p, int32_t capacity, int32_t swap_k
   return GAMBIT_OK;
 }
 
-size_t gambit_mlp_workspace_size(int32_t n, int32_t hidden) {
-  if (n <= 0 || hidden <= 0 || hidden % 64) return 0;  // the documented unit multiple
-  return 4 * (size_t)n * (hidden / gambit::kMlpTileH);
-}
-
-gambit_status gambit_mlp_score(int32_t n, const void* h, const gambit_mlp* mlp, float* scores_out,
-                               const int32_t* trace_ids, int32_t keep, int32_t* keep_out, void* workspace,
-                               size_t workspace_bytes, void* stream) {
-  if (!mlp || !h || !scores_out || n <= 0 || n > gambit::kMaxRank) return GAMBIT_ERR_INVALID;
-  if (mlp->dim <= 0 || mlp->dim % 128 || mlp->hidden <= 0 || mlp->hidden % 64 ||
-      (mlp->activation != GAMBIT_ACT_RELU && mlp->activation != GAMBIT_ACT_GELU) || !mlp->w1 || !mlp->b1 || !mlp->w2)
-    return GAMBIT_ERR_INVALID;
-  if (keep < 0 || keep > n || (keep > 0 && (!trace_ids || !keep_out))) return GAMBIT_ERR_INVALID;
-  if (!workspace || workspace_bytes < gambit_mlp_workspace_size(n, mlp->hidden)) return GAMBIT_ERR_WORKSPACE;
-  gambit::MlpLaunch L{};
-  L.n = n;
-  L.dim = mlp->dim;
-  L.hidden = mlp->hidden;
-  L.act = mlp->activation;
-  L.h = static_cast<const uint16_t*>(h);
-  L.w1 = static_cast<const uint16_t*>(mlp->w1);
-  L.b1 = mlp->b1;
-  L.w2 = mlp->w2;
-  L.b2 = mlp->b2;
-  L.parts = static_cast<float*>(workspace);
-  L.scores_out = scores_out;
-  L.ids = trace_ids;
-  L.keep = keep;
-  L.keep_out = keep_out;
-  return gambit::launch_mlp_score(L, S(stream)) == hipSuccess ? GAMBIT_OK : GAMBIT_ERR_DEVICE;
-}
-
 gambit_status gambit_record_scores(gambit_pool* p, int32_t n, const int32_t* ids, const float* f, void* stream) {
   if (!p) return GAMBIT_ERR_INVALID;
   gambit_status st = check_running(p, n, ids);

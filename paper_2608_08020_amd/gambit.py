@@ -89,7 +89,7 @@ EXPORTS = ["gambit_workspace_size", "gambit_pool_create", "gambit_pool_destroy",
            "gambit_mlp_workspace_size", "gambit_mlp_score", "gambit_scorer_workspace_size", "gambit_scorer_create",
            "gambit_scorer_destroy", "gambit_scorer_step", "gambit_scorer_fork", "gambit_scorer_free",
            "gambit_scorer_steps", "gambit_scorer_check", "gambit_scorer_last_error", "gambit_stream_read",
-           "gambit_plan_kinds"]
+           "gambit_plan_kinds", "gambit_mlp_score_static"]
 
 
 def lib() -> ctypes.CDLL:
@@ -138,6 +138,7 @@ def lib() -> ctypes.CDLL:
         "gambit_scorer_last_error": (ctypes.c_char_p, [vp]),
         "gambit_stream_read": (i32, [vp, ctypes.c_size_t, i32, i32, vp, vp]),
         "gambit_plan_kinds": (i32, [vp, i32, vp, vp]),
+        "gambit_mlp_score_static": (i32, [i32, vp, ctypes.POINTER(Mlp), vp, vp, i32, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -228,6 +229,46 @@ def mlp_score(h: torch.Tensor, w1: torch.Tensor, b1: torch.Tensor, w2: torch.Ten
     if st != OK:
         raise GambitError(st, "mlp_score")
     return scores, (keep_out[:keep] if keep > 0 else None)
+
+
+MLP_STATIC_SCRATCH_BYTES = 8 << 20
+
+
+def mlp_score_static(h: torch.Tensor, w1: torch.Tensor, b1: torch.Tensor, w2: torch.Tensor, b2: float,
+                     activation: str = "relu", ids: torch.Tensor | None = None, keep: int = 0,
+                     scores_out: torch.Tensor | None = None, keep_out: torch.Tensor | None = None, stream=None):
+    """gambit_mlp_score_static: as mlp_score, with the library's own device
+    scratch instead of a workspace (no device allocation inside the call when
+    the outputs are passed in)."""
+    if h.dim() != 2 or w1.dim() != 2:
+        raise ValueError("h: expected [n][dim], w1: expected [hidden][dim]")
+    n, dim = h.shape
+    hidden = w1.shape[0]
+    _spec(h, torch.bfloat16, (n, dim), "h")
+    _spec(w1, torch.bfloat16, (hidden, dim), "w1")
+    _spec(b1, torch.float32, (hidden,), "b1")
+    _spec(w2, torch.float32, (hidden,), "w2")
+    if activation not in ("relu", "gelu"):
+        raise ValueError(f"activation: {activation!r}")
+    if keep > 0 and ids is None:
+        raise ValueError("ids: needed when keep > 0")
+    if ids is not None:
+        _spec(ids, torch.int32, (n,), "ids")
+    if scores_out is None:
+        scores_out = torch.empty(n, dtype=torch.float32, device=h.device)
+    _spec(scores_out, torch.float32, (n,), "scores_out")
+    if keep > 0:
+        if keep_out is None:
+            keep_out = torch.empty(keep, dtype=torch.int32, device=h.device)
+        _spec(keep_out, torch.int32, (keep,), "keep_out")
+    m = Mlp(dim, hidden, ACT_RELU if activation == "relu" else ACT_GELU, _dev(w1).value, _dev(b1).value,
+            _dev(w2).value, float(b2))
+    st = lib().gambit_mlp_score_static(n, _dev(h), ctypes.byref(m), _dev(scores_out),
+                                       None if ids is None else _dev(ids), keep,
+                                       _dev(keep_out) if keep > 0 else None, _stream(stream))
+    if st != OK:
+        raise GambitError(st, "mlp_score_static")
+    return scores_out, (keep_out if keep > 0 else None)
 
 
 def stream_read(buf: torch.Tensor, nontemporal: bool, grid: int, sink: torch.Tensor, stream=None) -> None:
