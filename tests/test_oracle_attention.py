@@ -122,3 +122,31 @@ def test_head_mapping_is_consecutive_groups():
 def test_empty_context_rejected():
     with pytest.raises(ValueError):
         decode_attention(np.zeros((4, D)), np.zeros((0, 1, D)), np.zeros((0, 1, D)), 1.0)
+
+
+def _brute_force(q, K, V, scale):
+    """Scalar loops over Python floats and math.exp, straight from the
+    definition (no max subtraction, no library linear algebra)."""
+    Hq, L, Hkv, Dd = len(q), len(K), len(K[0]), len(q[0])
+    g = Hq // Hkv
+    out = []
+    for h in range(Hq):
+        w = []
+        for j in range(L):
+            dot = 0.0
+            for d in range(Dd):
+                dot += q[h][d] * K[j][h // g][d]
+            w.append(math.exp(scale * dot))
+        z = sum(w)
+        out.append([sum(w[j] * V[j][h // g][d] for j in range(L)) / z for d in range(Dd)])
+    return out
+
+
+@pytest.mark.parametrize("L,Hq,Hkv,Dd", [(1, 2, 1, 3), (2, 4, 2, 5), (5, 8, 2, 4), (7, 6, 3, 2), (9, 4, 4, 8)])
+def test_matches_scalar_brute_force_on_tiny_inputs(L, Hq, Hkv, Dd):
+    rng = np.random.default_rng(100 + L)
+    q, K, V = _rand(rng, Hq, Dd), _rand(rng, L, Hkv, Dd), _rand(rng, L, Hkv, Dd)
+    scale = 0.7
+    ref = np.array(_brute_force(q.tolist(), K.tolist(), V.tolist(), scale))
+    o = decode_attention(q, K, V, scale)
+    assert np.abs(o - ref).max() < 1e-12
