@@ -363,8 +363,9 @@ gambit_status gambit_plan_stats(gambit_pool* pool, int32_t n, const int32_t* tra
  * plan is made by the first decode step after the list or the pool's block
  * sharing changed, so call this after such a step).  kinds_out host [n]:
  * an OR of GAMBIT_UNIT_* bits, one per kind of work unit whose rows include
- * the trace (narrow one-wave units; cooperative workgroup items with one or
- * two row blocks per wave, or - fp8 items of at most 32 rows - tile pairs);
+ * the trace (narrow one-wave units of one row block, or - fp8, 17 to 32
+ * rows - two; cooperative workgroup items with one or two row blocks per
+ * wave);
  * GAMBIT_UNIT_TAIL_SLOT when one of them sits in the workgroup slots that
  * the launch claims at run time.  For test coverage of the kernel's paths.
  * GAMBIT_ERR_INVALID when the current plan is not for this list. */
@@ -372,8 +373,8 @@ enum {
   GAMBIT_UNIT_NARROW = 1,
   GAMBIT_UNIT_COOP_ONE = 2,
   GAMBIT_UNIT_COOP_TWO = 4,
-  GAMBIT_UNIT_COOP_PAIRS = 8,
-  GAMBIT_UNIT_TAIL_SLOT = 16
+  GAMBIT_UNIT_TAIL_SLOT = 16,
+  GAMBIT_UNIT_NARROW_TWO = 32
 };
 gambit_status gambit_plan_kinds(gambit_pool* pool, int32_t n, const int32_t* trace_ids, int32_t* kinds_out);
 

@@ -11,19 +11,17 @@
 // by log-sum-exp.
 //
 // Two kinds of workgroup share one launch, interleaved on every XCD:
-//  * narrow: four independent one-row-block units, one per wave.  A wave
-//    streams its chunk 32 tokens at a time straight from HBM into matrix-core
-//    operand registers, double-buffered, with no LDS and no barrier (this is
-//    where most of the bytes are: chunks that 1-4 traces share).
+//  * narrow: four independent units, one per wave, of one row block (fp8:
+//    up to two).  A wave streams its chunk 32 tokens at a time straight from
+//    HBM into matrix-core operand registers, double-buffered, with no LDS
+//    and no barrier (this is where most of the bytes are: chunks that 1-4
+//    traces share).
 //  * cooperative: one chunk with 2-8 row blocks (more rows become several
 //    workgroups, placed on one XCD so their re-reads hit its L2).  The
 //    workgroup streams 32-token tiles into a 4-stage LDS ring by direct
 //    global-to-LDS loads, three tiles ahead, and each wave applies a tile to
 //    its one or two row blocks, so a chunk is read once per up to eight row
-//    blocks instead of once per row block.  fp8 items of at most two row
-//    blocks run in tile pairs: waves w and w + 2 take the even and the odd
-//    tiles of row block w & 1, and their running states are combined at the
-//    end, so no wave idles.
+//    blocks instead of once per row block.
 //
 // The launch also performs the decode step's append: the unit that covers
 // a trace's last block writes the new token's K and V there (quantising
@@ -145,6 +143,14 @@ __device__ inline uint4 ld_stream16(const uint8_t* p) {
 __device__ inline uint2 ld_stream8(const uint8_t* p) {
   const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
   return make_uint2(v.x, v.y);
+}
+
+// A zero the compiler cannot see through (keeps loads that use it where
+// they are written).
+__device__ inline int opaque_zero() {
+  int z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+  return z;
 }
 
 struct RowState {
@@ -412,34 +418,50 @@ __device__ inline void load_v(const uint8_t* vc0, const uint8_t* vc1, const Lane
   }
 }
 
-template <bool FP8>
-__device__ inline void qk_direct(const Tile<FP8>& t, const bf16x8 (&qf)[4], f32x4& s0, f32x4& s1) {
-  bf16x8 kf[2][4];
+// Scores of one tile for RB row blocks: every K operand feeds all of them.
+// fp8 operands are widened two at a time right before their products (the
+// products accumulate in the same order as qk_mfma's), which keeps few
+// widened operands live.
+template <bool FP8, int RB>
+__device__ inline void qk_direct(const Tile<FP8>& t, const bf16x8 (&qf)[RB][4], f32x4 (&s0)[RB], f32x4 (&s1)[RB]) {
+  if constexpr (!FP8) {
+    bf16x8 kf[2][4];
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    if constexpr (!FP8) {
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) kf[h][kb] = __builtin_bit_cast(bf16x8, t.k[h][kb]);
-    } else {
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        kf[h][2 * j] = __builtin_bit_cast(bf16x8, fp8x8_to_bf16(t.k[h][j].x, t.k[h][j].y));
-        kf[h][2 * j + 1] = __builtin_bit_cast(bf16x8, fp8x8_to_bf16(t.k[h][j].z, t.k[h][j].w));
+    for (int r = 0; r < RB; ++r) qk_mfma(kf, qf[r], s0[r], s1[r]);
+  } else {
+#pragma unroll
+    for (int r = 0; r < RB; ++r) s0[r] = s1[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const bf16x8 a = __builtin_bit_cast(bf16x8, fp8x8_to_bf16(t.k[h][j].x, t.k[h][j].y));
+        const bf16x8 b = __builtin_bit_cast(bf16x8, fp8x8_to_bf16(t.k[h][j].z, t.k[h][j].w));
+#pragma unroll
+        for (int r = 0; r < RB; ++r) {
+          f32x4& acc = h ? s1[r] : s0[r];
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[r][2 * j], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b, qf[r][2 * j + 1], acc, 0, 0, 0);
+        }
       }
     }
   }
-  qk_mfma(kf, qf, s0, s1);
 }
 
-template <bool FP8>
-__device__ inline void pv_direct(Tile<FP8>& t, f32x4 s0, f32x4 s1, int t0, int ntok, const LaneGeom& g,
-                                 const TileMeta& m, float sl, RowState& st) {
+template <bool FP8, int RB>
+__device__ inline void pv_direct(Tile<FP8>& t, const f32x4 (&s0)[RB], const f32x4 (&s1)[RB], int t0, int ntok,
+                                 const LaneGeom& g, const TileMeta& m, float sl, RowState (&st)[RB]) {
   const bool partial = t0 + 32 > ntok;
   const int nv = min(max(ntok - t0 - 8 * g.q, 0), 8);
   float c, vsc;
   lane_scales(g, m, sl, c, vsc);
-  bf16x8 ph, pl;
-  softmax_p<FP8>(s0, s1, partial, nv, c, vsc, st, ph, pl);
+  bf16x8 ph[RB], pl[RB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) softmax_p<FP8>(s0[r], s1[r], partial, nv, c, vsc, st[r], ph[r], pl[r]);
   // A token past the end reads as zero (its P is zero, but the slot may
   // hold stale bits).  Masked in place, so the common path copies nothing.
   if (partial) {
@@ -451,22 +473,22 @@ __device__ inline void pv_direct(Tile<FP8>& t, f32x4 s0, f32x4 s1, int t0, int n
         t.v[r] = make_uint2(keep_bytes(t.v[r].x, nv), keep_bytes(t.v[r].y, nv - 4));
     }
   }
-  bf16x8 vf[8];
+  // each V operand (widened from fp8 right before use) feeds every row block
 #pragma unroll
-  for (int r = 0; r < 8; ++r) {
+  for (int d = 0; d < 8; ++d) {
+    bf16x8 vf;
     if constexpr (!FP8)
-      vf[r] = __builtin_bit_cast(bf16x8, t.v[r]);
+      vf = __builtin_bit_cast(bf16x8, t.v[d]);
     else
-      vf[r] = __builtin_bit_cast(bf16x8, fp8x8_to_bf16(t.v[r].x, t.v[r].y));
+      vf = __builtin_bit_cast(bf16x8, fp8x8_to_bf16(t.v[d].x, t.v[d].y));
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+      st[r].acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph[r], st[r].acc[d], 0, 0, 0);
+      st[r].acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl[r], st[r].acc[d], 0, 0, 0);
+    }
   }
-  pv_mfma(vf, ph, pl, st);
 }
 
-// One wave, one 16-row unit.  Tile j lives in register buffer j % 2.  Step
-// i issues the QK product of tile i + 1 before the softmax and P.V of tile
-// i, so the matrix cores and the vector ALUs overlap; a buffer's K half is
-// refilled with tile j + 2 right after QK(j) and its V half right after
-// P.V(j), so two tiles are always in flight.
 // The decode step's append, for one KV head: the unit whose end is read at
 // run time covers its trace's last block, so it writes the new token there;
 // the unit waits for the stores before its first tile load.  Only this wave
@@ -573,22 +595,54 @@ __device__ inline int append_token(const DevPool& P, const AttnLaunch& A, const 
   return fresh;
 }
 
-template <bool FP8>
-__device__ void narrow_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int lane) {
+// One wave, one unit of up to 16 RB rows (RB row blocks; each K and V
+// operand loaded from HBM feeds all of them).  Tile j lives in register
+// buffer j % 2.  Step i issues the QK product of tile i + 1 before the
+// softmax and P.V of tile i, so the matrix cores and the vector ALUs
+// overlap; a buffer's K half is refilled with tile j + 2 right after QK(j)
+// and its V half right after P.V(j), so two tiles are always in flight.
+template <bool FP8, int RB>
+__device__ void narrow_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int lane, uint8_t* qlds) {
   const int32_t* brow = P.table + (size_t)U.owner * P.max_blocks + U.jb0;
   const int len = U.nblk >= 0 ? 0 : P.seq_len[U.owner] + A.len_bias;
   const int ntok = U.nblk >= 0 ? U.nblk * kBlock : len - U.jb0 * kBlock;
   if (ntok <= 0) return;
   const int fresh = U.nblk < 0 ? append_token<FP8>(P, A, U, lane, len) : -1;
-  const int R = U.mem_cnt * P.g;  // <= 16
+  const int R = U.mem_cnt * P.g;  // <= 16 RB
   const LaneGeom g = lane_geom(lane);
   const int nblk = (ntok + kBlock - 1) / kBlock;
   const int ntile = (ntok + 31) / 32;
   BlockIds<FP8> ids(P, brow, nblk, lane, fresh >= 0 ? nblk - 1 : -1, fresh, A.new_scale);
-  bf16x8 qf[4];
-  load_q(P, A, U, 0, R, FP8, g.q, g.lr, qf);
-  RowState st;
-  row_init(st);
+  // One row block keeps its Q operands in registers; two keep them in this
+  // wave's LDS region (a narrow workgroup uses no other LDS) and read them
+  // back for every tile, which leaves the registers to the two running
+  // states and the tiles in flight.
+  bf16x8 qf[1][4];
+  RowState st[RB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) {
+    load_q(P, A, U, 16 * r, R, FP8, g.q, g.lr, qf[0]);
+    if constexpr (RB > 1) {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+        *reinterpret_cast<bf16x8*>(qlds + (4 * r + kb) * 1024 + lane * 16) = qf[0][kb];
+    }
+    row_init(st[r]);
+  }
+  auto scores = [&](const Tile<FP8>& t, f32x4 (&s0)[RB], f32x4 (&s1)[RB]) {
+    if constexpr (RB == 1) {
+      qk_direct<FP8, 1>(t, qf, s0, s1);
+    } else {
+      // the offset is an opaque zero, so the reads stay in the loop
+      const uint8_t* qb = qlds + lane * 16 + opaque_zero();
+      bf16x8 qq[RB][4];
+#pragma unroll
+      for (int r = 0; r < RB; ++r)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) qq[r][kb] = *reinterpret_cast<const bf16x8*>(qb + (4 * r + kb) * 1024);
+      qk_direct<FP8, RB>(t, qq, s0, s1);
+    }
+  };
   const float sl = A.scale_log2;
 
   auto fetch_k = [&](const TileMeta& m, Tile<FP8>& t) {
@@ -610,22 +664,27 @@ __device__ void narrow_unit(const DevPool& P, const AttnLaunch& A, const AttnUni
     fetch_k(mb, tb);
     fetch_v(mb, tb);
   }
-  f32x4 s0, s1;
-  qk_direct<FP8>(ta, qf, s0, s1);
+  f32x4 s0[RB], s1[RB];
+  scores(ta, s0, s1);
   if (ntile > 2) {
     meta(2, na);
     fetch_k(na, ta);
   }
   auto step = [&](int i, Tile<FP8>& t, TileMeta& m, TileMeta& n, Tile<FP8>& to, TileMeta& no) {
-    const f32x4 r0 = s0, r1 = s1;
+    f32x4 r0[RB], r1[RB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+      r0[r] = s0[r];
+      r1[r] = s1[r];
+    }
     if (i + 1 < ntile) {
-      qk_direct<FP8>(to, qf, s0, s1);
+      scores(to, s0, s1);
       if (i + 3 < ntile) {
         meta(i + 3, no);
         fetch_k(no, to);
       }
     }
-    pv_direct<FP8>(t, r0, r1, 32 * i, ntok, g, m, sl, st);
+    pv_direct<FP8, RB>(t, r0, r1, 32 * i, ntok, g, m, sl, st);
     if (i + 2 < ntile) {
       fetch_v(n, t);
       m = n;
@@ -635,7 +694,8 @@ __device__ void narrow_unit(const DevPool& P, const AttnLaunch& A, const AttnUni
     step(i, ta, ma, na, tb, nb);
     if (i + 1 < ntile) step(i + 1, tb, mb, nb, ta, na);
   }
-  write_partial(P, A, U, 0, R, g.q, g.lr, st);
+#pragma unroll
+  for (int r = 0; r < RB; ++r) write_partial(P, A, U, 16 * r, R, g.q, g.lr, st[r]);
 }
 
 // ----------------------------------------------------------- cooperative --
@@ -734,13 +794,10 @@ __device__ inline void barrier_no_fence() { asm volatile("s_barrier" ::: "memory
 // stages hold the raw tiles in the cache's layout, and every wave widens
 // the operands it reads (as the narrow path does from HBM), so an fp8 tile
 // moves half the bytes and the ring is deeper.
-template <bool FP8, int RB, bool PAIR = false>
+template <bool FP8, int RB>
 __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit& U, int wave, int lane,
                           uint8_t* lds) {
-  static_assert(!PAIR || (FP8 && RB == 1), "tile pairs: fp8 items of at most two row blocks");
-  // Tile pairs keep four tiles in use (two being applied, two being scored),
-  // so they run two fewer tiles ahead.
-  constexpr int ring = FP8 ? kRing8 : kRing, ahead = FP8 ? (PAIR ? kRing8 - 2 : kAhead8) : kAhead;
+  constexpr int ring = FP8 ? kRing8 : kRing, ahead = FP8 ? kAhead8 : kAhead;
   constexpr int stage = FP8 ? kStage8 : kStage;
   const int32_t* brow = P.table + (size_t)U.owner * P.max_blocks + U.jb0;
   // a cooperative item is a shared run: its end is in the plan
@@ -750,10 +807,7 @@ __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit&
   const LaneGeom g = lane_geom(lane);
   const int nblk = (ntok + kBlock - 1) / kBlock;
   const int ntile = (ntok + 31) / 32;
-  // tile pairs: waves w and w + 2 share row block w & 1 and take the even
-  // and the odd tiles
-  const int row0 = PAIR ? 16 * (wave & 1) : 16 * RB * wave;
-  const int par = PAIR ? wave >> 1 : 0;
+  const int row0 = 16 * RB * wave;
   const bool active = row0 < R;
   bf16x8 qf[RB][4];
   RowState st[RB];
@@ -891,65 +945,6 @@ __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit&
   __builtin_amdgcn_s_waitcnt(0x0F70);  // Q operands and the first id windows are in
   barrier_no_fence();
   for (int i = 0; i < ahead && i < ntile; ++i) issue(i);
-  if constexpr (PAIR) {
-    // Step k applies tiles 2k (waves 0-1) and 2k + 1 (waves 2-3) and scores
-    // each wave's next tile (2k + 2 or 2k + 3); tiles up to 2k + ahead + 1
-    // are then issued, into the stages of tiles 2k - 2 and 2k - 1, which
-    // every wave finished with in step k - 1.  Every wave takes part in
-    // every barrier, whatever its tiles.
-    wait(max(min(ahead, ntile) - 2, 0));  // tiles 0 and 1 are in LDS
-    barrier_no_fence();
-    f32x4 s0[1], s1[1];
-    if (active && par < ntile) qk(lds + par * stage, s0, s1);
-    for (int k = 0; 2 * k < ntile; ++k) {
-      const int i = 2 * k + par;
-      // tiles up to 2k + 3 in LDS: of the tiles issued so far, the ones past it may still be in flight
-      wait(max(min(ahead + 2 * k, ntile) - 1 - min(2 * k + 3, ntile - 1), 0));
-      barrier_no_fence();
-      if (2 * k + ahead < ntile) issue(2 * k + ahead);
-      if (2 * k + ahead + 1 < ntile) issue(2 * k + ahead + 1);
-      if (active && i < ntile) {
-        f32x4 n0[1], n1[1];
-        if (i + 2 < ntile) qk(lds + ((i + 2) % ring) * stage, n0, n1);
-        pv(lds + (i % ring) * stage, i, s0, s1);
-        s0[0] = n0[0];
-        s1[0] = n1[0];
-      }
-    }
-    // Waves 2-3 hand their running state to waves 0-1 through LDS (the ring
-    // is idle: every issued tile was waited for), which combine and write.
-    float* xch = reinterpret_cast<float*>(lds) + (wave & 1) * 34 * 64;
-    __builtin_amdgcn_s_waitcnt(0x0F70);
-    barrier_no_fence();
-    if (par == 1) {
-      xch[lane] = st[0].m;
-      xch[64 + lane] = st[0].l;
-#pragma unroll
-      for (int r = 0; r < 8; ++r)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) xch[128 + (4 * r + e) * 64 + lane] = st[0].acc[r][e];
-    }
-    __syncthreads();
-    if (par == 0 && active) {
-      const float mb = xch[lane], lb = xch[64 + lane];
-      RowState& a = st[0];
-      if (mb > a.m) {  // the other half moved further; also when this half saw no tile (m = -inf)
-        const float alpha = a.m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(a.m - mb);
-        a.l *= alpha;
-#pragma unroll
-        for (int r = 0; r < 8; ++r) a.acc[r] *= alpha;
-        a.m = mb;
-      }
-      const float beta = mb == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mb - a.m);
-      a.l += beta * lb;
-#pragma unroll
-      for (int r = 0; r < 8; ++r)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) a.acc[r][e] += beta * xch[128 + (4 * r + e) * 64 + lane];
-      write_partial(P, A, U, row0, R, g.q, g.lr, a);
-    }
-    return;
-  }
   wait(min(ahead, ntile) - 1);  // tile 0 is in LDS
   barrier_no_fence();
   f32x4 s0[RB], s1[RB];
@@ -1000,6 +995,7 @@ __device__ inline int tail_start(const AttnLaunch& A, int x) {
 template <bool FP8>
 __global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(DevPool P, AttnLaunch A) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[(FP8 ? kRing8 * kStage8 : kRing * kStage) + kIdsBytes];
+  static_assert(!FP8 || 4 * 8192 <= kRing8 * kStage8, "narrow waves' Q regions (two row blocks)");
   __shared__ int claimed;
   if (threadIdx.x == 0) {
     const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
@@ -1028,14 +1024,21 @@ __global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(DevPool P, Attn
     // up to 64 rows: one row block per wave; more: two
     if (U0.mem_cnt * P.g > 4 * kRowsPerUnit)
       coop_unit<FP8, 2>(P, A, U0, wave, lane, lds);
-    else if (FP8 && U0.mem_cnt * P.g <= 2 * kRowsPerUnit && U0.mem_cnt > 0)
-      coop_unit<FP8, 1, FP8>(P, A, U0, wave, lane, lds);  // fp8, at most 32 rows: tile pairs
     else if (U0.mem_cnt > 0)
       coop_unit<FP8, 1>(P, A, U0, wave, lane, lds);
     return;
   }
   const AttnUnit U = A.units[base + wave];  // a narrow slot always has four entries
-  if (U.mem_cnt > 0) narrow_unit<FP8>(P, A, U, lane);  // no barrier on the narrow path
+  // no barrier on the narrow path; fp8 units of 17-32 rows take two row
+  // blocks in one wave
+  if constexpr (FP8) {
+    if (U.mem_cnt * P.g > kRowsPerUnit)
+      narrow_unit<FP8, 2>(P, A, U, lane, lds + wave * 8192);
+    else if (U.mem_cnt > 0)
+      narrow_unit<FP8, 1>(P, A, U, lane, nullptr);
+  } else if (U.mem_cnt > 0) {
+    narrow_unit<FP8, 1>(P, A, U, lane, nullptr);
+  }
 }
 
 // Log-sum-exp merge of a row's partials.  One wave per (list position,

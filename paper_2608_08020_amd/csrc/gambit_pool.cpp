@@ -37,6 +37,17 @@ constexpr int kDefaultChunkBlocks = 64;  // blocks per attention chunk before ba
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int cdiv(int a, int b) { return (a + b - 1) / b; }
 
+// Per-token times of one attention unit on MI355X (microseconds), by kind and
+// cache dtype, from per-wave timelines of the 256- and 512-trace workloads:
+// narrow units per wave, cooperative items per workgroup.
+constexpr double kUsNarrow16 = 0.10;     // bf16, <= 16 rows
+constexpr double kUsNarrow8 = 0.045;     // fp8, <= 16 rows
+constexpr double kUsNarrowTwo8 = 0.055;  // fp8, 17-32 rows (two row blocks)
+constexpr double kUsCoop32_16 = 0.033, kUsCoop64_16 = 0.044, kUsCoop128_16 = 0.053;
+constexpr double kUsCoopPair8 = 0.031, kUsCoop64_8 = 0.037, kUsCoop128_8 = 0.051;
+// Chunk caps as fractions of the estimated launch length.
+constexpr double kCapNarrow = 1.0, kCapCoop = 0.5;
+
 // Workspace carve-up.  All offsets are kAlign-aligned.
 struct Layout {
   size_t list, ids, req_trace, req_ntok, pairs, free_list, nk, ticket, queues, err, scales, freebits,
@@ -330,6 +341,9 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
   const int Hkv = p->d.num_kv_heads;
   const int kmax = p->L.kmax;
   const int nb_total = p->d.num_blocks;
+  const bool fp8 = p->d.kv_dtype == GAMBIT_KV_FP8_E4M3;
+  // rows a narrow (one-wave) unit takes: 16, or two row blocks for fp8
+  const int narrow_rows = fp8 ? gambit::kRowsPerNarrowFp8 : gambit::kRowsPerUnit;
   if ((int)p->first.size() != nb_total) p->first.assign(nb_total, -1);
   std::vector<int> nb(n);
   for (int pos = 0; pos < n; ++pos) nb[pos] = cdiv(p->seq_len[ids[pos]], 16);
@@ -418,33 +432,42 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
 
   // Chunk caps from the launch's own length.  A chunk is one unit's work, and
   // a unit that runs longer than the launch would take with its work spread
-  // evenly sets the launch's length.  The estimate uses per-token times
-  // measured on MI355X with bf16 pools (fp8 tiles move half the bytes): a
-  // narrow unit streams ~0.16 us per token on one wave, four units to a
-  // workgroup slot; a cooperative item ~0.042 us per token on a whole slot;
-  // two slots per compute unit.  Narrow chunks are capped at the estimated
-  // launch length, cooperative ones (which start early) at half of it; on the
-  // 512-trace workload (~0.85 ms launches) neither cap binds.
-  double cap_n = 1e9, cap_c = 1e9;  // blocks
+  // evenly sets the launch's length.  The estimate uses per-token times of
+  // one unit by kind, read from per-wave timelines of MI355X launches: a
+  // narrow unit on one wave (four to a workgroup slot), a cooperative item on
+  // a whole slot, two slots per compute unit.  Narrow chunks are capped at a
+  // fraction kCapNarrow of the estimated launch length, cooperative ones
+  // (which start early) at kCapCoop.
+  auto unit_us = [&](int rows) {  // us per token of the unit that takes `rows` rows
+    if (rows <= narrow_rows) return fp8 ? (rows > gambit::kRowsPerUnit ? kUsNarrowTwo8 : kUsNarrow8) : kUsNarrow16;
+    if (rows <= 2 * gambit::kRowsPerUnit) return fp8 ? kUsCoopPair8 : kUsCoop32_16;
+    if (rows <= 4 * gambit::kRowsPerUnit) return fp8 ? kUsCoop64_8 : kUsCoop64_16;
+    return fp8 ? kUsCoop128_8 : kUsCoop128_16;
+  };
+  double launch_us = 0.0;
   {
-    const double e = p->d.kv_dtype == GAMBIT_KV_FP8_E4M3 ? 0.5 : 1.0;
-    const double a_n = 0.16 * e, a_c = 0.042 * e;
     double slot_us = 0.0;
     for (int pos = 0; pos < n; ++pos)
       for (int r = run_off[pos]; r < run_off[pos + 1]; ++r) {
         const Run& R = runs[r];
         const double tok = 16.0 * (R.j1 - R.j0);
+        const int rows = R.c * p->g;
         if (R.c == 1) {
-          slot_us += tok * a_n / 4;
+          slot_us += tok * unit_us(rows) / 4;
         } else if (mem[R.rid][0] == pos) {
-          const int rows = R.c * p->g;
-          slot_us += rows <= gambit::kRowsPerUnit ? tok * a_n / 4 : tok * a_c * cdiv(rows, gambit::kRowsPerCoop);
+          slot_us += rows <= narrow_rows
+                         ? tok * unit_us(rows) / 4
+                         : tok * unit_us(std::min(rows, gambit::kRowsPerCoop)) * cdiv(rows, gambit::kRowsPerCoop);
         }
       }
-    const double launch_us = slot_us * Hkv / (2.0 * p->n_cu);
-    cap_n = std::max(16.0, launch_us / a_n / 16.0);
-    cap_c = std::max(16.0, 0.5 * launch_us / a_c / 16.0);
+    launch_us = slot_us * Hkv / (2.0 * p->n_cu);
   }
+  // largest chunk (blocks) for a run of `rows` rows
+  auto chunk_cap = [&](int rows) {
+    const bool nar = rows <= narrow_rows;
+    const double f = nar ? kCapNarrow : kCapCoop;
+    return std::max(16.0, f * launch_us / unit_us(nar ? rows : std::min(rows, gambit::kRowsPerCoop)) / 16.0);
+  };
 
   std::vector<Group> groups;
   std::vector<AttnUnit> gunits;  // the groups' units, contiguous per group
@@ -456,14 +479,14 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
     gunits.clear();
     members.clear();
     int worst = 0;
-    // One group per (chunk, KV head): a chunk with <= 16 rows is one narrow
-    // unit; a wider chunk becomes cooperative items of up to 128 rows.
+    // One group per (chunk, KV head): a chunk with <= narrow_rows rows is one
+    // narrow unit; a wider chunk becomes cooperative items of up to 128 rows.
     auto emit = [&](int owner_pos, int jb0, int nblk, int ntok_est, const int32_t* mem_ids, int mcnt,
                     int kidx) {
       const int moff = (int)members.size();
       members.insert(members.end(), mem_ids, mem_ids + mcnt);
       const double tok = std::max(ntok_est, 1);
-      if (mcnt * p->g <= gambit::kRowsPerUnit) {
+      if (mcnt * p->g <= narrow_rows) {
         for (int h = 0; h < Hkv; ++h) {
           groups.push_back(Group{tok, (int32_t)gunits.size(), 1, false});
           gunits.push_back(AttnUnit{ids[owner_pos], jb0, nblk, h, moff, mcnt, kidx, 0});
@@ -491,7 +514,7 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
         // longer chunks, the chunk lengths no longer depend on them
         const double grow = chunk_blocks == kDefaultChunkBlocks ? 1.0 : 1e9;
         if (R.c == 1) {  // private run: through the trace's last block, chunks of 4 chunk_blocks
-          const int clen = (int)std::max(1.0, std::min(4.0 * chunk_blocks, cap_n * grow));
+          const int clen = (int)std::max(1.0, std::min(4.0 * chunk_blocks, chunk_cap(p->g) * grow));
           const int nch = std::max(1, cdiv(len, clen));
           for (int k = 0, jb = R.j0; k < nch; ++k) {
             const int sz = len / nch + (k < len % nch ? 1 : 0);
@@ -501,15 +524,16 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
           }
           break;
         }
-        // Chunk lengths (in units of chunk_blocks, 64 at first): 4 for runs of
-        // one row block (narrow units), the row-block count up to 8 for wider
-        // runs (cooperative items re-read their chunk per item, so longer
-        // chunks mean fewer partials for the same bytes per row block).
-        // Measured on the 512-trace workload; shorter chunks lose more to
-        // per-unit start-up and merging than they gain at the launch's tail.
+        // Chunk lengths (in units of chunk_blocks, 64 at first): 4 for runs
+        // of narrow units, the row-block count up to 8 for wider runs
+        // (cooperative items re-read their chunk per item, so longer chunks
+        // mean fewer partials for the same bytes per row block).  Measured on
+        // the 512-trace workload; shorter chunks lose more to per-unit
+        // start-up and merging than they gain at the launch's tail.
+        const bool nar = R.c * p->g <= narrow_rows;
         const int nrb = cdiv(R.c * p->g, gambit::kRowsPerUnit);
-        const int clen = (int)std::max(1.0, std::min((double)chunk_blocks * (nrb == 1 ? 4 : std::min(nrb, 8)),
-                                                     (nrb == 1 ? cap_n : cap_c) * grow));
+        const int clen = (int)std::max(1.0, std::min((double)chunk_blocks * (nar ? 4 : std::min(nrb, 8)),
+                                                     chunk_cap(R.c * p->g) * grow));
         const int nch = cdiv(len, clen);
         const auto& ml = mem[R.rid];
         for (int k = 0, jb = R.j0; k < nch; ++k) {
@@ -605,11 +629,12 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
       const AttnUnit& u0 = units[base];
       if (u0.flags & gambit::kUnitCoop) {
         const int rows = u0.mem_cnt * p->g;
-        mark(u0, rows > 4 * gambit::kRowsPerUnit ? GAMBIT_UNIT_COOP_TWO
-                 : (p->d.kv_dtype == GAMBIT_KV_FP8_E4M3 && rows <= 2 * gambit::kRowsPerUnit) ? GAMBIT_UNIT_COOP_PAIRS
-                                                                                             : GAMBIT_UNIT_COOP_ONE);
+        mark(u0, rows > 4 * gambit::kRowsPerUnit ? GAMBIT_UNIT_COOP_TWO : GAMBIT_UNIT_COOP_ONE);
       } else {
-        for (int w = 0; w < gambit::kUnitsPerWG; ++w) mark(units[base + w], GAMBIT_UNIT_NARROW);
+        for (int w = 0; w < gambit::kUnitsPerWG; ++w) {
+          const AttnUnit& u = units[base + w];
+          mark(u, u.mem_cnt * p->g > gambit::kRowsPerUnit ? GAMBIT_UNIT_NARROW_TWO : GAMBIT_UNIT_NARROW);
+        }
       }
     }
   }

@@ -39,6 +39,9 @@ struct AttnUnit {
 
 enum : int32_t { kUnitCoop = 1 };
 
+// Rows of an fp8 narrow unit: one wave takes two row blocks (the widened K
+// and V operands feed both); bf16 narrow units keep one.
+constexpr int kRowsPerNarrowFp8 = 32;
 constexpr int kRowsPerCoop = 128;  // rows of one cooperative item (4 waves x up to 2 row blocks)
 constexpr int kTailSlots = 96;     // last workgroup slots of an XCD, claimed at run time
 

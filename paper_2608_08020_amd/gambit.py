@@ -22,7 +22,7 @@ OK, ERR_INVALID, ERR_OUT_OF_BLOCKS, ERR_SHARED_WRITE, ERR_UNSUPPORTED, ERR_DEVIC
 KV_BF16, KV_FP8_E4M3 = 0, 1
 OUT_BF16, OUT_F32 = 0, 1
 NEW_CACHE, NEW_BF16 = 0, 1
-UNIT_NARROW, UNIT_COOP_ONE, UNIT_COOP_TWO, UNIT_COOP_PAIRS, UNIT_TAIL_SLOT = 1, 2, 4, 8, 16
+UNIT_NARROW, UNIT_COOP_ONE, UNIT_COOP_TWO, UNIT_TAIL_SLOT, UNIT_NARROW_TWO = 1, 2, 4, 16, 32
 CODE_NAMES = {ERR_INVALID: "INVALID", ERR_OUT_OF_BLOCKS: "OUT_OF_BLOCKS",
               ERR_SHARED_WRITE: "SHARED_WRITE", ERR_UNSUPPORTED: "UNSUPPORTED",
               ERR_DEVICE: "DEVICE", ERR_WORKSPACE: "WORKSPACE"}

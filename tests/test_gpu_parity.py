@@ -8,11 +8,11 @@ import pytest
 import torch
 
 from _parity import replay
-from paper_2608_08020_amd.gambit import UNIT_COOP_ONE, UNIT_COOP_PAIRS, UNIT_COOP_TWO, UNIT_NARROW, UNIT_TAIL_SLOT
+from paper_2608_08020_amd.gambit import UNIT_COOP_ONE, UNIT_COOP_TWO, UNIT_NARROW, UNIT_NARROW_TWO, UNIT_TAIL_SLOT
 from workload import CONFIGS, Workload, tiny
 
-KINDS = {UNIT_NARROW: "narrow", UNIT_COOP_ONE: "cooperative, one row block per wave",
-         UNIT_COOP_TWO: "cooperative, two row blocks per wave", UNIT_COOP_PAIRS: "cooperative tile pairs",
+KINDS = {UNIT_NARROW: "narrow", UNIT_NARROW_TWO: "narrow, two row blocks", UNIT_COOP_ONE: "cooperative, one row block per wave",
+         UNIT_COOP_TWO: "cooperative, two row blocks per wave",
          UNIT_TAIL_SLOT: "slot claimed at run time"}
 
 
@@ -121,10 +121,13 @@ def test_cfg4_512_traces_full_size_fp32_strict():
 
 
 @pytest.mark.timeout(900)
-def test_cfg5_fp8_covers_tile_pairs():
-    """The fp8 workload's cooperative items of at most 32 rows run in tile
-    pairs; traces chosen from the plan so that those items are checked too."""
+def test_cfg5_fp8_covers_every_unit_kind():
+    """The fp8 workload's chunks of 17-32 rows run as narrow units of two row
+    blocks; traces chosen from the plan so that those units, one-block narrow
+    units and cooperative items are all checked, before and after the first
+    round."""
     wl = Workload(CONFIGS[5], total_steps=140)
     cover = PlanCover(want=24)
     replay(wl, sample_steps=[0, 129, 139], sample_traces=cover)
-    assert {UNIT_NARROW, UNIT_COOP_PAIRS} <= cover.seen, [KINDS[k] for k in cover.seen]
+    want = {UNIT_NARROW, UNIT_NARROW_TWO, UNIT_COOP_ONE}
+    assert want <= cover.seen, f"kinds not covered: {[KINDS[k] for k in want - cover.seen]}"
