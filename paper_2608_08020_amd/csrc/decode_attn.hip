@@ -46,6 +46,7 @@
 #include <cmath>
 
 #include "kernels.h"
+#include "lds_dma.h"
 
 namespace gambit {
 namespace {
@@ -708,38 +709,8 @@ constexpr int kRing = 4;
 constexpr int kAhead = 3;
 constexpr int kDmaPerTile = 4;  // 16-byte loads per thread per tile
 
-// Direct global->LDS loads: 16 (or 4) bytes per lane into LDS at l + 16
-// (4) x lane, l wave-uniform.  Written as inline assembly so the compiler
-// does not track them: it would otherwise wait for every one in flight
-// before any LDS read.  Completion is waited for explicitly (wait_tiles);
-// waits the compiler derives for other loads stay correct (untracked loads
-// only make them wait longer).
-__device__ inline uint32_t lds_addr(const void* l) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)l;
-}
-
-// M0 carries the LDS address; it is saved and restored around the load, so
-// the compiler's view of M0 never changes.
-__device__ inline void dma16(const void* g, uint8_t* l) {
-  uint32_t save;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_nop 0\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(save)
-      : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds_addr(l)))
-      : "memory");
-}
-
-__device__ inline void dma4(const void* g, void* l) {
-  uint32_t save;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %1, off\n\ts_nop 0\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(save)
-      : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds_addr(l)))
-      : "memory");
-}
-
+// Direct global->LDS loads (dma16, dma4) come from lds_dma.h; completion is
+// waited for explicitly (wait_tiles).
 constexpr int kIdsBytes = 2 * 64 * 4;  // two windows of 64 block ids
 
 // fp8 stage: the raw tiles (K of both blocks, then V^T of both, 2 KiB each,
@@ -778,11 +749,6 @@ __device__ inline void wait_tiles_per(int later) {
     default: __builtin_amdgcn_s_waitcnt(0x0F70 | (5 * PER)); break;
   }
 }
-
-// Workgroup barrier that keeps the compiler from moving memory accesses
-// across it but adds no wait for outstanding loads (a fenced barrier would
-// wait for every in-flight direct load, emptying the ring).
-__device__ inline void barrier_no_fence() { asm volatile("s_barrier" ::: "memory"); }
 
 // One workgroup, one chunk, up to 4 x RB row blocks: wave w owns row
 // blocks RB w .. RB w + RB - 1, so each K/V operand a wave reads from LDS

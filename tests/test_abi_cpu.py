@@ -165,3 +165,23 @@ def test_binding_checks_every_device_argument():
     _raises(lambda: mlp_score(h, w1, b1, w2, 0.0, keep=2), "ids: needed")
     _raises(lambda: mlp_score(h, w1, b1, w2, 0.0, ids=z(n - 1, dt=i32), keep=2), "ids: expected shape")
     _raises(lambda: rank_topk(z(n, dt=i32), z(n - 1, dt=f32), 2), "scores: expected shape")
+
+
+def test_mlp_workspace_sizes_and_checks():
+    """Workspace sizes of the MLP scorer: 0 for sizes outside the contract,
+    every n <= 4096 with hidden <= 16384 within the static buffer, and a
+    short workspace refused before anything is launched."""
+    import ctypes
+
+    from paper_2608_08020_amd import gambit
+    L = gambit.lib()
+    ws = L.gambit_mlp_workspace_size
+    assert ws(0, 64) == 0 and ws(8, 96) == 0 and ws(8, 0) == 0
+    assert ws(512, 1024) >= 4 * 512 * (1024 // 32)  # the tiles' partial logits
+    assert all(0 < ws(n, hd) <= gambit.MLP_STATIC_SCRATCH_BYTES
+               for n in (1, 100, 128, 512, 1000, 4096) for hd in (64, 1024, 4096, 16384))
+    fake = ctypes.c_void_p(1 << 20)              # never dereferenced: the calls fail their checks
+    m = gambit.Mlp(256, 128, gambit.ACT_RELU, fake.value, fake.value, fake.value, 0.0)
+    need = ws(16, 128)
+    assert L.gambit_mlp_score(16, fake, ctypes.byref(m), fake, None, 0, None, fake, need - 1,
+                              None) == gambit.ERR_WORKSPACE
