@@ -38,13 +38,17 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 // Per-token times of one attention unit on MI355X (microseconds), by kind and
-// cache dtype, from per-wave timelines of the 256- and 512-trace workloads:
-// narrow units per wave, cooperative items per workgroup.
-constexpr double kUsNarrow16 = 0.10;     // bf16, <= 16 rows
+// cache dtype: narrow units per wave, cooperative items per workgroup.  fp8:
+// read from per-wave timelines of the 256-trace workload.  bf16: the figures
+// the chunk caps were tuned with on the 256- and 512-trace workloads (per-
+// wave timelines give 0.10 for narrow units and 0.033-0.053 for cooperative
+// items, but caps from them cut the 512-trace launch's cooperative chunks
+// shorter: 1.7% more HBM traffic, no gain).
+constexpr double kUsNarrow16 = 0.16;     // bf16, <= 16 rows
 constexpr double kUsNarrow8 = 0.045;     // fp8, <= 16 rows
 constexpr double kUsNarrowTwo8 = 0.055;  // fp8, 17-32 rows (two row blocks)
-constexpr double kUsCoop32_16 = 0.033, kUsCoop64_16 = 0.044, kUsCoop128_16 = 0.053;
-constexpr double kUsCoopPair8 = 0.031, kUsCoop64_8 = 0.037, kUsCoop128_8 = 0.051;
+constexpr double kUsCoop16 = 0.042;     // bf16, any row count
+constexpr double kUsCoop64_8 = 0.037, kUsCoop128_8 = 0.051;  // fp8, 33-64 and 65-128 rows
 // Chunk caps as fractions of the estimated launch length.
 constexpr double kCapNarrow = 1.0, kCapCoop = 0.5;
 
@@ -440,9 +444,8 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
   // (which start early) at kCapCoop.
   auto unit_us = [&](int rows) {  // us per token of the unit that takes `rows` rows
     if (rows <= narrow_rows) return fp8 ? (rows > gambit::kRowsPerUnit ? kUsNarrowTwo8 : kUsNarrow8) : kUsNarrow16;
-    if (rows <= 2 * gambit::kRowsPerUnit) return fp8 ? kUsCoopPair8 : kUsCoop32_16;
-    if (rows <= 4 * gambit::kRowsPerUnit) return fp8 ? kUsCoop64_8 : kUsCoop64_16;
-    return fp8 ? kUsCoop128_8 : kUsCoop128_16;
+    if (!fp8) return kUsCoop16;
+    return rows <= 4 * gambit::kRowsPerUnit ? kUsCoop64_8 : kUsCoop128_8;
   };
   double launch_us = 0.0;
   {
