@@ -715,9 +715,13 @@ constexpr int kIdsBytes = 2 * 64 * 4;  // two windows of 64 block ids
 
 // fp8 stage: the raw tiles (K of both blocks, then V^T of both, 2 KiB each,
 // in the cache's own layout) and the tile's block scales (K0, V0, K1, V1,
-// repeated over 256 bytes).  Half the bytes of a bf16 tile, so the ring is
-// deeper for the same bytes in flight.
-constexpr int kMeta8 = 4 * 2048;
+// repeated over 256 bytes).  The second block's K starts 128 bytes later, so
+// the two 128-byte halves of a K read (one per block) fall in different
+// banks.  Half the bytes of a bf16 tile, so the ring is deeper for the same
+// bytes in flight.
+constexpr int kK1_8 = 2048 + 128;       // second block's K
+constexpr int kV8 = kK1_8 + 2048;       // V^T of both blocks
+constexpr int kMeta8 = kV8 + 2 * 2048;  // block scales
 constexpr int kStage8 = kMeta8 + 256;
 constexpr int kRing8 = 7;
 constexpr int kAhead8 = 6;
@@ -784,9 +788,9 @@ __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit&
   }
   const float sl = A.scale_log2;
   // lane's operand offsets in a stage
-  const int koff = FP8 ? (g.kb1 ? 2048 : 0) + g.q * 256 + (lane & 7) * 16
+  const int koff = FP8 ? (g.kb1 ? kK1_8 : 0) + g.q * 256 + (lane & 7) * 16
                        : (g.kb1 ? kLdsK1 : 0) + g.q * 256 + (lane & 7) * 16;
-  const int voff = FP8 ? 2 * 2048 + (g.vb1 ? 2048 : 0) + g.lr * 16 + (g.q & 1) * 8 : lds_v(g.vb1 ? 1 : 0, g.lr, g.q & 1);
+  const int voff = FP8 ? kV8 + (g.vb1 ? 2048 : 0) + g.lr * 16 + (g.q & 1) * 8 : lds_v(g.vb1 ? 1 : 0, g.lr, g.q & 1);
 
   // Scores of one tile for every row block (K from the stage holding it).
   auto qk = [&](const uint8_t* stg, f32x4 (&s0)[RB], f32x4 (&s1)[RB]) {
@@ -888,12 +892,12 @@ __device__ void coop_unit(const DevPool& P, const AttnLaunch& A, const AttnUnit&
       dma16(P.v_cache + o1 + vofs, dst + kLdsV + kTileBytes);
     } else {
       // Waves 0-1 move block b0's K and V^T tiles, waves 2-3 block b1's
-      // (lane t to byte 16 t of each 4 KB half); wave 0 also moves the
-      // scales, lane l the l % 4-th of (K0, V0, K1, V1).
+      // (lane t to byte 16 (t % 128) of its block's K and V^T); wave 0 also
+      // moves the scales, lane l the l % 4-th of (K0, V0, K1, V1).
       if (wave == 0) dma4(P.kv_scale + 2 * ((lane & 2) ? b1 : b0) + (lane & 1), stg + kMeta8);
       const size_t o = head_off<true>(wave < 2 ? b0 : b1, P.Hkv, U.kvh) + (t & 127) * 16;
-      dma16(P.k_cache + o, stg + wave * 1024);
-      dma16(P.v_cache + o, stg + 2 * 2048 + wave * 1024);
+      dma16(P.k_cache + o, stg + wave * 1024 + (wave < 2 ? 0 : kK1_8 - 2048));
+      dma16(P.v_cache + o, stg + kV8 + wave * 1024);
     }
   };
   // Waits until this wave's loads of the tiles before the `later` last
