@@ -301,8 +301,11 @@ gambit_status gambit_record_scores(gambit_pool* pool, int32_t n, const int32_t* 
  * paper gives no dimensions, activation or weights, so they are parameters):
  *     f(h) = 1 / (1 + exp(-(w2 . act(W1 h + b1) + b2)))
  * with act = ReLU or GELU (x * Phi(x), erf form).  W1 h runs on the bf16
- * matrix cores with fp32 accumulation; bias, activation and w2 are applied in
- * the same tiles; the tiles' partial logits are summed in a fixed order.
+ * matrix cores with fp32 accumulation, in 128 x 128 tiles whose k range is
+ * split so that the chip has ~256 tiles of work (at most 16 MiB of fp32
+ * partial sums); the partial sums are added in a fixed order before bias,
+ * activation and w2, so a call's result depends only on its sizes and
+ * inputs.  The ranking counts, for every score, the scores ahead of it.
  */
 enum { GAMBIT_ACT_RELU = 0, GAMBIT_ACT_GELU = 1 };
 typedef struct {
@@ -330,16 +333,16 @@ gambit_status gambit_mlp_score(int32_t n, const void* h, const gambit_mlp* mlp, 
 
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, serving loops or harnesses that forbid allocation): the same
- * scoring as gambit_mlp_score, with its scratch (the tiles' partial logits)
+ * scoring as gambit_mlp_score, with its scratch (the tiles' partial sums)
  * in a buffer the library holds in device memory, one per device, for the
  * life of the process, instead of a caller workspace.  It calls no
  * allocator.  Sizes whose gambit_mlp_workspace_size(n, hidden) exceeds
- * GAMBIT_MLP_STATIC_SCRATCH_BYTES (8 MiB: n = 4096 with hidden up to 16384)
+ * GAMBIT_MLP_STATIC_SCRATCH_BYTES (16 MiB: any n <= 4096 with hidden up to 131072)
  * fail with GAMBIT_ERR_WORKSPACE.  Every call on one device shares that
  * device's buffer: calls that overlap on one device (other streams, other
  * threads) race and must be ordered by the caller.  Other arguments and
  * results as gambit_mlp_score. */
-#define GAMBIT_MLP_STATIC_SCRATCH_BYTES ((size_t)8 << 20)
+#define GAMBIT_MLP_STATIC_SCRATCH_BYTES ((size_t)16 << 20)
 gambit_status gambit_mlp_score_static(int32_t n, const void* h, const gambit_mlp* mlp, float* scores_out,
                                       const int32_t* trace_ids, int32_t keep, int32_t* keep_out, void* stream);
 

@@ -189,26 +189,39 @@ hipError_t launch_tournament(const DevPool& P, int32_t capacity, int32_t swap_k,
 
 constexpr int kMaxRank = 4096;  // largest population the in-LDS ranking handles
 
-// The 2-layer MLP scorer f = sigmoid(w2 . act(W1 h + b1) + b2), fused:
-// tiles of 16 hidden states x 64 hidden units on the bf16 matrix cores with
-// bias, activation and the w2 product applied in the tile, then one
-// workgroup sums the tiles' partial logits in a fixed order, applies the
-// sigmoid and (keep > 0) ranks the top `keep` ids.
-constexpr int kMlpTileT = 32, kMlpTileH = 32;
+// The 2-layer MLP scorer f = sigmoid(w2 . act(W1 h + b1) + b2): W1 h in
+// 128 x 128 tiles on the bf16 matrix cores with the k range split `splits`
+// ways; with splits > 1 the tiles write fp32 pre-activation partial sums
+// [splits][n][hidden] that a second launch adds in split order before bias,
+// activation and w2; with splits = 1 the tiles apply them and write partial
+// logits [tiles_u][n].  A third launch ranks when keep > 0.
 struct MlpLaunch {
   int32_t n, dim, hidden, act;   // act: 0 ReLU, 1 GELU (erf)
+  int32_t tiles_t, tiles_u;      // ceil(n / 128), ceil(hidden / 128)
+  int32_t splits;                // k splits, <= dim / 128
   const uint16_t* h;             // [n][dim] bf16
   const uint16_t* w1;            // [hidden][dim] bf16
   const float* b1;               // [hidden]
   const float* w2;               // [hidden]
   float b2;
-  float* parts;                  // [hidden / kMlpTileH][n] partial logits
+  float* parts;                  // scratch, mlp_workspace_bytes(n, hidden)
   float* scores_out;             // [n]
-  const int32_t* ids;            // [n] or NULL (ranking only)
-  int32_t keep;
-  int32_t* keep_out;             // [keep]
 };
-hipError_t launch_mlp_score(const MlpLaunch& L, hipStream_t s);
+// k splits for n hidden states and `hidden` units: enough 128 x 128 tiles
+// for ~256 workgroups, at most 32 and at most kMlpSplitBytes of partial sums
+// (capped again by dim / 128 at launch).
+constexpr size_t kMlpSplitBytes = (size_t)16 << 20;
+inline int mlp_splits(int32_t n, int32_t hidden) {
+  const long tiles = (long)((n + 127) / 128) * ((hidden + 127) / 128);
+  long s = 256 / tiles;
+  s = s < 1 ? 1 : (s > 32 ? 32 : s);
+  while (s > 1 && (size_t)s * n * hidden * 4 > kMlpSplitBytes) --s;
+  return (int)s;
+}
+inline size_t mlp_workspace_bytes(int32_t n, int32_t hidden) {
+  const int s = mlp_splits(n, hidden);
+  return s > 1 ? (size_t)s * n * hidden * 4 : (size_t)((hidden + 127) / 128) * n * 4;
+}
 // Running means from thought scores computed elsewhere (f device [n]).
 hipError_t launch_record_scores(const DevPool& P, const int32_t* list, const float* f, int32_t n,
                                 hipStream_t s);

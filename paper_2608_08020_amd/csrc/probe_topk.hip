@@ -428,132 +428,6 @@ __global__ __launch_bounds__(kTournThreads) void tournament_kernel(DevPool P, in
   }
 }
 
-// ------------------------------------------------------------- MLP scorer --
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-__device__ inline float mlp_act(float x, int act) {
-  return act == 0 ? fmaxf(x, 0.f) : 0.5f * x * (1.f + erff(x * 0.70710678118654752f));
-}
-
-// One workgroup: hidden states t0 .. t0 + 31 x hidden units h0 .. h0 + 31,
-// D[trace][unit] = sum_k h[trace][k] W1[unit][k] on v_mfma_f32_16x16x32_bf16.
-// Both operand tiles (32 rows x 256 k, bf16) are staged in LDS, double
-// buffered: the next k-slab's global loads are issued before the current
-// one is multiplied (small tiles, so that many workgroups keep loads in
-// flight).  Wave w computes the 16 x 16 block of traces 16 (w >> 1) and
-// units 16 (w & 1); per 32-wide k step a lane reads A[i][8q .. 8q + 7] and
-// W1[j][8q .. 8q + 7] (i, j = lane % 16, q = lane / 16), one 16-byte LDS
-// read each, and lane (q, j) holds traces 4q .. 4q + 3 of unit j.
-// Epilogue: bias, activation, times w2, summed over the tile's 32 units
-// (lanes, then the two waves that share traces) into parts[unit tile][trace].
-constexpr int kMlpBK = 256;
-constexpr int kMlpChunks = kMlpBK / 64;  // 16-byte column chunks per loader thread and row
-constexpr int kMlpRow = kMlpBK + 8;  // LDS row in bf16, padded 16 B against bank conflicts
-
-__global__ __launch_bounds__(256) void mlp_tile_kernel(MlpLaunch L) {
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][kMlpTileT * kMlpRow];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kMlpTileH * kMlpRow];
-  __shared__ float red[2][kMlpTileT];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int q = lane >> 4, j = lane & 15;
-  const int t0 = blockIdx.x * kMlpTileT, h0 = blockIdx.y * kMlpTileH;
-  const int wm = 16 * (wave >> 1), wn = 16 * (wave & 1);
-  // loader: threads 0-127 stage the traces, 128-255 the units; rows lr and
-  // lr + 16, 8 bf16 at columns 8 lc + 64 c
-  const bool loads_a = tid < 128;
-  const int lr = (tid & 127) >> 3, lc = tid & 7;
-  // rows past n read row n - 1 (in bounds) and are zeroed by value
-  const bool ok0 = !loads_a || t0 + lr < L.n, ok1 = !loads_a || t0 + lr + 16 < L.n;
-  const uint16_t* src0 = loads_a ? L.h + (size_t)min(t0 + lr, L.n - 1) * L.dim + 8 * lc
-                                 : L.w1 + (size_t)(h0 + lr) * L.dim + 8 * lc;
-  const uint16_t* src1 = loads_a ? L.h + (size_t)min(t0 + lr + 16, L.n - 1) * L.dim + 8 * lc
-                                 : L.w1 + (size_t)(h0 + lr + 16) * L.dim + 8 * lc;
-  uint16_t* dst = loads_a ? &As[0][lr * kMlpRow + 8 * lc] : &Bs[0][lr * kMlpRow + 8 * lc];
-  const int buf_stride = loads_a ? kMlpTileT * kMlpRow : kMlpTileH * kMlpRow;
-  const uint32_t m0 = ok0 ? ~0u : 0u, m1 = ok1 ? ~0u : 0u;  // zero rows past n by masking
-  auto masked = [](uint4 v, uint32_t m) { return make_uint4(v.x & m, v.y & m, v.z & m, v.w & m); };
-  uint4 r0[kMlpChunks], r1[kMlpChunks];
-#pragma unroll
-  for (int c = 0; c < kMlpChunks; ++c) {
-    r0[c] = *reinterpret_cast<const uint4*>(src0 + 64 * c);
-    r1[c] = *reinterpret_cast<const uint4*>(src1 + 64 * c);
-  }
-#pragma unroll
-  for (int c = 0; c < kMlpChunks; ++c) {
-    *reinterpret_cast<uint4*>(dst + 64 * c) = masked(r0[c], m0);
-    *reinterpret_cast<uint4*>(dst + 16 * kMlpRow + 64 * c) = masked(r1[c], m1);
-  }
-  __syncthreads();
-  f32x4 acc = {};
-  const int nk = L.dim / kMlpBK, rem = L.dim % kMlpBK;  // dim is a multiple of 128
-  for (int s = 0; s < nk + (rem ? 1 : 0); ++s) {
-    const int buf = s & 1;
-    const int kb_next = (s + 1) * kMlpBK;
-    const bool more = kb_next < L.dim;
-    if (more) {
-#pragma unroll
-      for (int c = 0; c < kMlpChunks; ++c) {
-        // the last slab may be 128 wide: its missing chunks re-read an in-row
-        // column and are never multiplied
-        const int col = min(kb_next + 64 * c, L.dim - 64);
-        r0[c] = *reinterpret_cast<const uint4*>(src0 + col);
-        r1[c] = *reinterpret_cast<const uint4*>(src1 + col);
-      }
-    }
-    const int width = min(kMlpBK, L.dim - s * kMlpBK);
-    for (int kk = 0; kk < width; kk += 32) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(&As[buf][(wm + j) * kMlpRow + kk + 8 * q]);
-      const bf16x8 b = *reinterpret_cast<const bf16x8*>(&Bs[buf][(wn + j) * kMlpRow + kk + 8 * q]);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
-    }
-    if (more) {  // the other buffer was last read before the previous barrier
-      uint16_t* d = dst + (buf ^ 1) * buf_stride;
-#pragma unroll
-      for (int c = 0; c < kMlpChunks; ++c) {
-        *reinterpret_cast<uint4*>(d + 64 * c) = masked(r0[c], m0);
-        *reinterpret_cast<uint4*>(d + 16 * kMlpRow + 64 * c) = masked(r1[c], m1);
-      }
-    }
-    __syncthreads();
-  }
-  // epilogue: lane (q, j): traces wm + 4q + e, unit wn + j
-  const int u = h0 + wn + j;
-  const float w2 = L.w2[u], b1 = L.b1[u];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    float v = w2 * mlp_act(acc[e] + b1, L.act);
-#pragma unroll
-    for (int off = 8; off > 0; off >>= 1) v += __shfl_xor(v, off);  // over the 16 units of the lane group
-    if (j == 0) red[wave & 1][wm + 4 * q + e] = v;
-  }
-  __syncthreads();
-  if (tid < kMlpTileT && t0 + tid < L.n)  // the two unit halves, in a fixed order
-    L.parts[(size_t)blockIdx.y * L.n + t0 + tid] = red[0][tid] + red[1][tid];
-}
-
-// One workgroup: logit = b2 + the tiles' partials in tile order; sigmoid;
-// optionally the top `keep` ids by (score descending, id ascending).
-__global__ __launch_bounds__(kProbeThreads) void mlp_finish_kernel(MlpLaunch L) {
-  const int nt = L.hidden / kMlpTileH;
-  for (int t = threadIdx.x; t < L.n; t += kProbeThreads) {
-    float z = L.b2;
-    int i = 0;
-    for (; i + 8 <= nt; i += 8) {  // eight loads in flight, added in tile order
-      float p[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) p[e] = L.parts[(size_t)(i + e) * L.n + t];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) z += p[e];
-    }
-    for (; i < nt; ++i) z += L.parts[(size_t)i * L.n + t];
-    L.scores_out[t] = 1.f / (1.f + expf(-z));
-  }
-  if (L.keep <= 0) return;
-  __syncthreads();  // the scores written above are visible to the whole workgroup
-  rank_and_plan(L.n, L.ids, L.scores_out, false, L.keep, 0, L.keep_out, nullptr, nullptr);
-}
-
 __global__ void record_scores_kernel(DevPool P, const int32_t* list, const float* f, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
@@ -564,15 +438,6 @@ __global__ void record_scores_kernel(DevPool P, const int32_t* list, const float
 }
 
 }  // namespace
-
-hipError_t launch_mlp_score(const MlpLaunch& L, hipStream_t s) {
-  hipLaunchKernelGGL(mlp_tile_kernel, dim3((L.n + kMlpTileT - 1) / kMlpTileT, L.hidden / kMlpTileH), dim3(256),
-                     0, s, L);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(mlp_finish_kernel, dim3(1), dim3(kProbeThreads), 0, s, L);
-  return hipGetLastError();
-}
 
 hipError_t launch_record_scores(const DevPool& P, const int32_t* list, const float* f, int32_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;

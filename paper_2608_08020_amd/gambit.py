@@ -231,7 +231,7 @@ def mlp_score(h: torch.Tensor, w1: torch.Tensor, b1: torch.Tensor, w2: torch.Ten
     return scores, (keep_out[:keep] if keep > 0 else None)
 
 
-MLP_STATIC_SCRATCH_BYTES = 8 << 20
+MLP_STATIC_SCRATCH_BYTES = 16 << 20
 
 
 def mlp_score_static(h: torch.Tensor, w1: torch.Tensor, b1: torch.Tensor, w2: torch.Tensor, b2: float,

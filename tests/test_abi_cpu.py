@@ -169,7 +169,7 @@ def test_binding_checks_every_device_argument():
 
 def test_mlp_workspace_sizes_and_checks():
     """Workspace sizes of the MLP scorer: 0 for sizes outside the contract,
-    every n <= 4096 with hidden <= 16384 within the static buffer, and a
+    every n <= 4096 with hidden <= 131072 within the static buffer, and a
     short workspace refused before anything is launched."""
     import ctypes
 
@@ -177,9 +177,11 @@ def test_mlp_workspace_sizes_and_checks():
     L = gambit.lib()
     ws = L.gambit_mlp_workspace_size
     assert ws(0, 64) == 0 and ws(8, 96) == 0 and ws(8, 0) == 0
-    assert ws(512, 1024) >= 4 * 512 * (1024 // 32)  # the tiles' partial logits
+    assert ws(512, 1024) == 8 * 512 * 1024 * 4       # eight k splits' fp32 partial sums
+    assert ws(4096, 16384) == 4096 * (16384 // 128) * 4  # one split: the tiles' partial logits
     assert all(0 < ws(n, hd) <= gambit.MLP_STATIC_SCRATCH_BYTES
-               for n in (1, 100, 128, 512, 1000, 4096) for hd in (64, 1024, 4096, 16384))
+               for n in (1, 100, 128, 512, 1000, 4096) for hd in (64, 1024, 4096, 16384, 131072))
+    assert ws(4096, 131136) > gambit.MLP_STATIC_SCRATCH_BYTES
     fake = ctypes.c_void_p(1 << 20)              # never dereferenced: the calls fail their checks
     m = gambit.Mlp(256, 128, gambit.ACT_RELU, fake.value, fake.value, fake.value, 0.0)
     need = ws(16, 128)

@@ -49,10 +49,10 @@ def test_static_scratch_entry_matches_workspace_entry():
 
 def test_static_scratch_entry_refuses_sizes_beyond_its_buffer():
     L = gambit.lib()
-    n, dim, hidden = 4096, 128, 16448          # 4 * 4096 * (16448 / 32) bytes > 8 MiB
+    n, dim, hidden = 4096, 128, 131136         # 4 * 4096 * ceil(131136 / 128) bytes > 16 MiB
     assert L.gambit_mlp_workspace_size(n, hidden) > gambit.MLP_STATIC_SCRATCH_BYTES
     fake = ctypes.c_void_p(1 << 20)            # never dereferenced: the call fails its size check
     m = gambit.Mlp(dim, hidden, gambit.ACT_RELU, fake.value, fake.value, fake.value, 0.0)
     st = L.gambit_mlp_score_static(n, fake, ctypes.byref(m), fake, None, 0, None, None)
     assert st == gambit.ERR_WORKSPACE
-    assert L.gambit_mlp_workspace_size(4096, 16384) <= gambit.MLP_STATIC_SCRATCH_BYTES
+    assert L.gambit_mlp_workspace_size(4096, 131072) <= gambit.MLP_STATIC_SCRATCH_BYTES
