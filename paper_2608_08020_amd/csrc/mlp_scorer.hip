@@ -7,9 +7,10 @@
 //   1. mlp_gemm_kernel: W1 h on the bf16 matrix cores in 128 x 128 tiles
 //      (hidden states x hidden units), the k range split S ways so that the
 //      whole chip has work (512 x 4096 -> 1024: 32 tiles x 8 splits, one
-//      workgroup per CU).  With S > 1 each workgroup writes its fp32
-//      pre-activation partial sums; with S = 1 it applies bias, activation
-//      and w2 itself and writes one partial logit per hidden state and tile.
+//      eight-wave workgroup per CU).  With S > 1 each workgroup writes its
+//      fp32 pre-activation partial sums; with S = 1 it applies bias,
+//      activation and w2 itself and writes one partial logit per hidden state
+//      and tile.
 //   2. mlp_logit_kernel: per hidden state, the S partial sums in split order,
 //      bias, activation, times w2, summed over the units (or the tiles'
 //      partial logits in tile order), plus b2, sigmoid.
@@ -43,6 +44,10 @@ constexpr int kGK = 64;                  // k per LDS slab (128 B of each row)
 constexpr int kGStages = 4;              // slabs in the LDS ring
 constexpr int kGSlabA = kGT * kGK * 2;   // 16 KiB: one operand's slab
 constexpr int kGSlab = 2 * kGSlabA;
+constexpr int kGWaves = 8;               // two per SIMD
+constexpr int kGThreads = 64 * kGWaves;
+constexpr int kGLoads = kGT / 8 / kGWaves;       // 8-row loads per operand, wave and slab
+constexpr int kGUB = kGU / 16 / (kGWaves / 2);   // 16-unit blocks per wave
 static_assert(kGT == kGU, "both operands' slabs have the same shape");
 
 __device__ inline float mlp_act(float x, int act) {
@@ -59,23 +64,23 @@ __device__ inline uint32_t orderable(float f) {
 // next barrier.
 __device__ inline void wait_lds_reads() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
-// One workgroup, four waves: tile (tt, tu) of split s, i.e. hidden states
+// One workgroup, eight waves: tile (tt, tu) of split s, i.e. hidden states
 // t0 .. t0 + 127 x units u0 .. u0 + 127 over k in [k0, k0 + 64 nslab).
 //
 // Operands go from global memory straight into an LDS ring of four 64-deep
-// slabs (direct loads, three slabs in flight); wave w fills rows 32 w ..
-// 32 w + 31 of both operands, eight rows of 128 B per load.  Row r's 16-byte
+// slabs (direct loads, three slabs in flight); wave w fills rows 16 w ..
+// 16 w + 15 of both operands, eight rows of 128 B per load.  Row r's 16-byte
 // chunk c sits at chunk position c ^ ((r >> 1) & 7) of its 128-byte row, so
 // the sixteen rows that one matrix-core operand read touches (a 16 x 32
 // block, 16 B per lane) fall on sixteen different 16-byte bank groups.
 //
-// Wave w computes hidden states 64 (w & 1) .. + 63 x units 64 (w >> 1) .. +
-// 63: 4 x 4 blocks of v_mfma_f32_16x16x32_bf16, where lane (q, i) supplies
+// Wave w computes hidden states 64 (w & 1) .. + 63 x units 32 (w >> 1) .. +
+// 31: 4 x 2 blocks of v_mfma_f32_16x16x32_bf16, where lane (q, i) supplies
 // row i's k values 8q .. 8q + 7 of both operands and holds, in block (a, b),
 // hidden states 16 a + 4 q + e (e = 0..3) of unit 16 b + i.
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void mlp_gemm_kernel(MlpLaunch L) {
+__global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void mlp_gemm_kernel(MlpLaunch L) {
   __shared__ __attribute__((aligned(1024))) uint8_t ring[kGStages * kGSlab];
-  __shared__ float red[2][kGT];
+  __shared__ float red[kGWaves / 2][kGT];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   // Work items in (split, unit tile, state tile) order; when the grid is a
   // multiple of 8, consecutive items go to the same XCD (workgroup b runs on
@@ -91,13 +96,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int c0 = s * C / L.splits, c1 = (s + 1) * C / L.splits;
   const int k0 = c0 * 128, nslab = (c1 - c0) * 2;
 
-  // this lane's load sources: rows 32 w + 8 d + lane / 8, chunk position
+  // this lane's load sources: rows 16 w + 8 d + lane / 8, chunk position
   // lane % 8 (rows past the end re-read the last row; never stored)
-  const uint16_t* asrc[4];
-  const uint16_t* bsrc[4];
+  const uint16_t* asrc[kGLoads];
+  const uint16_t* bsrc[kGLoads];
 #pragma unroll
-  for (int d = 0; d < 4; ++d) {
-    const int r = 32 * wave + 8 * d + (lane >> 3);
+  for (int d = 0; d < kGLoads; ++d) {
+    const int r = 8 * kGLoads * wave + 8 * d + (lane >> 3);
     const int c = (lane & 7) ^ ((r >> 1) & 7);
     asrc[d] = L.h + (size_t)min(t0 + r, L.n - 1) * L.dim + k0 + 8 * c;
     bsrc[d] = L.w1 + (size_t)min(u0 + r, L.hidden - 1) * L.dim + k0 + 8 * c;
@@ -113,22 +118,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     kk = kk >= nslab ? kk - nslab : kk;
     const int ko = kk * kGK;
 #pragma unroll
-    for (int d = 0; d < 4; ++d) dma16(asrc[d] + ko, st + (32 * wave + 8 * d) * 128);
+    for (int d = 0; d < kGLoads; ++d) dma16(asrc[d] + ko, st + (8 * kGLoads * wave + 8 * d) * 128);
 #pragma unroll
-    for (int d = 0; d < 4; ++d) dma16(bsrc[d] + ko, st + kGSlabA + (32 * wave + 8 * d) * 128);
+    for (int d = 0; d < kGLoads; ++d) dma16(bsrc[d] + ko, st + kGSlabA + (8 * kGLoads * wave + 8 * d) * 128);
   };
 
   // operand read offsets (bytes within a stage) for the two 32-deep halves
   const int i = lane & 15, q = lane >> 4, swz = (i >> 1) & 7;
   const int wt = wave & 1, wu = wave >> 1;
-  const int offa = (64 * wt + i) * 128, offb = kGSlabA + (64 * wu + i) * 128;
+  const int offa = (64 * wt + i) * 128, offb = kGSlabA + (16 * kGUB * wu + i) * 128;
   const int pos0 = (q ^ swz) * 16, pos1 = ((q | 4) ^ swz) * 16;
 
-  f32x4 acc[4][4];
+  f32x4 acc[4][kGUB];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int b = 0; b < kGUB; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // Per slab: wait for it (this wave's loads of the slabs after it stay in
   // flight), barrier, refill the stage of the slab before it (every wave has
@@ -136,32 +141,32 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   for (int sl = 0; sl < kGStages - 1 && sl < nslab; ++sl) issue(sl);
   for (int sl = 0; sl < nslab; ++sl) {
     switch (min(kGStages - 2, nslab - 1 - sl)) {  // slabs issued after this one
-      case 2: wait_vmcnt<16>(); break;
-      case 1: wait_vmcnt<8>(); break;
+      case 2: wait_vmcnt<4 * kGLoads>(); break;
+      case 1: wait_vmcnt<2 * kGLoads>(); break;
       default: wait_vmcnt<0>(); break;
     }
     wait_lds_reads();
     barrier_no_fence();  // slab sl is in LDS; every wave is done with slab sl - 1
     if (sl + kGStages - 1 < nslab) issue(sl + kGStages - 1);
     const uint8_t* st = ring + (sl % kGStages) * kGSlab;
-    bf16x8 A0[4], B0[4], A1[4], B1[4];
+    bf16x8 A0[4], B0[kGUB], A1[4], B1[kGUB];
 #pragma unroll
     for (int a = 0; a < 4; ++a) A0[a] = *reinterpret_cast<const bf16x8*>(st + offa + a * 2048 + pos0);
 #pragma unroll
-    for (int b = 0; b < 4; ++b) B0[b] = *reinterpret_cast<const bf16x8*>(st + offb + b * 2048 + pos0);
+    for (int b = 0; b < kGUB; ++b) B0[b] = *reinterpret_cast<const bf16x8*>(st + offb + b * 2048 + pos0);
 #pragma unroll
     for (int a = 0; a < 4; ++a) A1[a] = *reinterpret_cast<const bf16x8*>(st + offa + a * 2048 + pos1);
 #pragma unroll
-    for (int b = 0; b < 4; ++b) B1[b] = *reinterpret_cast<const bf16x8*>(st + offb + b * 2048 + pos1);
+    for (int b = 0; b < kGUB; ++b) B1[b] = *reinterpret_cast<const bf16x8*>(st + offb + b * 2048 + pos1);
     __builtin_amdgcn_sched_barrier(0);  // all sixteen reads are issued before the first product
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
-      for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0[a], B0[b], acc[a][b], 0, 0, 0);
+      for (int b = 0; b < kGUB; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A0[a], B0[b], acc[a][b], 0, 0, 0);
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
-      for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1[a], B1[b], acc[a][b], 0, 0, 0);
+      for (int b = 0; b < kGUB; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1[a], B1[b], acc[a][b], 0, 0, 0);
   }
 
   if (L.splits > 1) {
@@ -177,14 +182,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
-      for (int b = 0; b < 4; ++b)
+      for (int b = 0; b < kGUB; ++b)
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          *reinterpret_cast<float*>(ring + (64 * wt + 16 * a + 4 * q + e) * kRow + (64 * wu + 16 * b + i) * 4) =
+          *reinterpret_cast<float*>(ring + (64 * wt + 16 * a + 4 * q + e) * kRow + (16 * kGUB * wu + 16 * b + i) * 4) =
               acc[a][b][e];
     __syncthreads();
     float* out = L.parts + (size_t)s * L.n * L.hidden;
-    for (int x = threadIdx.x; x < kGT * (kGU / 4); x += 256) {
+    for (int x = threadIdx.x; x < kGT * (kGU / 4); x += kGThreads) {
       const int r = x / (kGU / 4), c = 4 * (x % (kGU / 4));
       if (t0 + r < L.n && u0 + c < L.hidden)
         __builtin_nontemporal_store(*reinterpret_cast<const f32x4*>(ring + r * kRow + c * 4),
@@ -192,12 +197,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
     return;
   }
-  // S = 1: bias, activation, w2, summed over this wave's 64 units (blocks b
-  // in order, then the 16 lanes of a row group), then the two unit halves
-  float w2v[4], b1v[4];
+  // S = 1: bias, activation, w2, summed over this wave's units (blocks b in
+  // order, then the 16 lanes of a row group), then the unit groups in order
+  float w2v[kGUB], b1v[kGUB];
 #pragma unroll
-  for (int b = 0; b < 4; ++b) {
-    const int u = u0 + 64 * wu + 16 * b + i;
+  for (int b = 0; b < kGUB; ++b) {
+    const int u = u0 + 16 * kGUB * wu + 16 * b + i;
     w2v[b] = u < L.hidden ? L.w2[u] : 0.f;
     b1v[b] = u < L.hidden ? L.b1[u] : 0.f;
   }
@@ -207,14 +212,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     for (int e = 0; e < 4; ++e) {
       float v = 0.f;
 #pragma unroll
-      for (int b = 0; b < 4; ++b) v += w2v[b] * mlp_act(acc[a][b][e] + b1v[b], L.act);
+      for (int b = 0; b < kGUB; ++b) v += w2v[b] * mlp_act(acc[a][b][e] + b1v[b], L.act);
 #pragma unroll
       for (int off = 8; off > 0; off >>= 1) v += __shfl_xor(v, off);
       if (i == 0) red[wu][64 * wt + 16 * a + 4 * q + e] = v;
     }
   __syncthreads();
-  if (threadIdx.x < kGT && t0 + (int)threadIdx.x < L.n)
-    L.parts[(size_t)tu * L.n + t0 + threadIdx.x] = red[0][threadIdx.x] + red[1][threadIdx.x];
+  if (threadIdx.x < kGT && t0 + (int)threadIdx.x < L.n) {
+    float z = red[0][threadIdx.x];
+#pragma unroll
+    for (int g = 1; g < kGWaves / 2; ++g) z += red[g][threadIdx.x];
+    L.parts[(size_t)tu * L.n + t0 + threadIdx.x] = z;
+  }
 }
 
 // One workgroup per hidden state t.  S > 1: thread i takes units 4 i +
@@ -368,7 +377,7 @@ gambit_status launch(int32_t n, const void* h, const gambit_mlp* mlp, float* sco
   L.parts = parts;
   L.scores_out = scores_out;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipLaunchKernelGGL(mlp_gemm_kernel, dim3(L.tiles_t * L.tiles_u * L.splits), dim3(256), 0, s, L);
+  hipLaunchKernelGGL(mlp_gemm_kernel, dim3(L.tiles_t * L.tiles_u * L.splits), dim3(kGThreads), 0, s, L);
   if (hipGetLastError() != hipSuccess) return GAMBIT_ERR_DEVICE;
   hipLaunchKernelGGL(mlp_logit_kernel, dim3(n), dim3(256), 0, s, L);
   if (hipGetLastError() != hipSuccess) return GAMBIT_ERR_DEVICE;
