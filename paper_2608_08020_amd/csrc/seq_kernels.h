@@ -22,17 +22,19 @@ struct SeqDev {
   int32_t d_model, n_heads, n_layers, max_steps;
 };
 
-hipError_t seq_ln_rows(const void* in, bool in_bf16, float* out, int dim, const float* g, const float* b, int n,
-                       hipStream_t s);
 // Per-row (mean, 1 / sqrt(var + eps)) of bf16 rows.
 hipError_t seq_row_stats(const uint16_t* h, int dim, float2* stats, int n, hipStream_t s);
-// C = A W^T (+ epilogue); N a multiple of 64, K / splits a multiple of 16;
-// part holds splits * M * N floats when splits > 1.  With ln_stats, A is
+// C = A W^T; N a multiple of 64, K / splits a multiple of 16.  part != NULL:
+// the raw sums of the splits go to part[splits][M][N] (for seq_reduce_ln);
+// else one split, the epilogue applied and C written.  With ln_stats, A is
 // bf16 and LayerNorm-ed (stats, gain ln_g, bias ln_b) on the fly; else fp32.
 hipError_t seq_gemm(const void* A, const float2* ln_stats, const float* ln_g, const float* ln_b, const float* W,
                     float* C, int M, int N, int K, int splits, int epi, const float* R, float* part, hipStream_t s);
+// x = epi(sum of the splits of part) (R: the residual), then u = LN(x; g, b),
+// or with head the output head's scores and the step counts' advance.
+hipError_t seq_reduce_ln(const float* part, int splits, int epi, const float* R, float* x, int d, const float* g,
+                         const float* b, float* u, bool head, const SeqDev& S, float* scores, int n, hipStream_t s);
 hipError_t seq_attention(const SeqDev& S, int layer, const float* qkv, float* o, int n, hipStream_t s);
-hipError_t seq_head(const SeqDev& S, const float* x, float* scores, int n, hipStream_t s);
 hipError_t seq_fork(const SeqDev& S, const int32_t* pairs, int n, hipStream_t s);
 hipError_t seq_set_len(const SeqDev& S, const int32_t* ids, int n, int value, hipStream_t s);
 

@@ -220,27 +220,40 @@ gambit_status gambit_scorer_step(gambit_scorer* q, int32_t n, const int32_t* ids
   float* g = wsp<float>(q, q->L.g);
   using namespace gambit;
   SEQ_TRY(q, seq_row_stats(static_cast<const uint16_t*>(h), D, stats, n, s), "input LN statistics");
-  SEQ_TRY(q, seq_gemm(h, stats, d.ln_in_g, d.ln_in_b, d.w_in, x, n, dm, D, q->L.splits, kEpiGelu, nullptr, part, s),
+  SEQ_TRY(q, seq_gemm(h, stats, d.ln_in_g, d.ln_in_b, d.w_in, x, n, dm, D, q->L.splits, kEpiNone, nullptr, part, s),
           "input projection");
+  // each K-split projection's reduce also takes the LayerNorm after it: LN1
+  // of the next layer, LN2, or LN_out with the head after the last layer
+  auto reduce_ln = [&](int splits, int epi, const float* R, int next_ln1, const char* where) -> gambit_status {
+    const bool head = next_ln1 >= d.n_layers;
+    const float* g = head ? nullptr : d.ln1_g + (size_t)next_ln1 * dm;
+    const float* b = head ? nullptr : d.ln1_b + (size_t)next_ln1 * dm;
+    SEQ_TRY(q, seq_reduce_ln(part, splits, epi, R, x, dm, g, b, u, head, q->dev, scores_out, n, s), where);
+    return GAMBIT_OK;
+  };
+  st = reduce_ln(q->L.splits, kEpiGelu, nullptr, 0, "input projection reduce");
+  if (st) return st;
   for (int l = 0; l < d.n_layers; ++l) {
     const size_t dd = (size_t)dm * dm;
-    SEQ_TRY(q, seq_ln_rows(x, false, u, dm, d.ln1_g + (size_t)l * dm, d.ln1_b + (size_t)l * dm, n, s), "LN1");
     SEQ_TRY(q, seq_gemm(u, nullptr, nullptr, nullptr, d.w_qkv + 3 * dd * l, qkv, n, 3 * dm, dm, 1, kEpiNone, nullptr,
                         nullptr, s),
             "QKV");
     SEQ_TRY(q, seq_attention(q->dev, l, qkv, o, n, s), "attention step");
-    SEQ_TRY(q, seq_gemm(o, nullptr, nullptr, nullptr, d.w_o + dd * l, x, n, dm, dm, q->L.out_splits, kEpiResid, x,
+    SEQ_TRY(q, seq_gemm(o, nullptr, nullptr, nullptr, d.w_o + dd * l, x, n, dm, dm, q->L.out_splits, kEpiNone, nullptr,
                         part, s),
             "output projection");
-    SEQ_TRY(q, seq_ln_rows(x, false, u, dm, d.ln2_g + (size_t)l * dm, d.ln2_b + (size_t)l * dm, n, s), "LN2");
+    SEQ_TRY(q, seq_reduce_ln(part, q->L.out_splits, kEpiResid, x, x, dm, d.ln2_g + (size_t)l * dm,
+                             d.ln2_b + (size_t)l * dm, u, false, q->dev, scores_out, n, s),
+            "output projection reduce, LN2");
     SEQ_TRY(q, seq_gemm(u, nullptr, nullptr, nullptr, d.w_13 + 2 * (size_t)f * dm * l, g, n, 2 * f, dm, 1,
                         kEpiSwiGLU, nullptr, nullptr, s),
             "SwiGLU");
     SEQ_TRY(q, seq_gemm(g, nullptr, nullptr, nullptr, d.w_2 + (size_t)f * dm * l, x, n, dm, f, q->L.out_splits,
-                        kEpiResid, x, part, s),
+                        kEpiNone, nullptr, part, s),
             "SwiGLU out");
+    st = reduce_ln(q->L.out_splits, kEpiResid, x, l + 1, "SwiGLU out reduce, next LayerNorm");
+    if (st) return st;
   }
-  SEQ_TRY(q, seq_head(q->dev, x, scores_out, n, s), "output head");
   for (int i = 0; i < n; ++i) ++q->lens[ids[i]];
   return GAMBIT_OK;
 }

@@ -4,12 +4,15 @@
 // arrive in bf16.
 //
 // Per boundary, for the n listed traces (rows):
-//   u0 = LN_in(h)                          ln_rows_kernel (bf16 input)
-//   x  = GELU(u0 W_in^T)                   gemm_kernel, split over K, reduce + GELU
+//   x  = GELU(LN_in(h) W_in^T)             row_stats_kernel; gemm_kernel (LN
+//                                           applied while staging, K split)
 //   per layer: u = LN1(x); qkv = u Wqkv^T; o = attention step (RoPE, append
 //   the step's key and value, attend over the trace's steps 0..t);
 //   x += o Wo^T; u = LN2(x); a = u W13^T; g = SiLU(a1) * a3; x += g W2^T
 //   y  = sigmoid(w_out . LN_out(x)), and the trace's step count advances.
+// A K-split projection's partial sums are added, its epilogue applied and the
+// LayerNorm that follows it (LN1, LN2, or LN_out and the head) taken in one
+// launch, reduce_ln_kernel: 17 launches per boundary with two layers.
 #include <hip/hip_runtime.h>
 
 #include "seq_kernels.h"
@@ -34,26 +37,6 @@ __device__ inline float wave_max(float v) {
 __device__ inline float load_elem(const void* p, size_t i, bool bf16) {
   if (bf16) return __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(p)[i] << 16);
   return reinterpret_cast<const float*>(p)[i];
-}
-
-// LayerNorm of each row (one wave per row): mean, then the mean squared
-// deviation, both over the row; out = (x - mean) / sqrt(var + eps) * g + b.
-__global__ __launch_bounds__(256) void ln_rows_kernel(const void* in, int in_bf16, float* out, int dim,
-                                                      const float* g, const float* b, int n) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (row >= n) return;
-  const size_t base = (size_t)row * dim;
-  float s = 0.f;
-  for (int i = lane; i < dim; i += 64) s += load_elem(in, base + i, in_bf16);
-  const float mean = wave_sum(s) / dim;
-  float v = 0.f;
-  for (int i = lane; i < dim; i += 64) {
-    const float d = load_elem(in, base + i, in_bf16) - mean;
-    v += d * d;
-  }
-  const float rstd = 1.f / sqrtf(wave_sum(v) / dim + kSeqLnEps);
-  for (int i = lane; i < dim; i += 64)
-    out[base + i] = (load_elem(in, base + i, in_bf16) - mean) * rstd * g[i] + b[i];
 }
 
 __device__ inline float gelu_erf(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
@@ -104,8 +87,9 @@ __global__ __launch_bounds__(256) void row_stats_kernel(const uint16_t* h, int d
 // holds A[l % 16][k + l / 16] and B[k + l / 16][l % 16] = W[l % 16][k + l / 16];
 // result element (4 (l / 16) + r, l % 16) sits in lane l, register r.
 // LN_A: A is the bf16 step states, normalised while staged:
-// (h - mean) * rstd * g[k] + b[k].  One split: the epilogue is applied and C
-// written; several: the raw sums go to part[z][M][N] for seq_reduce_kernel.
+// (h - mean) * rstd * g[k] + b[k].  part != NULL: the raw sums of split z go
+// to part[z][M][N] for reduce_ln_kernel; else the epilogue is applied and C
+// written (one split).
 // kEpiSwiGLU: W holds W_1 and W_3 rows interleaved in groups of 16, so a
 // wave's two column blocks are W_1 and W_3 of the same 16 outputs, and
 // C[m][16 c + i] = SiLU(a1) * a3 with row stride N / 2.
@@ -185,7 +169,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const void* Av, const float2*
       }
     return;
   }
-  const bool split = gridDim.z > 1;
+  const bool split = part != nullptr;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -206,16 +190,64 @@ __global__ __launch_bounds__(256) void gemm_kernel(const void* Av, const float2*
       }
 }
 
-// Sum of the splits in split order, then the epilogue.
-__global__ __launch_bounds__(256) void seq_reduce_kernel(const float* part, int splits, float* C, size_t MN, int epi,
-                                                         const float* R) {
-  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= MN) return;
+// One workgroup per row of a K-split projection (width d, a multiple of 64;
+// thread c takes columns c + 256 k): the splits' partial sums added in split
+// order (loaded eight splits at a time, indices clamped so all eight loads
+// are in flight together), the epilogue (GELU, or the residual R added), the
+// row x written; then the LayerNorm of x (mean, then the mean squared
+// deviation, each a fixed reduction over the workgroup): head == 0 writes
+// u = LN(x) with gain g, bias b; head != 0 takes LN_out and the output head,
+// scores[row] = sigmoid(w_out . LN_out(x)), and advances the trace's step
+// count.  Each thread re-reads only the columns it wrote.
+__device__ inline float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  __syncthreads();  // red[] is free
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return ((red[0] + red[1]) + red[2]) + red[3];
+}
+
+__global__ __launch_bounds__(256) void reduce_ln_kernel(const float* part, int splits, int epi, const float* R,
+                                                        float* x, int d, const float* g, const float* b, float* u,
+                                                        int head, SeqDev S, float* scores, int n) {
+  __shared__ float red[4];
+  const int row = blockIdx.x;
+  const size_t MN = (size_t)n * d, base = (size_t)row * d;
   float s = 0.f;
-  for (int z = 0; z < splits; ++z) s += part[(size_t)z * MN + i];
-  if (epi == kEpiGelu) s = gelu_erf(s);
-  if (epi == kEpiResid) s += R[i];
-  C[i] = s;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    float y = 0.f;
+    for (int z0 = 0; z0 < splits; z0 += 8) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = part[(size_t)min(z0 + e, splits - 1) * MN + base + i];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (z0 + e < splits) y += v[e];
+    }
+    if (epi == kEpiGelu) y = gelu_erf(y);
+    else if (epi == kEpiResid) y += R[base + i];
+    x[base + i] = y;
+    s += y;
+  }
+  const float mean = block_sum(s, red) / d;
+  float v = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    const float e = x[base + i] - mean;
+    v += e * e;
+  }
+  const float rstd = 1.f / sqrtf(block_sum(v, red) / d + kSeqLnEps);
+  if (!head) {
+    for (int i = threadIdx.x; i < d; i += 256) u[base + i] = (x[base + i] - mean) * rstd * g[i] + b[i];
+    return;
+  }
+  float z = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256)
+    z += ((x[base + i] - mean) * rstd * S.ln_out_g[i] + S.ln_out_b[i]) * S.w_out[i];
+  z = block_sum(z, red);
+  if (threadIdx.x == 0) {
+    scores[row] = 1.f / (1.f + expf(-z));
+    S.lens[S.ids[row]] += 1;
+  }
 }
 
 // One attention step of one (trace row, head), head_dim 64, four waves.
@@ -310,27 +342,6 @@ __global__ __launch_bounds__(256) void seq_attn_kernel(SeqDev S, int layer, cons
   }
 }
 
-// y = sigmoid(w_out . LN_out(x_row)); the trace's step count advances.
-__global__ __launch_bounds__(256) void seq_head_kernel(SeqDev S, const float* x, float* scores, int n) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (row >= n) return;
-  const int d = S.d_model;
-  const float* xr = x + (size_t)row * d;
-  float s = 0.f;
-  for (int i = lane; i < d; i += 64) s += xr[i];
-  const float mean = wave_sum(s) / d;
-  float v = 0.f;
-  for (int i = lane; i < d; i += 64) v += (xr[i] - mean) * (xr[i] - mean);
-  const float rstd = 1.f / sqrtf(wave_sum(v) / d + kSeqLnEps);
-  float z = 0.f;
-  for (int i = lane; i < d; i += 64) z += ((xr[i] - mean) * rstd * S.ln_out_g[i] + S.ln_out_b[i]) * S.w_out[i];
-  z = wave_sum(z);
-  if (lane == 0) {
-    scores[row] = 1.f / (1.f + expf(-z));
-    S.lens[S.ids[row]] += 1;
-  }
-}
-
 // Branch: the child's history is the parent's (its whole cache region and
 // its step count).  One workgroup per (pair, slice of the region).
 __global__ __launch_bounds__(256) void seq_fork_kernel(SeqDev S, const int32_t* pairs, size_t region_f4) {
@@ -349,12 +360,6 @@ __global__ void seq_set_len_kernel(SeqDev S, const int32_t* ids, int n, int valu
 
 }  // namespace
 
-hipError_t seq_ln_rows(const void* in, bool in_bf16, float* out, int dim, const float* g, const float* b, int n,
-                       hipStream_t s) {
-  hipLaunchKernelGGL(ln_rows_kernel, dim3((n + 3) / 4), dim3(256), 0, s, in, (int)in_bf16, out, dim, g, b, n);
-  return hipGetLastError();
-}
-
 hipError_t seq_row_stats(const uint16_t* h, int dim, float2* stats, int n, hipStream_t s) {
   hipLaunchKernelGGL(row_stats_kernel, dim3(n), dim3(256), 0, s, h, dim, stats, n);
   return hipGetLastError();
@@ -370,22 +375,19 @@ hipError_t seq_gemm(const void* A, const float2* ln_stats, const float* ln_g, co
   else
     hipLaunchKernelGGL(gemm_kernel<false>, grid, dim3(256), 0, s, A, ln_stats, ln_g, ln_b, W, C, M, N, K, ks, epi,
                        R, part);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || splits == 1) return e;
-  const size_t MN = (size_t)M * N;
-  hipLaunchKernelGGL(seq_reduce_kernel, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, s, part, splits, C, MN,
-                     epi, R);
+  return hipGetLastError();
+}
+
+hipError_t seq_reduce_ln(const float* part, int splits, int epi, const float* R, float* x, int d, const float* g,
+                         const float* b, float* u, bool head, const SeqDev& S, float* scores, int n, hipStream_t s) {
+  hipLaunchKernelGGL(reduce_ln_kernel, dim3(n), dim3(256), 0, s, part, splits, epi, R, x, d, g, b, u, (int)head, S,
+                     scores, n);
   return hipGetLastError();
 }
 
 hipError_t seq_attention(const SeqDev& S, int layer, const float* qkv, float* o, int n, hipStream_t s) {
   const size_t lds = sizeof(float) * ((size_t)S.max_steps + 64 + 4 * 64 + 8);
   hipLaunchKernelGGL(seq_attn_kernel, dim3(n * S.n_heads), dim3(256), lds, s, S, layer, qkv, o, n);
-  return hipGetLastError();
-}
-
-hipError_t seq_head(const SeqDev& S, const float* x, float* scores, int n, hipStream_t s) {
-  hipLaunchKernelGGL(seq_head_kernel, dim3((n + 3) / 4), dim3(256), 0, s, S, x, scores, n);
   return hipGetLastError();
 }
 
