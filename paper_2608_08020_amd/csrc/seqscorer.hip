@@ -20,8 +20,6 @@
 namespace gambit {
 namespace {
 
-constexpr int kBM = 64, kBN = 64, kBK = 16;
-
 __device__ inline float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -80,12 +78,17 @@ __global__ __launch_bounds__(256) void row_stats_kernel(const uint16_t* h, int d
 }
 
 // C[M][N] = A[M][K] . W[N][K]^T over K range [z * ks, (z + 1) * ks) of split
-// z = blockIdx.z, on the fp32 matrix cores (v_mfma_f32_16x16x4f32).  64 x 64
-// tiles staged through LDS 16 deep, the next tile's loads in flight while
-// the current one is multiplied; each of the 4 waves computes a 32 x 32
-// quarter as 2 x 2 products of 16 x 16.  Operands of one product: lane l
-// holds A[l % 16][k + l / 16] and B[k + l / 16][l % 16] = W[l % 16][k + l / 16];
-// result element (4 (l / 16) + r, l % 16) sits in lane l, register r.
+// z = blockIdx.z, on the fp32 matrix cores (v_mfma_f32_16x16x4f32).  TM x 64
+// tiles (TM = 64 or 32); the K range is taken in chunks of 128 that are
+// staged whole in LDS (rows padded to 132 floats, so the 16 rows of an
+// operand read fall on 16 different 16-byte bank groups), the next chunk's
+// global loads in flight in registers while the current one is multiplied.
+// Each of the 4 waves computes a (TM / 2) x 32 quarter as 16 x 16 products.
+// A lane reads 4 consecutive k of its row (one 16-byte read) and feeds them
+// to 4 successive products: lane (q, i) contributes A[i][4q + kk] and
+// W[i][4q + kk] to product kk, the same k for both operands, so each product
+// sums over k = 4q + kk, q = 0..3; result element (4 (l / 16) + r, l % 16)
+// sits in lane l, register r.
 // LN_A: A is the bf16 step states, normalised while staged:
 // (h - mean) * rstd * g[k] + b[k].  part != NULL: the raw sums of split z go
 // to part[z][M][N] for reduce_ln_kernel; else the epilogue is applied and C
@@ -93,73 +96,98 @@ __global__ __launch_bounds__(256) void row_stats_kernel(const uint16_t* h, int d
 // kEpiSwiGLU: W holds W_1 and W_3 rows interleaved in groups of 16, so a
 // wave's two column blocks are W_1 and W_3 of the same 16 outputs, and
 // C[m][16 c + i] = SiLU(a1) * a3 with row stride N / 2.
-template <bool LN_A>
+constexpr int kKC = 128;       // k per staged chunk
+constexpr int kKP = kKC + 4;   // padded LDS row, floats
+template <bool LN_A, int TM>
 __global__ __launch_bounds__(256) void gemm_kernel(const void* Av, const float2* stats, const float* lg,
                                                    const float* lb, const float* W, float* C, int M, int N, int K,
                                                    int ks, int epi, const float* R, float* part) {
-  __shared__ float As[kBM][kBK + 1];
-  __shared__ float Ws[kBN][kBK + 1];
+  constexpr int MB = TM / 32;                    // 16-row blocks per wave
+  constexpr int AV = TM * (kKC / 4) / 256;       // float4 groups of A per thread and chunk
+  constexpr int WV = 64 * (kKC / 4) / 256;       // of W
+  __shared__ __attribute__((aligned(16))) float As[TM * kKP];
+  __shared__ __attribute__((aligned(16))) float Ws[64 * kKP];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int m0 = blockIdx.y * kBM, n0 = blockIdx.x * kBN;
-  const int k0 = blockIdx.z * ks, k1 = k0 + ks;
-  const int lr = tid >> 2, lk = (tid & 3) * 4;  // loader: row lr of the tile, k offset lk
-  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 32;
+  const int m0 = blockIdx.y * TM, n0 = blockIdx.x * 64;
+  const int k0 = blockIdx.z * ks;
   const int li = lane & 15, lq = lane >> 4;
-  const bool row_ok = m0 + lr < M;
-  float2 st = make_float2(0.f, 0.f);
-  if (LN_A && row_ok) st = stats[m0 + lr];
-  f32x4 acc[2][2];
+  const int wm = (wave >> 1) * (TM / 2), wn = (wave & 1) * 32;
+  // loader: group g = tid + 256 v is row g / 32, k offset 4 (g % 32); the k
+  // offset is the same for every v
+  const int lk = 4 * (tid & 31), lr = tid >> 5;
+  float2 st[AV];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int v = 0; v < AV; ++v) {
+    const int m = m0 + lr + 8 * v;
+    st[v] = (LN_A && m < M) ? stats[m] : make_float2(0.f, 0.f);
+  }
+  float4 ar[AV], wr[WV];
+  // chunk [kb, kb + kn): groups past kn (a shorter last chunk) stay zero and
+  // read nothing
+  auto fetch = [&](int kb, int kn) {
+    const bool kin = lk < kn;
+    float4 g4 = make_float4(0.f, 0.f, 0.f, 0.f), b4 = g4;
+    if (LN_A && kin) {
+      g4 = *reinterpret_cast<const float4*>(lg + kb + lk);
+      b4 = *reinterpret_cast<const float4*>(lb + kb + lk);
+    }
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float av[4];
-  float4 wv;
-  auto fetch = [&](int kb) {
-    av[0] = av[1] = av[2] = av[3] = 0.f;
-    if (row_ok) {
-      if constexpr (LN_A) {
-        const uint2 hv =
-            *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(Av) + (size_t)(m0 + lr) * K + kb + lk);
-        const float4 g = *reinterpret_cast<const float4*>(lg + kb + lk);
-        const float4 bb = *reinterpret_cast<const float4*>(lb + kb + lk);
-        av[0] = (__uint_as_float(hv.x << 16) - st.x) * st.y * g.x + bb.x;
-        av[1] = (__uint_as_float(hv.x & 0xFFFF0000u) - st.x) * st.y * g.y + bb.y;
-        av[2] = (__uint_as_float(hv.y << 16) - st.x) * st.y * g.z + bb.z;
-        av[3] = (__uint_as_float(hv.y & 0xFFFF0000u) - st.x) * st.y * g.w + bb.w;
-      } else {
-        const float4 a4 =
-            *reinterpret_cast<const float4*>(static_cast<const float*>(Av) + (size_t)(m0 + lr) * K + kb + lk);
-        av[0] = a4.x, av[1] = a4.y, av[2] = a4.z, av[3] = a4.w;
+    for (int v = 0; v < AV; ++v) {
+      const int m = m0 + lr + 8 * v;
+      ar[v] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (m < M && kin) {
+        if constexpr (LN_A) {
+          const uint2 hv = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(Av) + (size_t)m * K + kb + lk);
+          ar[v].x = (__uint_as_float(hv.x << 16) - st[v].x) * st[v].y * g4.x + b4.x;
+          ar[v].y = (__uint_as_float(hv.x & 0xFFFF0000u) - st[v].x) * st[v].y * g4.y + b4.y;
+          ar[v].z = (__uint_as_float(hv.y << 16) - st[v].x) * st[v].y * g4.z + b4.z;
+          ar[v].w = (__uint_as_float(hv.y & 0xFFFF0000u) - st[v].x) * st[v].y * g4.w + b4.w;
+        } else {
+          ar[v] = *reinterpret_cast<const float4*>(static_cast<const float*>(Av) + (size_t)m * K + kb + lk);
+        }
       }
     }
-    wv = *reinterpret_cast<const float4*>(W + (size_t)(n0 + lr) * K + kb + lk);
+#pragma unroll
+    for (int v = 0; v < WV; ++v)
+      wr[v] = kin ? *reinterpret_cast<const float4*>(W + (size_t)(n0 + lr + 8 * v) * K + kb + lk)
+                  : make_float4(0.f, 0.f, 0.f, 0.f);
   };
-  fetch(k0);
-  for (int kb = k0; kb < k1; kb += kBK) {
-    __syncthreads();  // the previous step's reads are done
+  f32x4 acc[MB][2];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) As[lr][lk + e] = av[e];
-    Ws[lr][lk + 0] = wv.x;
-    Ws[lr][lk + 1] = wv.y;
-    Ws[lr][lk + 2] = wv.z;
-    Ws[lr][lk + 3] = wv.w;
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  fetch(k0, min(kKC, ks));
+  for (int kb = k0; kb < k0 + ks; kb += kKC) {
+    const int kn = min(kKC, k0 + ks - kb);  // a multiple of 16
+    __syncthreads();  // the previous chunk's reads are done
+#pragma unroll
+    for (int v = 0; v < AV; ++v) *reinterpret_cast<float4*>(&As[(lr + 8 * v) * kKP + lk]) = ar[v];
+#pragma unroll
+    for (int v = 0; v < WV; ++v) *reinterpret_cast<float4*>(&Ws[(lr + 8 * v) * kKP + lk]) = wr[v];
     __syncthreads();
-    if (kb + kBK < k1) fetch(kb + kBK);
+    if (kb + kKC < k0 + ks) fetch(kb + kKC, min(kKC, k0 + ks - kb - kKC));
+    for (int kc = 0; kc < kn; kc += 16) {
+      float4 a[MB], b[2];
 #pragma unroll
-    for (int kk = 0; kk < kBK; kk += 4) {
-      const float a0 = As[wm + li][kk + lq], a1 = As[wm + 16 + li][kk + lq];
-      const float b0 = Ws[wn + li][kk + lq], b1 = Ws[wn + 16 + li][kk + lq];
-      acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0, acc[0][0], 0, 0, 0);
-      acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b1, acc[0][1], 0, 0, 0);
-      acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b0, acc[1][0], 0, 0, 0);
-      acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b1, acc[1][1], 0, 0, 0);
+      for (int i = 0; i < MB; ++i) a[i] = *reinterpret_cast<const float4*>(&As[(wm + 16 * i + li) * kKP + kc + 4 * lq]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = *reinterpret_cast<const float4*>(&Ws[(wn + 16 * j + li) * kKP + kc + 4 * lq]);
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].x, b[j].x, acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].y, b[j].y, acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].z, b[j].z, acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].w, b[j].w, acc[i][j], 0, 0, 0);
+        }
     }
   }
   if (epi == kEpiSwiGLU) {  // one split, no residual
     const int f = N / 2, c = (n0 + wn) / 32;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MB; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = m0 + wm + 16 * i + 4 * lq + r;
@@ -171,7 +199,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const void* Av, const float2*
   }
   const bool split = part != nullptr;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MB; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -368,13 +396,24 @@ hipError_t seq_row_stats(const uint16_t* h, int dim, float2* stats, int n, hipSt
 hipError_t seq_gemm(const void* A, const float2* ln_stats, const float* ln_g, const float* ln_b, const float* W,
                     float* C, int M, int N, int K, int splits, int epi, const float* R, float* part, hipStream_t s) {
   const int ks = K / splits;
-  const dim3 grid(N / kBN, (M + kBM - 1) / kBM, splits);
-  if (ln_stats)
-    hipLaunchKernelGGL(gemm_kernel<true>, grid, dim3(256), 0, s, A, ln_stats, ln_g, ln_b, W, C, M, N, K, ks, epi, R,
-                       part);
-  else
-    hipLaunchKernelGGL(gemm_kernel<false>, grid, dim3(256), 0, s, A, ln_stats, ln_g, ln_b, W, C, M, N, K, ks, epi,
-                       R, part);
+  // 64-row tiles when they alone give the GPU ~256 workgroups, else 32-row
+  const bool wide = (long)(N / 64) * ((M + 63) / 64) * splits >= 256;
+  const dim3 grid(N / 64, wide ? (M + 63) / 64 : (M + 31) / 32, splits);
+  if (ln_stats) {
+    if (wide)
+      hipLaunchKernelGGL((gemm_kernel<true, 64>), grid, dim3(256), 0, s, A, ln_stats, ln_g, ln_b, W, C, M, N, K, ks,
+                         epi, R, part);
+    else
+      hipLaunchKernelGGL((gemm_kernel<true, 32>), grid, dim3(256), 0, s, A, ln_stats, ln_g, ln_b, W, C, M, N, K, ks,
+                         epi, R, part);
+  } else {
+    if (wide)
+      hipLaunchKernelGGL((gemm_kernel<false, 64>), grid, dim3(256), 0, s, A, ln_stats, ln_g, ln_b, W, C, M, N, K, ks,
+                         epi, R, part);
+    else
+      hipLaunchKernelGGL((gemm_kernel<false, 32>), grid, dim3(256), 0, s, A, ln_stats, ln_g, ln_b, W, C, M, N, K, ks,
+                         epi, R, part);
+  }
   return hipGetLastError();
 }
 
