@@ -9,13 +9,16 @@
 namespace gambit {
 
 constexpr float kSeqLnEps = 1e-5f;
+// Row stride of a head's cached keys and values: max_steps rounded up to a
+// multiple of 4 (16-byte loads of four consecutive steps).
+__host__ __device__ constexpr int seq_kstride(int max_steps) { return (max_steps + 3) & ~3; }
 enum : int { kEpiNone = 0, kEpiGelu = 1, kEpiResid = 2, kEpiSwiGLU = 3 };
 
 struct SeqDev {
   const int32_t* ids;     // [n] listed trace slots, this boundary
   int32_t* lens;          // [max_traces] steps held per slot
   int32_t* err;           // device error word
-  float* cache;           // [max_traces][n_layers][n_heads][keys^T [64][max_steps], values [max_steps][64]]
+  float* cache;           // [max_traces][n_layers][n_heads][keys [ks / 4][64][4], values [ks][64]], ks = seq_kstride
   const float* ln_out_g;
   const float* ln_out_b;
   const float* w_out;

@@ -282,15 +282,31 @@ __global__ __launch_bounds__(256) void reduce_ln_kernel(const float* part, int s
 // The trace's step index t is its count of earlier steps.  Wave 0 (one
 // element per lane) applies RoPE - (x_i, x_{i+32}) rotated by
 // t * 10000^(-i/32) - and appends the rotated key and the value at t in the
-// trace's cache (keys transposed, [64][max_steps], so the score loop reads
-// consecutive steps across lanes; values [max_steps][64]).  All 256 threads
-// score the earlier steps, the softmax is taken over steps 0..t, and wave w
-// accumulates the values of steps j = w mod 4; the four partial sums and
-// step t's own term (its key and value in wave 0's registers) are added.
+// trace's cache: keys in groups of four steps, [ks / 4][64][4] (ks =
+// max_steps rounded up to a multiple of 4), so one group's 64 dimensions
+// are 1 KB of consecutive memory and four consecutive steps of a dimension
+// one 16-byte load; values [ks][64].  Scores of the earlier steps: thread
+// (j4, eq) takes steps 4 j4 .. 4 j4 + 3 over dimensions 16 eq .. 16 eq + 15
+// (256 consecutive bytes; the first group's loads are issued before wave 0
+// has finished the append, which they do not depend on), and the four
+// quarters are added by shuffles; steps past t - 1 in the last group are
+// masked (their slots are read but never used).  The softmax is taken over
+// steps 0..t; for the values, thread (g, c) takes dimensions 4 c .. 4 c + 3
+// of steps j = g mod 16, and the sixteen groups' sums and step t's own term
+// (its key and value in wave 0's registers) are added.
+__device__ inline float block_max(float v, float* red) {
+  v = wave_max(v);
+  __syncthreads();  // red[] is free
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
 __global__ __launch_bounds__(256) void seq_attn_kernel(SeqDev S, int layer, const float* qkv, float* o, int n) {
-  extern __shared__ float lds[];  // p[max_steps], q[64], partial outputs [4][64], reductions [8]
+  extern __shared__ __attribute__((aligned(16))) float lds[];  // p[ks], q[64], partial outputs [4][64], red[4]
+  const int ks = seq_kstride(S.max_steps);
   float* p = lds;
-  float* qs = p + S.max_steps;
+  float* qs = p + ks;
   float* op = qs + 64;
   float* red = op + 4 * 64;
   const int row = blockIdx.x / S.n_heads, h = blockIdx.x % S.n_heads;
@@ -303,9 +319,17 @@ __global__ __launch_bounds__(256) void seq_attn_kernel(SeqDev S, int layer, cons
     return;
   }
   const int d = S.d_model;
-  float* kt = S.cache + (((size_t)tr * S.n_layers + layer) * S.n_heads + h) * (size_t)(2 * 64 * S.max_steps);
-  float* vc = kt + (size_t)64 * S.max_steps;
-  float v = 0.f;
+  float* kq = S.cache + (((size_t)tr * S.n_layers + layer) * S.n_heads + h) * (size_t)(2 * 64 * ks);
+  float* vc = kq + (size_t)64 * ks;
+  const int eq = tid & 3, jq = tid >> 2;
+  // the first group of earlier steps' keys, before the append (disjoint slots)
+  float4 kv[16];
+  if (4 * jq < t) {
+    const float* kr = kq + (size_t)jq * 256 + 64 * eq;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) kv[e] = *reinterpret_cast<const float4*>(kr + 4 * e);
+  }
+  float v = 0.f, st = 0.f;
   if (wave == 0) {
     const float* src = qkv + (size_t)row * 3 * d + h * 64;
     const float q = src[lane], k = src[d + lane];
@@ -317,56 +341,87 @@ __global__ __launch_bounds__(256) void seq_attn_kernel(SeqDev S, int layer, cons
     const float qp = __shfl_xor(q, 32, 64), kp = __shfl_xor(k, 32, 64);
     const float qr = lane < 32 ? q * cs - qp * sn : qp * sn + q * cs;
     const float kr = lane < 32 ? k * cs - kp * sn : kp * sn + k * cs;
-    kt[(size_t)lane * S.max_steps + t] = kr;
+    kq[(size_t)(t >> 2) * 256 + 4 * lane + (t & 3)] = kr;
     vc[(size_t)t * 64 + lane] = v;
     qs[lane] = qr;
-    const float st = wave_sum(qr * kr) * 0.125f;  // scale 1 / sqrt(64)
-    if (lane == 0) red[0] = st;
+    st = wave_sum(qr * kr) * 0.125f;  // scale 1 / sqrt(64)
   }
-  __syncthreads();
-  const float st = red[0];
-  float mx = st;
-  for (int j = tid; j < t; j += 256) {
-    float s = 0.f;
-#pragma unroll 16
-    for (int e = 0; e < 64; ++e) s = fmaf(qs[e], kt[(size_t)e * S.max_steps + j], s);
-    s *= 0.125f;
-    p[j] = s;
-    mx = fmaxf(mx, s);
+  __syncthreads();  // qs[] is visible
+  float mx = -INFINITY;
+  for (int j0 = 4 * jq; j0 < t; j0 += 1024) {
+    if (j0 != 4 * jq) {
+      const float* kr = kq + (size_t)(j0 >> 2) * 256 + 64 * eq;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) kv[e] = *reinterpret_cast<const float4*>(kr + 4 * e);
+    }
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const float qe = qs[16 * eq + e];
+      a.x = fmaf(qe, kv[e].x, a.x);
+      a.y = fmaf(qe, kv[e].y, a.y);
+      a.z = fmaf(qe, kv[e].z, a.z);
+      a.w = fmaf(qe, kv[e].w, a.w);
+    }
+#pragma unroll
+    for (int m = 1; m <= 2; m <<= 1) {
+      a.x += __shfl_xor(a.x, m, 64);
+      a.y += __shfl_xor(a.y, m, 64);
+      a.z += __shfl_xor(a.z, m, 64);
+      a.w += __shfl_xor(a.w, m, 64);
+    }
+    a.x = j0 < t ? a.x * 0.125f : -INFINITY;
+    a.y = j0 + 1 < t ? a.y * 0.125f : -INFINITY;
+    a.z = j0 + 2 < t ? a.z * 0.125f : -INFINITY;
+    a.w = j0 + 3 < t ? a.w * 0.125f : -INFINITY;
+    if (eq == 0) *reinterpret_cast<float4*>(p + j0) = a;
+    mx = fmaxf(mx, fmaxf(fmaxf(a.x, a.y), fmaxf(a.z, a.w)));
   }
-  mx = wave_max(mx);
-  __syncthreads();  // red[0] has been read by every thread
-  if (lane == 0) red[wave] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  // the values of this thread's first two steps, in flight across the softmax
+  const int c = tid & 15, g = tid >> 4;
+  float4 v0 = make_float4(0.f, 0.f, 0.f, 0.f), v1 = v0;
+  if (g < t) v0 = *reinterpret_cast<const float4*>(vc + (size_t)g * 64 + 4 * c);
+  if (g + 16 < t) v1 = *reinterpret_cast<const float4*>(vc + (size_t)(g + 16) * 64 + 4 * c);
+  if (wave == 0 && lane == 0) mx = fmaxf(mx, st);
+  mx = block_max(mx, red);  // also publishes p[]
   float sum = 0.f;
   for (int j = tid; j < t; j += 256) {
     const float e = expf(p[j] - mx);
     p[j] = e;
     sum += e;
   }
-  sum = wave_sum(sum);
-  if (lane == 0) red[4 + wave] = sum;
-  __syncthreads();  // p[] and the partial sums are complete
-  // four steps' values in flight per iteration (independent sums)
-  float acc0 = 0.f, acc1 = 0.f, acc2 = 0.f, acc3 = 0.f;
-  int j = wave;
-  for (; j + 12 < t; j += 16) {
-    const float v0 = vc[(size_t)j * 64 + lane], v1 = vc[(size_t)(j + 4) * 64 + lane];
-    const float v2 = vc[(size_t)(j + 8) * 64 + lane], v3 = vc[(size_t)(j + 12) * 64 + lane];
-    acc0 = fmaf(p[j], v0, acc0);
-    acc1 = fmaf(p[j + 4], v1, acc1);
-    acc2 = fmaf(p[j + 8], v2, acc2);
-    acc3 = fmaf(p[j + 12], v3, acc3);
+  sum = block_sum(sum, red);  // also publishes the exponentials
+  float4 a0 = make_float4(0.f, 0.f, 0.f, 0.f), a1 = a0;
+  int j = g;
+  for (; j + 16 < t; j += 32) {  // two steps' values in flight per iteration (independent sums)
+    if (j != g) {
+      v0 = *reinterpret_cast<const float4*>(vc + (size_t)j * 64 + 4 * c);
+      v1 = *reinterpret_cast<const float4*>(vc + (size_t)(j + 16) * 64 + 4 * c);
+    }
+    const float p0 = p[j], p1 = p[j + 16];
+    a0.x = fmaf(p0, v0.x, a0.x), a0.y = fmaf(p0, v0.y, a0.y), a0.z = fmaf(p0, v0.z, a0.z), a0.w = fmaf(p0, v0.w, a0.w);
+    a1.x = fmaf(p1, v1.x, a1.x), a1.y = fmaf(p1, v1.y, a1.y), a1.z = fmaf(p1, v1.z, a1.z), a1.w = fmaf(p1, v1.w, a1.w);
   }
-  for (; j < t; j += 4) acc0 = fmaf(p[j], vc[(size_t)j * 64 + lane], acc0);
-  op[wave * 64 + lane] = (acc0 + acc1) + (acc2 + acc3);
+  if (j < t) {
+    if (j != g) v0 = *reinterpret_cast<const float4*>(vc + (size_t)j * 64 + 4 * c);
+    const float p0 = p[j];
+    a0.x = fmaf(p0, v0.x, a0.x), a0.y = fmaf(p0, v0.y, a0.y), a0.z = fmaf(p0, v0.z, a0.z), a0.w = fmaf(p0, v0.w, a0.w);
+  }
+  a0.x += a1.x, a0.y += a1.y, a0.z += a1.z, a0.w += a1.w;
+#pragma unroll
+  for (int m = 16; m <= 32; m <<= 1) {  // the wave's four step groups
+    a0.x += __shfl_xor(a0.x, m, 64);
+    a0.y += __shfl_xor(a0.y, m, 64);
+    a0.z += __shfl_xor(a0.z, m, 64);
+    a0.w += __shfl_xor(a0.w, m, 64);
+  }
+  if (lane < 16) *reinterpret_cast<float4*>(op + wave * 64 + 4 * lane) = a0;
   __syncthreads();
   if (wave == 0) {
     const float pt = expf(st - mx);
-    const float total = red[4] + red[5] + red[6] + red[7] + pt;
+    const float total = sum + pt;
     o[(size_t)row * d + h * 64 + lane] =
-        (op[lane] + op[64 + lane] + op[128 + lane] + op[192 + lane] + pt * v) / total;
+        (((op[lane] + op[64 + lane]) + op[128 + lane]) + op[192 + lane] + pt * v) / total;
   }
 }
 
@@ -425,13 +480,13 @@ hipError_t seq_reduce_ln(const float* part, int splits, int epi, const float* R,
 }
 
 hipError_t seq_attention(const SeqDev& S, int layer, const float* qkv, float* o, int n, hipStream_t s) {
-  const size_t lds = sizeof(float) * ((size_t)S.max_steps + 64 + 4 * 64 + 8);
+  const size_t lds = sizeof(float) * ((size_t)seq_kstride(S.max_steps) + 64 + 4 * 64 + 4);
   hipLaunchKernelGGL(seq_attn_kernel, dim3(n * S.n_heads), dim3(256), lds, s, S, layer, qkv, o, n);
   return hipGetLastError();
 }
 
 hipError_t seq_fork(const SeqDev& S, const int32_t* pairs, int n, hipStream_t s) {
-  const size_t region_f4 = (size_t)S.n_layers * S.n_heads * 2 * 64 * S.max_steps / 4;
+  const size_t region_f4 = (size_t)S.n_layers * S.n_heads * 2 * 64 * seq_kstride(S.max_steps) / 4;
   const unsigned slices = (unsigned)std::max<size_t>(1, std::min<size_t>(64, (region_f4 + 255) / 256));
   hipLaunchKernelGGL(seq_fork_kernel, dim3(slices, n), dim3(256), 0, s, S, pairs, region_f4);
   return hipGetLastError();
