@@ -12,13 +12,21 @@ constexpr float kSeqLnEps = 1e-5f;
 // Row stride of a head's cached keys and values: max_steps rounded up to a
 // multiple of 4 (16-byte loads of four consecutive steps).
 __host__ __device__ constexpr int seq_kstride(int max_steps) { return (max_steps + 3) & ~3; }
+// Floats of one (trace, layer, head) cache region: keys and values, plus 64
+// floats of padding so that regions do not start at the same offset modulo
+// a large power of two (every region's first lines would fall on the same
+// memory channels).
+__host__ __device__ constexpr size_t seq_region_floats(int max_steps) {
+  return (size_t)2 * 64 * seq_kstride(max_steps) + 64;
+}
 enum : int { kEpiNone = 0, kEpiGelu = 1, kEpiResid = 2, kEpiSwiGLU = 3 };
 
 struct SeqDev {
   const int32_t* ids;     // [n] listed trace slots, this boundary
   int32_t* lens;          // [max_traces] steps held per slot
   int32_t* err;           // device error word
-  float* cache;           // [max_traces][n_layers][n_heads][keys [ks / 4][64][4], values [ks][64]], ks = seq_kstride
+  float* cache;           // [max_traces][n_layers][n_heads] regions of seq_region_floats: keys [ks / 4][64][4],
+                          // values [ks][64], ks = seq_kstride
   const float* ln_out_g;
   const float* ln_out_b;
   const float* w_out;

@@ -49,7 +49,7 @@ bool seq_layout(const gambit_scorer_desc* d, SeqLayout* L) {
   L->pairs = take(8 * T);
   L->lens = take(4 * T);
   L->err = take(64);
-  L->cache = take(4 * T * d->n_layers * d->n_heads * 2 * 64 * (size_t)gambit::seq_kstride(d->max_steps));
+  L->cache = take(4 * T * d->n_layers * d->n_heads * gambit::seq_region_floats(d->max_steps));
   L->stats = take(8 * T);
   L->part = take(4 * (size_t)std::max(L->splits, L->out_splits) * T * dm);
   L->x = take(4 * T * dm);

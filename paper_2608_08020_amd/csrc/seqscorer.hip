@@ -319,7 +319,7 @@ __global__ __launch_bounds__(256) void seq_attn_kernel(SeqDev S, int layer, cons
     return;
   }
   const int d = S.d_model;
-  float* kq = S.cache + (((size_t)tr * S.n_layers + layer) * S.n_heads + h) * (size_t)(2 * 64 * ks);
+  float* kq = S.cache + (((size_t)tr * S.n_layers + layer) * S.n_heads + h) * seq_region_floats(S.max_steps);
   float* vc = kq + (size_t)64 * ks;
   const int eq = tid & 3, jq = tid >> 2;
   // the first group of earlier steps' keys, before the append (disjoint slots)
@@ -486,7 +486,7 @@ hipError_t seq_attention(const SeqDev& S, int layer, const float* qkv, float* o,
 }
 
 hipError_t seq_fork(const SeqDev& S, const int32_t* pairs, int n, hipStream_t s) {
-  const size_t region_f4 = (size_t)S.n_layers * S.n_heads * 2 * 64 * seq_kstride(S.max_steps) / 4;
+  const size_t region_f4 = (size_t)S.n_layers * S.n_heads * seq_region_floats(S.max_steps) / 4;
   const unsigned slices = (unsigned)std::max<size_t>(1, std::min<size_t>(64, (region_f4 + 255) / 256));
   hipLaunchKernelGGL(seq_fork_kernel, dim3(slices, n), dim3(256), 0, s, S, pairs, region_f4);
   return hipGetLastError();
