@@ -107,16 +107,11 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2, 2)
     asrc[d] = L.h + (size_t)min(t0 + r, L.n - 1) * L.dim + k0 + 8 * c;
     bsrc[d] = L.w1 + (size_t)min(u0 + r, L.hidden - 1) * L.dim + k0 + 8 * c;
   }
-  // Workgroups of one XCD take the slabs of their k range in rotated order:
-  // together they then request every slab at once, so each line is fetched
-  // into the XCD's L2 once and the other workgroups' reads of it hit there,
-  // instead of all of them waiting on the same misses.
-  const int rot = (G & 7) ? 0 : (blockIdx.x >> 3) % nslab;
+  // Every workgroup takes its slabs in k order, so equal hidden states in
+  // different tiles get bit-equal sums (and so equal scores, ranked by id).
   auto issue = [&](int sl) {
     uint8_t* st = ring + (sl % kGStages) * kGSlab;
-    int kk = sl + rot;
-    kk = kk >= nslab ? kk - nslab : kk;
-    const int ko = kk * kGK;
+    const int ko = sl * kGK;
 #pragma unroll
     for (int d = 0; d < kGLoads; ++d) dma16(asrc[d] + ko, st + (8 * kGLoads * wave + 8 * d) * 128);
 #pragma unroll

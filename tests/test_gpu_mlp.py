@@ -90,3 +90,25 @@ def test_mlp_scores_drive_the_tournament():
     sb, ns, _, _ = p.trace_state(list(range(16)))
     assert np.abs(sb - np.array(om.sbar)).max() <= 1e-5 and ns.tolist() == om.nsc
     p.pool_check()
+
+
+def test_exact_ties_rank_by_id():
+    """Many hidden states repeated exactly (bit-equal scores) under shuffled,
+    non-contiguous ids: the fused ranking is the total order (score
+    descending, id ascending) of the scores it returned, and the scores match
+    the oracle."""
+    cfg = MlpConfig(name="ties", seed=71, n=300, dim=512, hidden=256, act="relu")
+    W1, b1, w2, b2 = weights(cfg)
+    rng = np.random.default_rng(5)
+    src = rng.integers(0, 40, size=cfg.n)
+    h = hidden_states(cfg)[src]
+    ids = rng.permutation(1000)[:cfg.n].astype(np.int32)
+    got, top = mlp_score(_dev_bf16(h), _dev_bf16(W1), torch.from_numpy(b1).cuda(), torch.from_numpy(w2).cuda(), b2,
+                         cfg.act, ids=torch.from_numpy(ids).cuda(), keep=cfg.n)
+    s = got.cpu().numpy()
+    for k in np.unique(src):
+        assert np.all(s[src == k] == s[src == k][0]), "copies of one state scored differently"
+    order = sorted(range(cfg.n), key=lambda i: (-float(s[i]), int(ids[i])))
+    assert top.cpu().numpy().tolist() == [int(ids[i]) for i in order]
+    want = mlp_scores(bf16_to_f64(h), bf16_to_f64(W1), b1.astype(np.float64), w2.astype(np.float64), b2, cfg.act)
+    assert np.abs(s.astype(np.float64) - want).max() <= 1e-4
