@@ -134,3 +134,27 @@ def test_no_layers_and_single_step_capacity():
     gpu.free([0])
     assert gpu.steps(0) == 0 and gpu.steps(1) == 1
     gpu.check()
+
+
+def test_capacity_not_a_multiple_of_four_filled_with_forks():
+    """A history capacity of 13 steps (the cache rounds each head's rows up to
+    16): traces filled to capacity, a fork taken mid-way, every step against
+    the oracle - the last group of four cached keys is partly past the end
+    on most steps."""
+    import dataclasses
+    cfg = dataclasses.replace(SEQ_SMALL, max_steps=13, slots=6)
+    _, gpu, ref = _make(cfg)
+    ids = [0, 1, 2, 3]
+    for r in range(cfg.max_steps):
+        if r == 6:
+            gpu.fork([1, 2], [4, 5])
+            ref.fork([1, 2], [4, 5])
+            ids = [0, 1, 2, 3, 4, 5]
+        ids = [t for t in ids if len(ref.hist[t]) < cfg.max_steps]
+        H = step_states(cfg, r)[ids]
+        got = gpu.step(ids, _bf16(H)).cpu().numpy()
+        want = ref.step(ids, bf16_to_f64(H))
+        assert float(np.abs(got - want).max()) <= TOL, r
+    assert [gpu.steps(t) for t in range(cfg.slots)] == [len(h) for h in ref.hist]
+    assert gpu.steps(0) == cfg.max_steps
+    gpu.check()
