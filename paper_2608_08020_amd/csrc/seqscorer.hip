@@ -286,10 +286,10 @@ __global__ __launch_bounds__(256) void reduce_ln_kernel(const float* part, int s
 // max_steps rounded up to a multiple of 4), so one group's 64 dimensions
 // are 1 KB of consecutive memory and four consecutive steps of a dimension
 // one 16-byte load; values [ks][64].  Scores of the earlier steps: thread
-// (j4, eq) takes steps 4 j4 .. 4 j4 + 3 over dimensions 16 eq .. 16 eq + 15
-// (256 consecutive bytes; the first group's loads are issued before wave 0
-// has finished the append, which they do not depend on), and the four
-// quarters are added by shuffles; steps past t - 1 in the last group are
+// (j4, eq) takes steps 4 j4 .. 4 j4 + 3 over dimensions 8 eq .. 8 eq + 7
+// (128 consecutive bytes; the first group's loads are issued before wave 0
+// has finished the append, which they do not depend on), and the eight
+// parts are added by shuffles; steps past t - 1 in the last group are
 // masked (their slots are read but never used).  The softmax is taken over
 // steps 0..t; for the values, thread (g, c) takes dimensions 4 c .. 4 c + 3
 // of steps j = g mod 16, and the sixteen groups' sums and step t's own term
@@ -321,13 +321,13 @@ __global__ __launch_bounds__(256) void seq_attn_kernel(SeqDev S, int layer, cons
   const int d = S.d_model;
   float* kq = S.cache + (((size_t)tr * S.n_layers + layer) * S.n_heads + h) * seq_region_floats(S.max_steps);
   float* vc = kq + (size_t)64 * ks;
-  const int eq = tid & 3, jq = tid >> 2;
+  const int eq = tid & 7, jq = tid >> 3;
   // the first group of earlier steps' keys, before the append (disjoint slots)
-  float4 kv[16];
+  float4 kv[8];
   if (4 * jq < t) {
-    const float* kr = kq + (size_t)jq * 256 + 64 * eq;
+    const float* kr = kq + (size_t)jq * 256 + 32 * eq;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) kv[e] = *reinterpret_cast<const float4*>(kr + 4 * e);
+    for (int e = 0; e < 8; ++e) kv[e] = *reinterpret_cast<const float4*>(kr + 4 * e);
   }
   float v = 0.f, st = 0.f;
   if (wave == 0) {
@@ -348,23 +348,23 @@ __global__ __launch_bounds__(256) void seq_attn_kernel(SeqDev S, int layer, cons
   }
   __syncthreads();  // qs[] is visible
   float mx = -INFINITY;
-  for (int j0 = 4 * jq; j0 < t; j0 += 1024) {
+  for (int j0 = 4 * jq; j0 < t; j0 += 512) {
     if (j0 != 4 * jq) {
-      const float* kr = kq + (size_t)(j0 >> 2) * 256 + 64 * eq;
+      const float* kr = kq + (size_t)(j0 >> 2) * 256 + 32 * eq;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) kv[e] = *reinterpret_cast<const float4*>(kr + 4 * e);
+      for (int e = 0; e < 8; ++e) kv[e] = *reinterpret_cast<const float4*>(kr + 4 * e);
     }
     float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const float qe = qs[16 * eq + e];
+    for (int e = 0; e < 8; ++e) {
+      const float qe = qs[8 * eq + e];
       a.x = fmaf(qe, kv[e].x, a.x);
       a.y = fmaf(qe, kv[e].y, a.y);
       a.z = fmaf(qe, kv[e].z, a.z);
       a.w = fmaf(qe, kv[e].w, a.w);
     }
 #pragma unroll
-    for (int m = 1; m <= 2; m <<= 1) {
+    for (int m = 1; m <= 4; m <<= 1) {
       a.x += __shfl_xor(a.x, m, 64);
       a.y += __shfl_xor(a.y, m, 64);
       a.z += __shfl_xor(a.z, m, 64);
