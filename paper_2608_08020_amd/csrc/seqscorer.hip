@@ -348,7 +348,7 @@ __global__ __launch_bounds__(256) void seq_attn_kernel(SeqDev S, int layer, cons
   }
   __syncthreads();  // qs[] is visible
   float mx = -INFINITY;
-  for (int j0 = 4 * jq; j0 < t; j0 += 512) {
+  for (int j0 = 4 * jq; j0 < t; j0 += 128) {  // 32 groups of four steps per pass
     if (j0 != 4 * jq) {
       const float* kr = kq + (size_t)(j0 >> 2) * 256 + 32 * eq;
 #pragma unroll
@@ -377,11 +377,18 @@ __global__ __launch_bounds__(256) void seq_attn_kernel(SeqDev S, int layer, cons
     if (eq == 0) *reinterpret_cast<float4*>(p + j0) = a;
     mx = fmaxf(mx, fmaxf(fmaxf(a.x, a.y), fmaxf(a.z, a.w)));
   }
-  // the values of this thread's first two steps, in flight across the softmax
+  // the values of this thread's steps j0 + g + 16 i (i < 8) of a 128-step
+  // chunk, all in flight at once; the first chunk's across the softmax
   const int c = tid & 15, g = tid >> 4;
-  float4 v0 = make_float4(0.f, 0.f, 0.f, 0.f), v1 = v0;
-  if (g < t) v0 = *reinterpret_cast<const float4*>(vc + (size_t)g * 64 + 4 * c);
-  if (g + 16 < t) v1 = *reinterpret_cast<const float4*>(vc + (size_t)(g + 16) * 64 + 4 * c);
+  float4 vv[8];
+  auto load_v = [&](int j0) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int j = j0 + g + 16 * i;
+      vv[i] = j < t ? *reinterpret_cast<const float4*>(vc + (size_t)j * 64 + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  load_v(0);
   if (wave == 0 && lane == 0) mx = fmaxf(mx, st);
   mx = block_max(mx, red);  // also publishes p[]
   float sum = 0.f;
@@ -391,21 +398,18 @@ __global__ __launch_bounds__(256) void seq_attn_kernel(SeqDev S, int layer, cons
     sum += e;
   }
   sum = block_sum(sum, red);  // also publishes the exponentials
+  // steps g + 32 k into a0, g + 16 + 32 k into a1 (independent sums)
   float4 a0 = make_float4(0.f, 0.f, 0.f, 0.f), a1 = a0;
-  int j = g;
-  for (; j + 16 < t; j += 32) {  // two steps' values in flight per iteration (independent sums)
-    if (j != g) {
-      v0 = *reinterpret_cast<const float4*>(vc + (size_t)j * 64 + 4 * c);
-      v1 = *reinterpret_cast<const float4*>(vc + (size_t)(j + 16) * 64 + 4 * c);
+  for (int j0 = 0; j0 < t; j0 += 128) {
+    if (j0) load_v(j0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int j = j0 + g + 16 * i;
+      const float pj = j < t ? p[j] : 0.f;
+      float4& a = (i & 1) ? a1 : a0;
+      a.x = fmaf(pj, vv[i].x, a.x), a.y = fmaf(pj, vv[i].y, a.y), a.z = fmaf(pj, vv[i].z, a.z),
+      a.w = fmaf(pj, vv[i].w, a.w);
     }
-    const float p0 = p[j], p1 = p[j + 16];
-    a0.x = fmaf(p0, v0.x, a0.x), a0.y = fmaf(p0, v0.y, a0.y), a0.z = fmaf(p0, v0.z, a0.z), a0.w = fmaf(p0, v0.w, a0.w);
-    a1.x = fmaf(p1, v1.x, a1.x), a1.y = fmaf(p1, v1.y, a1.y), a1.z = fmaf(p1, v1.z, a1.z), a1.w = fmaf(p1, v1.w, a1.w);
-  }
-  if (j < t) {
-    if (j != g) v0 = *reinterpret_cast<const float4*>(vc + (size_t)j * 64 + 4 * c);
-    const float p0 = p[j];
-    a0.x = fmaf(p0, v0.x, a0.x), a0.y = fmaf(p0, v0.y, a0.y), a0.z = fmaf(p0, v0.z, a0.z), a0.w = fmaf(p0, v0.w, a0.w);
   }
   a0.x += a1.x, a0.y += a1.y, a0.z += a1.z, a0.w += a1.w;
 #pragma unroll

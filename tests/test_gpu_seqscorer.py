@@ -158,3 +158,31 @@ def test_capacity_not_a_multiple_of_four_filled_with_forks():
     assert [gpu.steps(t) for t in range(cfg.slots)] == [len(h) for h in ref.hist]
     assert gpu.steps(0) == cfg.max_steps
     gpu.check()
+
+
+def test_histories_past_one_pass_of_the_attention_step():
+    """Histories of up to 289 steps: the attention step scores 128 cached
+    steps per pass and reads the values 128 steps at a time, so lengths
+    just below, at and past 128 and 256 (and not multiples of four) take a
+    second and a third pass; a fork at step 140 copies a long history."""
+    import dataclasses
+    cfg = dataclasses.replace(SEQ_SMALL, max_steps=300, slots=4)
+    w, gpu, _ = _make(cfg)
+    hist = {t: [] for t in range(cfg.slots)}
+    ids = [0, 1, 2]
+    check = {0, 126, 127, 128, 129, 131, 141, 200, 255, 256, 257, 260, 288}
+    for r in range(289):
+        if r == 140:
+            gpu.fork([1], [3])
+            hist[3] = list(hist[1])
+            ids = [0, 1, 2, 3]
+        H = step_states(cfg, r)[ids]
+        got = gpu.step(ids, _bf16(H)).cpu().numpy()
+        for i, t in enumerate(ids):
+            hist[t].append(bf16_to_f64(H[i]))
+        if r in check:
+            for i, t in enumerate(ids):
+                want = scorer_outputs(w, np.stack(hist[t]), cfg.n_heads)[-1]
+                assert abs(got[i] - want) <= TOL, (r, t, got[i], want)
+    assert [gpu.steps(t) for t in range(cfg.slots)] == [289, 289, 289, 289]  # the fork copied 140 steps
+    gpu.check()
