@@ -160,7 +160,9 @@ def _check_plan(plan, m: PoolModel, Hkv, g, where):
         if slot[0][7] & 1:  # a cooperative item fills the whole slot
             assert all(u == slot[0] for u in slot), where
             slot = slot[:1]
-            assert slot[0][5] * g > 16, where
+            # up to 128 rows; the last item of a wide chunk takes what is
+            # left, as little as one member
+            assert 0 < slot[0][5] * g <= 128, where
         for owner, jb0, nblk, kvh, moff, mcnt, kidx, _ in slot:
             if mcnt == 0:
                 continue
