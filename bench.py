@@ -419,7 +419,7 @@ def scorer_measure(history: int = 128, reps: int = 10):
     return {"workload": c.name, "traces": n, "history_steps": history, "us_per_boundary": round(us, 1),
             "tflops": round(flops / us / 1e6, 3), "min_bytes_GB": round(nbytes / 1e9, 4),
             "gbps": round(nbytes / us / 1e3, 1), "cpu_oracle_us_per_trace": round(cpu_us, 1),
-            "note": "fp32 weights, activations and caches; 17 launches per boundary (2 layers)"}
+            "note": "fp32 weights, activations and caches (the input projection on the bf16 matrix cores against three bf16 planes that sum exactly to its fp32 weights); 16 launches per boundary (2 layers)"}
 
 
 def alg_bytes(cfg, st, T) -> int:

@@ -414,10 +414,16 @@ gambit_status gambit_profile_end(gambit_pool* pool, double* attn_ms, int32_t* la
  *                                          32c+31: W_3 rows 16c .. 16c+15
  *   w_2   [n_layers][d_model][d_ff]
  *   ln_out_g, ln_out_b, w_out [d_model]
- * d_model = 64 n_heads; input_dim and d_ff multiples of 64; max_steps <=
- * 8192.  The workspace (>= gambit_scorer_workspace_size, 256-B aligned)
+ * d_model = 64 n_heads; input_dim a multiple of 128, d_ff of 64; max_steps
+ * <= 8192.  The workspace (>= gambit_scorer_workspace_size, 256-B aligned)
  * holds the per-slot caches (fp32, max_traces * n_layers * n_heads * 2 * 64
- * * max_steps floats) and the step's activations.
+ * * max_steps floats), the step's activations and the input projection in
+ * the library's own form: gambit_scorer_create reads ln_in_g, ln_in_b and
+ * w_in once and keeps W_in scaled by ln_in_g as three bf16 planes whose sum
+ * is that product exactly (the bf16 step states are multiplied with them on
+ * the matrix cores, fp32 sums), its row sums and W_in ln_in_b; a change to
+ * those three weights takes a new scorer.  The other weights are read at
+ * every step.
  */
 typedef struct gambit_scorer gambit_scorer;
 typedef struct {

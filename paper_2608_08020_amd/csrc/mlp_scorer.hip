@@ -30,6 +30,7 @@
 
 #include "../../include/gambit.h"
 #include "kernels.h"
+#include "seq_kernels.h"
 #include "lds_dma.h"
 
 namespace gambit {
@@ -164,7 +165,7 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2, 2)
       for (int b = 0; b < kGUB; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A1[a], B1[b], acc[a][b], 0, 0, 0);
   }
 
-  if (L.splits > 1) {
+  if (L.splits > 1 || !L.b1) {  // b1 == NULL: partial sums only (bf16_gemm_partials)
     // pre-activation partial sums of split s, through LDS so that each row
     // of the tile leaves as 512 contiguous bytes (rows padded by 16 B: the
     // four row groups of a write fall on different banks); non-temporal
@@ -385,6 +386,28 @@ gambit_status launch(int32_t n, const void* h, const gambit_mlp* mlp, float* sco
 }
 
 }  // namespace
+
+// The split-k GEMM alone: parts[s][t][u] for every split, with no bias,
+// activation or w2 (L.b1 stays NULL), also when there is one split.
+hipError_t bf16_gemm_partials(const uint16_t* h, const uint16_t* w, int32_t n, int32_t dim, int32_t units,
+                              int32_t splits, float* parts, hipStream_t s) {
+  if (!h || !w || !parts || n <= 0 || dim <= 0 || dim % 128 || units <= 0 || units % 4 || splits < 1 ||
+      splits > dim / 128)
+    return hipErrorInvalidValue;
+  MlpLaunch L{};
+  L.n = n;
+  L.dim = dim;
+  L.hidden = units;
+  L.tiles_t = (n + kGT - 1) / kGT;
+  L.tiles_u = (units + kGU - 1) / kGU;
+  L.splits = splits;
+  L.h = h;
+  L.w1 = w;
+  L.parts = parts;
+  hipLaunchKernelGGL(mlp_gemm_kernel, dim3(L.tiles_t * L.tiles_u * L.splits), dim3(kGThreads), 0, s, L);
+  return hipGetLastError();
+}
+
 }  // namespace gambit
 
 extern "C" {

@@ -6,6 +6,8 @@
 #include <cstddef>
 #include <cstdint>
 
+#include "kernels.h"
+
 namespace gambit {
 
 constexpr float kSeqLnEps = 1e-5f;
@@ -33,18 +35,36 @@ struct SeqDev {
   int32_t d_model, n_heads, n_layers, max_steps;
 };
 
-// Per-row (mean, 1 / sqrt(var + eps)) of bf16 rows.
-hipError_t seq_row_stats(const uint16_t* h, int dim, float2* stats, int n, hipStream_t s);
-// C = A W^T; N a multiple of 64, K / splits a multiple of 16.  part != NULL:
-// the raw sums of the splits go to part[splits][M][N] (for seq_reduce_ln);
-// else one split, the epilogue applied and C written.  With ln_stats, A is
-// bf16 and LayerNorm-ed (stats, gain ln_g, bias ln_b) on the fly; else fp32.
-hipError_t seq_gemm(const void* A, const float2* ln_stats, const float* ln_g, const float* ln_b, const float* W,
-                    float* C, int M, int N, int K, int splits, int epi, const float* R, float* part, hipStream_t s);
+// C = A W^T (fp32); N a multiple of 64, K / splits a multiple of 16.
+// part != NULL: the raw sums of the splits go to part[splits][M][N] (for
+// seq_reduce_ln); else one split, the epilogue applied and C written.
+hipError_t seq_gemm(const float* A, const float* W, float* C, int M, int N, int K, int splits, int epi,
+                    const float* R, float* part, hipStream_t s);
+// The input projection's bf16 planes [3][dm][dim] of W_in scaled by the
+// input LayerNorm's gain (hi + mid + lo equal it exactly), their row sums c
+// and dv = W_in b (one launch, at creation).
+hipError_t seq_prep_input(const float* w_in, const float* ln_g, const float* ln_b, int dim, int dm, uint16_t* planes,
+                          float* c, float* dv, hipStream_t s);
+// x = GELU(LN_in(h) W_in^T) from the split partial sums of h against the
+// planes (part [splits][n][3 d]), then as seq_reduce_ln.
+hipError_t seq_reduce_in(const uint16_t* h, int dim, const float* part, int splits, const float* c, const float* dv,
+                         float* x, int d, const float* g, const float* b, float* u, bool head, const SeqDev& S,
+                         float* scores, int n, hipStream_t s);
 // x = epi(sum of the splits of part) (R: the residual), then u = LN(x; g, b),
 // or with head the output head's scores and the step counts' advance.
 hipError_t seq_reduce_ln(const float* part, int splits, int epi, const float* R, float* x, int d, const float* g,
                          const float* b, float* u, bool head, const SeqDev& S, float* scores, int n, hipStream_t s);
+// parts[s][t][u] = the sum over split s's k range of h[t][k] w[u][k], bf16
+// operands and fp32 sums, for s < splits: the MLP scorer's split-k GEMM
+// without its epilogue (mlp_scorer.hip).  dim a multiple of 128, units a
+// multiple of 4, 1 <= splits <= dim / 128; bf16_partial_splits gives the
+// MLP scorer's count (at most kMlpSplitBytes of sums when above one).
+inline int bf16_partial_splits(int32_t n, int32_t dim, int32_t units) {
+  const int s = mlp_splits(n, units);
+  return s < dim / 128 ? s : dim / 128;
+}
+hipError_t bf16_gemm_partials(const uint16_t* h, const uint16_t* w, int32_t n, int32_t dim, int32_t units,
+                              int32_t splits, float* parts, hipStream_t s);
 hipError_t seq_attention(const SeqDev& S, int layer, const float* qkv, float* o, int n, hipStream_t s);
 hipError_t seq_fork(const SeqDev& S, const int32_t* pairs, int n, hipStream_t s);
 hipError_t seq_set_len(const SeqDev& S, const int32_t* ids, int n, int value, hipStream_t s);

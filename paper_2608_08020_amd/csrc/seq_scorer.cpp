@@ -19,8 +19,7 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct SeqLayout {
-  size_t ids, pairs, lens, err, cache, stats, part, x, u, qkv, o, g, total;
-  int splits;      // of the input projection's K
+  size_t ids, pairs, lens, err, cache, planes, cvec, dvec, part, x, u, qkv, o, g, total;
   int out_splits;  // of the d_model-wide projections (W_o, W_2) over their K
 };
 
@@ -29,11 +28,9 @@ bool seq_layout(const gambit_scorer_desc* d, SeqLayout* L) {
       d->max_steps <= 0 || d->max_traces <= 0)
     return false;
   if (d->d_model != 64 * d->n_heads) return false;              // head_dim 64
-  if (d->input_dim % 64 || d->d_ff % 64) return false;          // GEMM tiles
+  if (d->input_dim % 128 || d->d_ff % 64) return false;         // GEMM tiles
   if (d->max_steps > 8192) return false;                        // LDS of the attention step
   const size_t T = d->max_traces, D = d->input_dim, dm = d->d_model, f = d->d_ff;
-  L->splits = (int)std::max<size_t>(1, D / 256);
-  while (D % (16 * (size_t)L->splits)) --L->splits;
   // W_o (K = d_model) and W_2 (K = d_ff) have d_model / 64 column tiles:
   // split their K four ways (while the parts stay >= 64 deep) to fill the GPU
   L->out_splits = 4;
@@ -50,8 +47,15 @@ bool seq_layout(const gambit_scorer_desc* d, SeqLayout* L) {
   L->lens = take(4 * T);
   L->err = take(64);
   L->cache = take(4 * T * d->n_layers * d->n_heads * gambit::seq_region_floats(d->max_steps));
-  L->stats = take(8 * T);
-  L->part = take(4 * (size_t)std::max(L->splits, L->out_splits) * T * dm);
+  L->planes = take(2 * 3 * dm * D);
+  L->cvec = take(4 * dm);
+  L->dvec = take(4 * dm);
+  // split partial sums: the input projection's (splits x n x 3 d_model, the
+  // largest over every n <= max_traces) or W_o's and W_2's
+  size_t part = (size_t)L->out_splits * T * dm;
+  for (size_t n = 1; n <= T; ++n)
+    part = std::max(part, (size_t)gambit::bf16_partial_splits((int)n, (int)D, (int)(3 * dm)) * n * 3 * dm);
+  L->part = take(4 * part);
   L->x = take(4 * T * dm);
   L->u = take(4 * T * dm);
   L->qkv = take(4 * T * 3 * dm);
@@ -168,6 +172,11 @@ gambit_status gambit_scorer_create(const gambit_scorer_desc* desc, void* stream,
                                hipHostMallocDefault);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&q->stage_ev, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventRecord(q->stage_ev, S(stream));
+  // the input projection's planes, row sums and bias term (w_in, ln_in_g and
+  // ln_in_b are not read again)
+  if (e == hipSuccess)
+    e = gambit::seq_prep_input(desc->w_in, desc->ln_in_g, desc->ln_in_b, desc->input_dim, desc->d_model,
+                               wsp<uint16_t>(q, L.planes), wsp<float>(q, L.cvec), wsp<float>(q, L.dvec), S(stream));
   // every slot starts with no steps; the error word starts clear
   std::vector<int32_t> all(desc->max_traces);
   for (int i = 0; i < desc->max_traces; ++i) all[i] = i;
@@ -211,7 +220,6 @@ gambit_status gambit_scorer_step(gambit_scorer* q, int32_t n, const int32_t* ids
   if (st) return st;
   const gambit_scorer_desc& d = q->d;
   const int D = d.input_dim, dm = d.d_model, f = d.d_ff;
-  float2* stats = wsp<float2>(q, q->L.stats);
   float* part = wsp<float>(q, q->L.part);
   float* x = wsp<float>(q, q->L.x);
   float* u = wsp<float>(q, q->L.u);
@@ -219,11 +227,18 @@ gambit_status gambit_scorer_step(gambit_scorer* q, int32_t n, const int32_t* ids
   float* o = wsp<float>(q, q->L.o);
   float* g = wsp<float>(q, q->L.g);
   using namespace gambit;
-  SEQ_TRY(q, seq_row_stats(static_cast<const uint16_t*>(h), D, stats, n, s), "input LN statistics");
-  SEQ_TRY(q, seq_gemm(h, stats, d.ln_in_g, d.ln_in_b, d.w_in, x, n, dm, D, q->L.splits, kEpiNone, nullptr, part, s),
+  const uint16_t* hb = static_cast<const uint16_t*>(h);
+  const int in_splits = bf16_partial_splits(n, D, 3 * dm);
+  SEQ_TRY(q, bf16_gemm_partials(hb, wsp<uint16_t>(q, q->L.planes), n, D, 3 * dm, in_splits, part, s),
           "input projection");
   // each K-split projection's reduce also takes the LayerNorm after it: LN1
   // of the next layer, LN2, or LN_out with the head after the last layer
+  {
+    const bool head = d.n_layers == 0;
+    SEQ_TRY(q, seq_reduce_in(hb, D, part, in_splits, wsp<float>(q, q->L.cvec), wsp<float>(q, q->L.dvec), x, dm,
+                             head ? nullptr : d.ln1_g, head ? nullptr : d.ln1_b, u, head, q->dev, scores_out, n, s),
+            "input projection reduce");
+  }
   auto reduce_ln = [&](int splits, int epi, const float* R, int next_ln1, const char* where) -> gambit_status {
     const bool head = next_ln1 >= d.n_layers;
     const float* g = head ? nullptr : d.ln1_g + (size_t)next_ln1 * dm;
@@ -231,25 +246,19 @@ gambit_status gambit_scorer_step(gambit_scorer* q, int32_t n, const int32_t* ids
     SEQ_TRY(q, seq_reduce_ln(part, splits, epi, R, x, dm, g, b, u, head, q->dev, scores_out, n, s), where);
     return GAMBIT_OK;
   };
-  st = reduce_ln(q->L.splits, kEpiGelu, nullptr, 0, "input projection reduce");
-  if (st) return st;
   for (int l = 0; l < d.n_layers; ++l) {
     const size_t dd = (size_t)dm * dm;
-    SEQ_TRY(q, seq_gemm(u, nullptr, nullptr, nullptr, d.w_qkv + 3 * dd * l, qkv, n, 3 * dm, dm, 1, kEpiNone, nullptr,
-                        nullptr, s),
+    SEQ_TRY(q, seq_gemm(u, d.w_qkv + 3 * dd * l, qkv, n, 3 * dm, dm, 1, kEpiNone, nullptr, nullptr, s),
             "QKV");
     SEQ_TRY(q, seq_attention(q->dev, l, qkv, o, n, s), "attention step");
-    SEQ_TRY(q, seq_gemm(o, nullptr, nullptr, nullptr, d.w_o + dd * l, x, n, dm, dm, q->L.out_splits, kEpiNone, nullptr,
-                        part, s),
+    SEQ_TRY(q, seq_gemm(o, d.w_o + dd * l, x, n, dm, dm, q->L.out_splits, kEpiNone, nullptr, part, s),
             "output projection");
     SEQ_TRY(q, seq_reduce_ln(part, q->L.out_splits, kEpiResid, x, x, dm, d.ln2_g + (size_t)l * dm,
                              d.ln2_b + (size_t)l * dm, u, false, q->dev, scores_out, n, s),
             "output projection reduce, LN2");
-    SEQ_TRY(q, seq_gemm(u, nullptr, nullptr, nullptr, d.w_13 + 2 * (size_t)f * dm * l, g, n, 2 * f, dm, 1,
-                        kEpiSwiGLU, nullptr, nullptr, s),
+    SEQ_TRY(q, seq_gemm(u, d.w_13 + 2 * (size_t)f * dm * l, g, n, 2 * f, dm, 1, kEpiSwiGLU, nullptr, nullptr, s),
             "SwiGLU");
-    SEQ_TRY(q, seq_gemm(g, nullptr, nullptr, nullptr, d.w_2 + (size_t)f * dm * l, x, n, dm, f, q->L.out_splits,
-                        kEpiNone, nullptr, part, s),
+    SEQ_TRY(q, seq_gemm(g, d.w_2 + (size_t)f * dm * l, x, n, dm, f, q->L.out_splits, kEpiNone, nullptr, part, s),
             "SwiGLU out");
     st = reduce_ln(q->L.out_splits, kEpiResid, x, l + 1, "SwiGLU out reduce, next LayerNorm");
     if (st) return st;

@@ -1,18 +1,23 @@
 // The history-aware sequence scorer (App. A.1, Eqs. 4-6), one new step per
 // trace per thought boundary against cached keys and values of the trace's
-// earlier steps.  fp32 throughout (weights and activations); the step states
-// arrive in bf16.
+// earlier steps.  fp32 weights, activations and caches; the step states
+// arrive in bf16, and the input projection runs on the bf16 matrix cores
+// with fp32 sums, its weights (scaled by the input LayerNorm's gain) split
+// exactly into three bf16 planes when the scorer is created.
 //
 // Per boundary, for the n listed traces (rows):
-//   x  = GELU(LN_in(h) W_in^T)             row_stats_kernel; gemm_kernel (LN
-//                                           applied while staging, K split)
+//   x  = GELU(LN_in(h) W_in^T)             bf16_gemm_partials (h against the
+//                                           planes, K split; mlp_scorer.hip);
+//                                           reduce_in_kernel (the splits and
+//                                           planes added, LN_in applied)
 //   per layer: u = LN1(x); qkv = u Wqkv^T; o = attention step (RoPE, append
 //   the step's key and value, attend over the trace's steps 0..t);
 //   x += o Wo^T; u = LN2(x); a = u W13^T; g = SiLU(a1) * a3; x += g W2^T
 //   y  = sigmoid(w_out . LN_out(x)), and the trace's step count advances.
 // A K-split projection's partial sums are added, its epilogue applied and the
 // LayerNorm that follows it (LN1, LN2, or LN_out and the head) taken in one
-// launch, reduce_ln_kernel: 17 launches per boundary with two layers.
+// launch (reduce_ln_kernel, reduce_in_kernel): 16 launches per boundary with
+// two layers.
 #include <hip/hip_runtime.h>
 
 #include "seq_kernels.h"
@@ -41,42 +46,6 @@ __device__ inline float gelu_erf(float x) { return 0.5f * x * (1.f + erff(x * 0.
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-// Row statistics of the step states for the input LayerNorm: one workgroup
-// per row, mean, then the mean squared deviation.
-__global__ __launch_bounds__(256) void row_stats_kernel(const uint16_t* h, int dim, float2* stats, int n) {
-  __shared__ float red[4];
-  const int row = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  if (row >= n) return;
-  const uint16_t* x = h + (size_t)row * dim;
-  const uint2* x4 = reinterpret_cast<const uint2*>(x);  // four bf16 per load (dim % 64 == 0)
-  auto f4 = [](uint2 u, float* o) {
-    o[0] = __uint_as_float(u.x << 16), o[1] = __uint_as_float(u.x & 0xFFFF0000u);
-    o[2] = __uint_as_float(u.y << 16), o[3] = __uint_as_float(u.y & 0xFFFF0000u);
-  };
-  float s = 0.f;
-  for (int i = threadIdx.x; i < dim / 4; i += 256) {
-    float e[4];
-    f4(x4[i], e);
-    s += (e[0] + e[1]) + (e[2] + e[3]);
-  }
-  s = wave_sum(s);
-  if (lane == 0) red[w] = s;
-  __syncthreads();
-  const float mean = (red[0] + red[1] + red[2] + red[3]) / dim;
-  __syncthreads();
-  float v = 0.f;
-  for (int i = threadIdx.x; i < dim / 4; i += 256) {
-    float e[4];
-    f4(x4[i], e);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) v += (e[k] - mean) * (e[k] - mean);
-  }
-  v = wave_sum(v);
-  if (lane == 0) red[w] = v;
-  __syncthreads();
-  if (threadIdx.x == 0) stats[row] = make_float2(mean, 1.f / sqrtf((red[0] + red[1] + red[2] + red[3]) / dim + kSeqLnEps));
-}
-
 // C[M][N] = A[M][K] . W[N][K]^T over K range [z * ks, (z + 1) * ks) of split
 // z = blockIdx.z, on the fp32 matrix cores (v_mfma_f32_16x16x4f32).  TM x 64
 // tiles (TM = 64 or 32); the K range is taken in chunks of 128 that are
@@ -89,8 +58,7 @@ __global__ __launch_bounds__(256) void row_stats_kernel(const uint16_t* h, int d
 // W[i][4q + kk] to product kk, the same k for both operands, so each product
 // sums over k = 4q + kk, q = 0..3; result element (4 (l / 16) + r, l % 16)
 // sits in lane l, register r.
-// LN_A: A is the bf16 step states, normalised while staged:
-// (h - mean) * rstd * g[k] + b[k].  part != NULL: the raw sums of split z go
+// part != NULL: the raw sums of split z go
 // to part[z][M][N] for reduce_ln_kernel; else the epilogue is applied and C
 // written (one split).
 // kEpiSwiGLU: W holds W_1 and W_3 rows interleaved in groups of 16, so a
@@ -98,9 +66,8 @@ __global__ __launch_bounds__(256) void row_stats_kernel(const uint16_t* h, int d
 // C[m][16 c + i] = SiLU(a1) * a3 with row stride N / 2.
 constexpr int kKC = 128;       // k per staged chunk
 constexpr int kKP = kKC + 4;   // padded LDS row, floats
-template <bool LN_A, int TM>
-__global__ __launch_bounds__(256) void gemm_kernel(const void* Av, const float2* stats, const float* lg,
-                                                   const float* lb, const float* W, float* C, int M, int N, int K,
+template <int TM>
+__global__ __launch_bounds__(256) void gemm_kernel(const float* A, const float* W, float* C, int M, int N, int K,
                                                    int ks, int epi, const float* R, float* part) {
   constexpr int MB = TM / 32;                    // 16-row blocks per wave
   constexpr int AV = TM * (kKC / 4) / 256;       // float4 groups of A per thread and chunk
@@ -115,37 +82,16 @@ __global__ __launch_bounds__(256) void gemm_kernel(const void* Av, const float2*
   // loader: group g = tid + 256 v is row g / 32, k offset 4 (g % 32); the k
   // offset is the same for every v
   const int lk = 4 * (tid & 31), lr = tid >> 5;
-  float2 st[AV];
-#pragma unroll
-  for (int v = 0; v < AV; ++v) {
-    const int m = m0 + lr + 8 * v;
-    st[v] = (LN_A && m < M) ? stats[m] : make_float2(0.f, 0.f);
-  }
   float4 ar[AV], wr[WV];
   // chunk [kb, kb + kn): groups past kn (a shorter last chunk) stay zero and
   // read nothing
   auto fetch = [&](int kb, int kn) {
     const bool kin = lk < kn;
-    float4 g4 = make_float4(0.f, 0.f, 0.f, 0.f), b4 = g4;
-    if (LN_A && kin) {
-      g4 = *reinterpret_cast<const float4*>(lg + kb + lk);
-      b4 = *reinterpret_cast<const float4*>(lb + kb + lk);
-    }
 #pragma unroll
     for (int v = 0; v < AV; ++v) {
       const int m = m0 + lr + 8 * v;
-      ar[v] = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (m < M && kin) {
-        if constexpr (LN_A) {
-          const uint2 hv = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(Av) + (size_t)m * K + kb + lk);
-          ar[v].x = (__uint_as_float(hv.x << 16) - st[v].x) * st[v].y * g4.x + b4.x;
-          ar[v].y = (__uint_as_float(hv.x & 0xFFFF0000u) - st[v].x) * st[v].y * g4.y + b4.y;
-          ar[v].z = (__uint_as_float(hv.y << 16) - st[v].x) * st[v].y * g4.z + b4.z;
-          ar[v].w = (__uint_as_float(hv.y & 0xFFFF0000u) - st[v].x) * st[v].y * g4.w + b4.w;
-        } else {
-          ar[v] = *reinterpret_cast<const float4*>(static_cast<const float*>(Av) + (size_t)m * K + kb + lk);
-        }
-      }
+      ar[v] = (m < M && kin) ? *reinterpret_cast<const float4*>(A + (size_t)m * K + kb + lk)
+                             : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 #pragma unroll
     for (int v = 0; v < WV; ++v)
@@ -235,6 +181,31 @@ __device__ inline float block_sum(float v, float* red) {
   return ((red[0] + red[1]) + red[2]) + red[3];
 }
 
+// The LayerNorm of row x[base ..] (s: this thread's sum of the columns it
+// wrote), then u = LN(x) or the output head.
+__device__ inline void ln_tail(float s, const float* x, size_t base, int d, const float* g, const float* b, float* u,
+                               int head, const SeqDev& S, float* scores, int row, float* red) {
+  const float mean = block_sum(s, red) / d;
+  float v = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    const float e = x[base + i] - mean;
+    v += e * e;
+  }
+  const float rstd = 1.f / sqrtf(block_sum(v, red) / d + kSeqLnEps);
+  if (!head) {
+    for (int i = threadIdx.x; i < d; i += 256) u[base + i] = (x[base + i] - mean) * rstd * g[i] + b[i];
+    return;
+  }
+  float z = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256)
+    z += ((x[base + i] - mean) * rstd * S.ln_out_g[i] + S.ln_out_b[i]) * S.w_out[i];
+  z = block_sum(z, red);
+  if (threadIdx.x == 0) {
+    scores[row] = 1.f / (1.f + expf(-z));
+    S.lens[S.ids[row]] += 1;
+  }
+}
+
 __global__ __launch_bounds__(256) void reduce_ln_kernel(const float* part, int splits, int epi, const float* R,
                                                         float* x, int d, const float* g, const float* b, float* u,
                                                         int head, SeqDev S, float* scores, int n) {
@@ -257,24 +228,134 @@ __global__ __launch_bounds__(256) void reduce_ln_kernel(const float* part, int s
     x[base + i] = y;
     s += y;
   }
-  const float mean = block_sum(s, red) / d;
-  float v = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) {
-    const float e = x[base + i] - mean;
-    v += e * e;
+  ln_tail(s, x, base, d, g, b, u, head, S, scores, row, red);
+}
+
+// The input projection's reduce, one workgroup per row: the input
+// LayerNorm's statistics of h[row] (mean, then the mean squared deviation),
+// the split partial sums of h W'^T over the three planes (parts
+// [splits][n][3 d]: plane p of column i at p d + i), added split by split in
+// order, then x = GELU(rstd (y - mean c[i]) + dv[i]) (LN_in(h) W_in^T
+// rearranged: c = the row sums of W', dv = W_in b), then ln_tail.  The
+// state's first 4096 values (four 8-byte loads per thread, kept in
+// registers for both statistics passes) and the first column's partial sums
+// of up to kInBatch splits are all requested before any of them is used.
+constexpr int kInBatch = 12;
+
+__global__ __launch_bounds__(256) void reduce_in_kernel(const uint16_t* h, int dim, const float* part, int splits,
+                                                        const float* c, const float* dv, float* x, int d,
+                                                        const float* g, const float* b, float* u, int head, SeqDev S,
+                                                        float* scores, int n) {
+  __shared__ float red[4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const uint2* h4 = reinterpret_cast<const uint2*>(h + (size_t)row * dim);  // four bf16 per load
+  const int nh4 = dim / 4;
+  const size_t units = (size_t)3 * d, MN = (size_t)n * units, pbase = (size_t)row * units, base = (size_t)row * d;
+  // split partials of column i, splits z0 .. z0 + kInBatch - 1 (indices
+  // clamped: every load is in bounds; only splits < `splits` are added)
+  float v[kInBatch][3];
+  auto load_parts = [&](int i, int z0) {
+#pragma unroll
+    for (int e = 0; e < kInBatch; ++e)
+#pragma unroll
+      for (int p = 0; p < 3; ++p) v[e][p] = part[(size_t)min(z0 + e, splits - 1) * MN + pbase + p * d + i];
+  };
+  uint2 hr[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) hr[j] = tid + 256 * j < nh4 ? h4[tid + 256 * j] : make_uint2(0u, 0u);
+  if (tid < d) load_parts(tid, 0);
+  auto f4 = [](uint2 w, float* o) {
+    o[0] = __uint_as_float(w.x << 16), o[1] = __uint_as_float(w.x & 0xFFFF0000u);
+    o[2] = __uint_as_float(w.y << 16), o[3] = __uint_as_float(w.y & 0xFFFF0000u);
+  };
+  float hs = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {  // zeros past the row add nothing
+    float e[4];
+    f4(hr[j], e);
+    hs += (e[0] + e[1]) + (e[2] + e[3]);
   }
-  const float rstd = 1.f / sqrtf(block_sum(v, red) / d + kSeqLnEps);
-  if (!head) {
-    for (int i = threadIdx.x; i < d; i += 256) u[base + i] = (x[base + i] - mean) * rstd * g[i] + b[i];
-    return;
+  for (int i = tid + 1024; i < nh4; i += 256) {
+    float e[4];
+    f4(h4[i], e);
+    hs += (e[0] + e[1]) + (e[2] + e[3]);
   }
-  float z = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256)
-    z += ((x[base + i] - mean) * rstd * S.ln_out_g[i] + S.ln_out_b[i]) * S.w_out[i];
-  z = block_sum(z, red);
+  const float hmean = block_sum(hs, red) / dim;
+  float hv = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (tid + 256 * j < nh4) {
+      float e[4];
+      f4(hr[j], e);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) hv += (e[k] - hmean) * (e[k] - hmean);
+    }
+  }
+  for (int i = tid + 1024; i < nh4; i += 256) {
+    float e[4];
+    f4(h4[i], e);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) hv += (e[k] - hmean) * (e[k] - hmean);
+  }
+  const float hrstd = 1.f / sqrtf(block_sum(hv, red) / dim + kSeqLnEps);
+  float s = 0.f;
+  for (int i = tid; i < d; i += 256) {
+    float y = 0.f;
+    for (int z0 = 0; z0 < splits; z0 += kInBatch) {
+      if (i != tid || z0 != 0) load_parts(i, z0);
+#pragma unroll
+      for (int e = 0; e < kInBatch; ++e)
+        if (z0 + e < splits) y += (v[e][0] + v[e][1]) + v[e][2];
+    }
+    y = gelu_erf(hrstd * (y - hmean * c[i]) + dv[i]);
+    x[base + i] = y;
+    s += y;
+  }
+  ln_tail(s, x, base, d, g, b, u, head, S, scores, row, red);
+}
+
+// The input projection's weights for the bf16 matrix cores, one workgroup
+// per output row n: W'[n][k] = W_in[n][k] g[k] (an fp32 product) split into
+// three bf16 planes, hi = bf16(W'), mid = bf16(W' - hi), lo = W' - hi - mid
+// (each difference exact in fp32; lo has at most 8 significant bits, so
+// hi + mid + lo = W' exactly), planes [3][dm][dim]; c[n] = sum_k W'[n][k]
+// and dv[n] = sum_k W_in[n][k] b[k], added in fp64 and rounded once.
+__device__ inline uint16_t bf16_rne(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+__global__ __launch_bounds__(256) void prep_input_kernel(const float* w, const float* g, const float* b, int dim,
+                                                         int dm, uint16_t* planes, float* c, float* dv) {
+  __shared__ double red[2][4];
+  const int n = blockIdx.x;
+  double sc = 0.0, sd = 0.0;
+  for (int k = threadIdx.x; k < dim; k += 256) {
+    const float wv = w[(size_t)n * dim + k];
+    const float x = wv * g[k];
+    const uint16_t hi = bf16_rne(x);
+    const float r1 = x - __uint_as_float((uint32_t)hi << 16);
+    const uint16_t mid = bf16_rne(r1);
+    const float r2 = r1 - __uint_as_float((uint32_t)mid << 16);
+    planes[(size_t)n * dim + k] = hi;
+    planes[((size_t)dm + n) * dim + k] = mid;
+    planes[((size_t)2 * dm + n) * dim + k] = bf16_rne(r2);  // exact: r2 has at most 8 significant bits
+    sc += (double)x;
+    sd += (double)wv * (double)b[k];
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    sc += __shfl_xor(sc, o, 64);
+    sd += __shfl_xor(sd, o, 64);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = sc;
+    red[1][threadIdx.x >> 6] = sd;
+  }
+  __syncthreads();
   if (threadIdx.x == 0) {
-    scores[row] = 1.f / (1.f + expf(-z));
-    S.lens[S.ids[row]] += 1;
+    c[n] = (float)(((red[0][0] + red[0][1]) + red[0][2]) + red[0][3]);
+    dv[n] = (float)(((red[1][0] + red[1][1]) + red[1][2]) + red[1][3]);
   }
 }
 
@@ -447,32 +528,30 @@ __global__ void seq_set_len_kernel(SeqDev S, const int32_t* ids, int n, int valu
 
 }  // namespace
 
-hipError_t seq_row_stats(const uint16_t* h, int dim, float2* stats, int n, hipStream_t s) {
-  hipLaunchKernelGGL(row_stats_kernel, dim3(n), dim3(256), 0, s, h, dim, stats, n);
-  return hipGetLastError();
-}
-
-hipError_t seq_gemm(const void* A, const float2* ln_stats, const float* ln_g, const float* ln_b, const float* W,
-                    float* C, int M, int N, int K, int splits, int epi, const float* R, float* part, hipStream_t s) {
+hipError_t seq_gemm(const float* A, const float* W, float* C, int M, int N, int K, int splits, int epi,
+                    const float* R, float* part, hipStream_t s) {
   const int ks = K / splits;
   // 64-row tiles when they alone give the GPU ~256 workgroups, else 32-row
   const bool wide = (long)(N / 64) * ((M + 63) / 64) * splits >= 256;
   const dim3 grid(N / 64, wide ? (M + 63) / 64 : (M + 31) / 32, splits);
-  if (ln_stats) {
-    if (wide)
-      hipLaunchKernelGGL((gemm_kernel<true, 64>), grid, dim3(256), 0, s, A, ln_stats, ln_g, ln_b, W, C, M, N, K, ks,
-                         epi, R, part);
-    else
-      hipLaunchKernelGGL((gemm_kernel<true, 32>), grid, dim3(256), 0, s, A, ln_stats, ln_g, ln_b, W, C, M, N, K, ks,
-                         epi, R, part);
-  } else {
-    if (wide)
-      hipLaunchKernelGGL((gemm_kernel<false, 64>), grid, dim3(256), 0, s, A, ln_stats, ln_g, ln_b, W, C, M, N, K, ks,
-                         epi, R, part);
-    else
-      hipLaunchKernelGGL((gemm_kernel<false, 32>), grid, dim3(256), 0, s, A, ln_stats, ln_g, ln_b, W, C, M, N, K, ks,
-                         epi, R, part);
-  }
+  if (wide)
+    hipLaunchKernelGGL((gemm_kernel<64>), grid, dim3(256), 0, s, A, W, C, M, N, K, ks, epi, R, part);
+  else
+    hipLaunchKernelGGL((gemm_kernel<32>), grid, dim3(256), 0, s, A, W, C, M, N, K, ks, epi, R, part);
+  return hipGetLastError();
+}
+
+hipError_t seq_prep_input(const float* w_in, const float* ln_g, const float* ln_b, int dim, int dm, uint16_t* planes,
+                          float* c, float* dv, hipStream_t s) {
+  hipLaunchKernelGGL(prep_input_kernel, dim3(dm), dim3(256), 0, s, w_in, ln_g, ln_b, dim, dm, planes, c, dv);
+  return hipGetLastError();
+}
+
+hipError_t seq_reduce_in(const uint16_t* h, int dim, const float* part, int splits, const float* c, const float* dv,
+                         float* x, int d, const float* g, const float* b, float* u, bool head, const SeqDev& S,
+                         float* scores, int n, hipStream_t s) {
+  hipLaunchKernelGGL(reduce_in_kernel, dim3(n), dim3(256), 0, s, h, dim, part, splits, c, dv, x, d, g, b, u,
+                     (int)head, S, scores, n);
   return hipGetLastError();
 }
 

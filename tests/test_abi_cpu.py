@@ -67,7 +67,7 @@ def test_scorer_workspace_size_validates_descriptions():
     ok = int(L.gambit_scorer_workspace_size(ctypes.byref(d)))
     # the per-slot key / value caches dominate: 512 x 2 layers x 4 heads x 2 x 64 x 256 fp32
     assert ok >= 512 * 2 * 4 * 2 * 64 * 256 * 4
-    for field, bad in [("d_model", 200), ("n_heads", 3), ("input_dim", 100), ("d_ff", 100), ("max_steps", 0),
+    for field, bad in [("d_model", 200), ("n_heads", 3), ("input_dim", 100), ("input_dim", 192), ("d_ff", 100), ("max_steps", 0),
                        ("max_steps", 9000), ("n_layers", -1), ("max_traces", 0)]:
         d2 = gambit.ScorerDesc.from_buffer_copy(d)
         setattr(d2, field, bad)

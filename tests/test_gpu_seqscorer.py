@@ -118,6 +118,32 @@ def test_errors_change_nothing():
     assert abs(got - ref.step([0], bf16_to_f64(H[5:6]))[0]) <= TOL
 
 
+def test_offset_step_states_and_one_input_chunk():
+    """Step states with a large common offset (mean 4, spread 0.5: the input
+    LayerNorm removes most of each state) and an input width of 128 (one
+    k chunk, one split), against the oracle, which normalises first; the
+    input LayerNorm's gains are drawn wide (0.1 to 3) and its biases large."""
+    import dataclasses
+    from workload.generate import to_bf16_bits
+    cfg = dataclasses.replace(SEQ_SMALL, input_dim=128, n_layers=1, max_steps=6, slots=8)
+    w = weights(cfg)
+    rng = np.random.default_rng(77)
+    w["ln_in_g"] = rng.uniform(0.1, 3.0, cfg.input_dim).astype(np.float32)
+    w["ln_in_b"] = rng.normal(0.0, 1.0, cfg.input_dim).astype(np.float32)
+    gpu = Scorer(w, n_heads=cfg.n_heads, max_steps=cfg.max_steps, max_traces=cfg.slots)
+    hist = {t: [] for t in range(cfg.slots)}
+    for r in range(cfg.max_steps):
+        ids = list(range(cfg.slots)) if r % 2 == 0 else [1, 6, 3]
+        x = 4.0 + 0.5 * bf16_to_f64(step_states(cfg, r)[ids])
+        H = to_bf16_bits(x.astype(np.float32))
+        got = gpu.step(ids, _bf16(H)).cpu().numpy()
+        for i, t in enumerate(ids):
+            hist[t].append(bf16_to_f64(H[i]))
+            want = scorer_outputs(w, np.stack(hist[t]), cfg.n_heads)[-1]
+            assert abs(got[i] - want) <= TOL, (r, t, got[i], want)
+    gpu.check()
+
+
 def test_no_layers_and_single_step_capacity():
     """The scorer without Transformer layers (input LN, projection, GELU,
     output head) and a history capacity of one step."""
