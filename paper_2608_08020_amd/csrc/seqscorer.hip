@@ -367,9 +367,10 @@ __global__ __launch_bounds__(256) void prep_input_kernel(const float* w, const f
 // max_steps rounded up to a multiple of 4), so one group's 64 dimensions
 // are 1 KB of consecutive memory and four consecutive steps of a dimension
 // one 16-byte load; values [ks][64].  Scores of the earlier steps: thread
-// (j4, eq) takes steps 4 j4 .. 4 j4 + 3 over dimensions 8 eq .. 8 eq + 7
-// (128 consecutive bytes; the first group's loads are issued before wave 0
-// has finished the append, which they do not depend on), and the eight
+// (j4, eq) takes steps 4 j4 .. 4 j4 + 3 over dimensions eq + 8 e, e < 8
+// (the eight threads of a group read 128 consecutive bytes per load, so a
+// wave's load touches eight whole lines; the first group's loads are issued
+// before wave 0 has finished the append, which they do not depend on), and the eight
 // parts are added by shuffles; steps past t - 1 in the last group are
 // masked (their slots are read but never used).  The softmax is taken over
 // steps 0..t; for the values, thread (g, c) takes dimensions 4 c .. 4 c + 3
@@ -406,9 +407,9 @@ __global__ __launch_bounds__(256) void seq_attn_kernel(SeqDev S, int layer, cons
   // the first group of earlier steps' keys, before the append (disjoint slots)
   float4 kv[8];
   if (4 * jq < t) {
-    const float* kr = kq + (size_t)jq * 256 + 32 * eq;
+    const float* kr = kq + (size_t)jq * 256 + 4 * eq;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) kv[e] = *reinterpret_cast<const float4*>(kr + 4 * e);
+    for (int e = 0; e < 8; ++e) kv[e] = *reinterpret_cast<const float4*>(kr + 32 * e);
   }
   float v = 0.f, st = 0.f;
   if (wave == 0) {
@@ -431,14 +432,14 @@ __global__ __launch_bounds__(256) void seq_attn_kernel(SeqDev S, int layer, cons
   float mx = -INFINITY;
   for (int j0 = 4 * jq; j0 < t; j0 += 128) {  // 32 groups of four steps per pass
     if (j0 != 4 * jq) {
-      const float* kr = kq + (size_t)(j0 >> 2) * 256 + 32 * eq;
+      const float* kr = kq + (size_t)(j0 >> 2) * 256 + 4 * eq;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) kv[e] = *reinterpret_cast<const float4*>(kr + 4 * e);
+      for (int e = 0; e < 8; ++e) kv[e] = *reinterpret_cast<const float4*>(kr + 32 * e);
     }
     float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const float qe = qs[8 * eq + e];
+      const float qe = qs[eq + 8 * e];
       a.x = fmaf(qe, kv[e].x, a.x);
       a.y = fmaf(qe, kv[e].y, a.y);
       a.z = fmaf(qe, kv[e].z, a.z);
