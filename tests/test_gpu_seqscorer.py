@@ -144,6 +144,27 @@ def test_offset_step_states_and_one_input_chunk():
     gpu.check()
 
 
+def test_wide_model_six_heads_three_output_splits():
+    """d_model 384 (six heads): the reduces' column loops take a second pass
+    past 256 columns, and W_o / W_2 split their K three ways (d_ff 384);
+    every step against the oracle, a fork on the way."""
+    import dataclasses
+    cfg = dataclasses.replace(SEQ_SMALL, d_model=384, n_heads=6, d_ff=384, max_steps=10, slots=6)
+    _, gpu, ref = _make(cfg)
+    ids = [0, 1, 2, 3]
+    for r in range(8):
+        if r == 4:
+            gpu.fork([2], [5])
+            ref.fork([2], [5])
+            ids = [0, 1, 2, 3, 5]
+        H = step_states(cfg, r)[ids]
+        got = gpu.step(ids, _bf16(H)).cpu().numpy()
+        want = ref.step(ids, bf16_to_f64(H))
+        assert float(np.abs(got - want).max()) <= TOL, r
+    assert [gpu.steps(t) for t in range(cfg.slots)] == [len(h) for h in ref.hist]
+    gpu.check()
+
+
 def test_no_layers_and_single_step_capacity():
     """The scorer without Transformer layers (input LN, projection, GELU,
     output head) and a history capacity of one step."""
