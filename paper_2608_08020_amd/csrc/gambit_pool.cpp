@@ -576,9 +576,15 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
   // Workgroup slots of four entries per XCD: a cooperative item (repeated
   // four times, flagged) or four narrow units.  The two kinds are interleaved
   // in proportion so compute-bound and HBM-bound workgroups share every CU,
-  // the cooperative items over the first 85% of the narrow slots: they are
-  // the long ones, and one that starts late ends the launch late (measured:
-  // 853 vs 858 us at 512 traces; 50% starts too few narrow units early).
+  // the cooperative items over the first part of the narrow slots: they are
+  // the long ones, and one that starts late ends the launch late.  bf16
+  // (bound by HBM): over the first 85% (853 vs 858 us at 512 traces with all
+  // of them; 50% starts too few narrow units early there: 947 vs 936-939 us,
+  // though at 256 traces it gives 268 vs 273 us).
+  // fp8 (bound by instruction issue, where the cooperative items' share of
+  // the work starting early matters more than the overlap): over the first
+  // 50% (217-220 vs 233-241 us at 256 traces; 45%: 226, 55%: 228, 70%: 224).
+  const long spread_pct = p->d.kv_dtype == GAMBIT_KV_FP8_E4M3 ? 50 : 85;
   std::vector<AttnUnit> units;
   units.reserve(4 * gunits.size() + 8 * gambit::kUnitsPerWG);  // a cooperative item fills a 4-entry slot
   const AttnUnit empty{0, 0, 0, 0, 0, 0, 0, 0};
@@ -594,7 +600,7 @@ gambit_status build_plan(gambit_pool* p, int n, const int32_t* ids, hipStream_t 
     const long nC = (long)C.size(), nN = cdiv((int)N.size(), gambit::kUnitsPerWG);
     long ci = 0, ni = 0;
     while (ci < nC || ni < nN) {
-      if (ni >= nN || (ci < nC && ci * std::max(1L, nN * 85 / 100) <= ni * nC)) {
+      if (ni >= nN || (ci < nC && ci * std::max(1L, nN * spread_pct / 100) <= ni * nC)) {
         for (int w = 0; w < gambit::kUnitsPerWG; ++w) units.push_back(C[ci]);
         ++ci;
       } else {
