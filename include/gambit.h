@@ -436,6 +436,7 @@ typedef struct {
 } gambit_scorer_desc;
 
 size_t gambit_scorer_workspace_size(const gambit_scorer_desc* desc);
+/* Set-up work runs on `stream`; create returns after it has finished. */
 gambit_status gambit_scorer_create(const gambit_scorer_desc* desc, void* stream, gambit_scorer** out);
 gambit_status gambit_scorer_destroy(gambit_scorer* scorer);
 

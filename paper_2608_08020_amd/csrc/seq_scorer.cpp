@@ -186,6 +186,9 @@ gambit_status gambit_scorer_create(const gambit_scorer_desc* desc, void* stream,
   } else if (e == hipSuccess) {
     e = hipErrorUnknown;
   }
+  // the set-up is complete before create returns, so steps on any stream
+  // see the planes, the step counts and the error word
+  if (e == hipSuccess) e = hipStreamSynchronize(S(stream));
   if (e != hipSuccess) {
     gambit_scorer_destroy(q);
     return GAMBIT_ERR_DEVICE;
