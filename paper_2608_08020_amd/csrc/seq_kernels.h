@@ -21,7 +21,7 @@ __host__ __device__ constexpr int seq_kstride(int max_steps) { return (max_steps
 __host__ __device__ constexpr size_t seq_region_floats(int max_steps) {
   return (size_t)2 * 64 * seq_kstride(max_steps) + 64;
 }
-enum : int { kEpiNone = 0, kEpiGelu = 1, kEpiResid = 2, kEpiSwiGLU = 3 };
+enum : int { kEpiNone = 0, kEpiSwiGLU = 1 };
 
 struct SeqDev {
   const int32_t* ids;     // [n] listed trace slots, this boundary
@@ -37,9 +37,10 @@ struct SeqDev {
 
 // C = A W^T (fp32); N a multiple of 64, K / splits a multiple of 16.
 // part != NULL: the raw sums of the splits go to part[splits][M][N] (for
-// seq_reduce_ln); else one split, the epilogue applied and C written.
-hipError_t seq_gemm(const float* A, const float* W, float* C, int M, int N, int K, int splits, int epi,
-                    const float* R, float* part, hipStream_t s);
+// seq_reduce_ln); else one split, written to C as it is (kEpiNone) or
+// through the SwiGLU gate (kEpiSwiGLU).
+hipError_t seq_gemm(const float* A, const float* W, float* C, int M, int N, int K, int splits, int epi, float* part,
+                    hipStream_t s);
 // The input projection's bf16 planes [3][dm][dim] of W_in scaled by the
 // input LayerNorm's gain (hi + mid + lo equal it exactly), their row sums c
 // and dv = W_in b (one launch, at creation).
@@ -50,9 +51,10 @@ hipError_t seq_prep_input(const float* w_in, const float* ln_g, const float* ln_
 hipError_t seq_reduce_in(const uint16_t* h, int dim, const float* part, int splits, const float* c, const float* dv,
                          float* x, int d, const float* g, const float* b, float* u, bool head, const SeqDev& S,
                          float* scores, int n, hipStream_t s);
-// x = epi(sum of the splits of part) (R: the residual), then u = LN(x; g, b),
-// or with head the output head's scores and the step counts' advance.
-hipError_t seq_reduce_ln(const float* part, int splits, int epi, const float* R, float* x, int d, const float* g,
+// x = R + the sum of the splits of part (R, the residual, may be x itself),
+// then u = LN(x; g, b), or with head the output head's scores and the step
+// counts' advance.
+hipError_t seq_reduce_ln(const float* part, int splits, const float* R, float* x, int d, const float* g,
                          const float* b, float* u, bool head, const SeqDev& S, float* scores, int n, hipStream_t s);
 // parts[s][t][u] = the sum over split s's k range of h[t][k] w[u][k], bf16
 // operands and fp32 sums, for s < splits: the MLP scorer's split-k GEMM

@@ -242,28 +242,28 @@ gambit_status gambit_scorer_step(gambit_scorer* q, int32_t n, const int32_t* ids
                              head ? nullptr : d.ln1_g, head ? nullptr : d.ln1_b, u, head, q->dev, scores_out, n, s),
             "input projection reduce");
   }
-  auto reduce_ln = [&](int splits, int epi, const float* R, int next_ln1, const char* where) -> gambit_status {
+  auto reduce_ln = [&](int splits, const float* R, int next_ln1, const char* where) -> gambit_status {
     const bool head = next_ln1 >= d.n_layers;
     const float* g = head ? nullptr : d.ln1_g + (size_t)next_ln1 * dm;
     const float* b = head ? nullptr : d.ln1_b + (size_t)next_ln1 * dm;
-    SEQ_TRY(q, seq_reduce_ln(part, splits, epi, R, x, dm, g, b, u, head, q->dev, scores_out, n, s), where);
+    SEQ_TRY(q, seq_reduce_ln(part, splits, R, x, dm, g, b, u, head, q->dev, scores_out, n, s), where);
     return GAMBIT_OK;
   };
   for (int l = 0; l < d.n_layers; ++l) {
     const size_t dd = (size_t)dm * dm;
-    SEQ_TRY(q, seq_gemm(u, d.w_qkv + 3 * dd * l, qkv, n, 3 * dm, dm, 1, kEpiNone, nullptr, nullptr, s),
+    SEQ_TRY(q, seq_gemm(u, d.w_qkv + 3 * dd * l, qkv, n, 3 * dm, dm, 1, kEpiNone, nullptr, s),
             "QKV");
     SEQ_TRY(q, seq_attention(q->dev, l, qkv, o, n, s), "attention step");
-    SEQ_TRY(q, seq_gemm(o, d.w_o + dd * l, x, n, dm, dm, q->L.out_splits, kEpiNone, nullptr, part, s),
+    SEQ_TRY(q, seq_gemm(o, d.w_o + dd * l, x, n, dm, dm, q->L.out_splits, kEpiNone, part, s),
             "output projection");
-    SEQ_TRY(q, seq_reduce_ln(part, q->L.out_splits, kEpiResid, x, x, dm, d.ln2_g + (size_t)l * dm,
+    SEQ_TRY(q, seq_reduce_ln(part, q->L.out_splits, x, x, dm, d.ln2_g + (size_t)l * dm,
                              d.ln2_b + (size_t)l * dm, u, false, q->dev, scores_out, n, s),
             "output projection reduce, LN2");
-    SEQ_TRY(q, seq_gemm(u, d.w_13 + 2 * (size_t)f * dm * l, g, n, 2 * f, dm, 1, kEpiSwiGLU, nullptr, nullptr, s),
+    SEQ_TRY(q, seq_gemm(u, d.w_13 + 2 * (size_t)f * dm * l, g, n, 2 * f, dm, 1, kEpiSwiGLU, nullptr, s),
             "SwiGLU");
-    SEQ_TRY(q, seq_gemm(g, d.w_2 + (size_t)f * dm * l, x, n, dm, f, q->L.out_splits, kEpiNone, nullptr, part, s),
+    SEQ_TRY(q, seq_gemm(g, d.w_2 + (size_t)f * dm * l, x, n, dm, f, q->L.out_splits, kEpiNone, part, s),
             "SwiGLU out");
-    st = reduce_ln(q->L.out_splits, kEpiResid, x, l + 1, "SwiGLU out reduce, next LayerNorm");
+    st = reduce_ln(q->L.out_splits, x, l + 1, "SwiGLU out reduce, next LayerNorm");
     if (st) return st;
   }
   for (int i = 0; i < n; ++i) ++q->lens[ids[i]];

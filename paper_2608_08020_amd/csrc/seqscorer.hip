@@ -78,7 +78,7 @@ constexpr int kKC = 128;       // k per staged chunk
 constexpr int kKP = kKC + 4;   // padded LDS row, floats
 template <int TM>
 __global__ __launch_bounds__(256) void gemm_kernel(const float* A, const float* W, float* C, int M, int N, int K,
-                                                   int ks, int epi, const float* R, float* part) {
+                                                   int ks, int epi, float* part) {
   constexpr int MB = TM / 32;                    // 16-row blocks per wave
   constexpr int AV = TM * (kKC / 4) / 256;       // float4 groups of A per thread and chunk
   constexpr int WV = 64 * (kKC / 4) / 256;       // of W
@@ -140,7 +140,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const float* A, const float* 
         }
     }
   }
-  if (epi == kEpiSwiGLU) {  // one split, no residual
+  if (epi == kEpiSwiGLU) {  // one split
     const int f = N / 2, c = (n0 + wn) / 32;
 #pragma unroll
     for (int i = 0; i < MB; ++i)
@@ -164,25 +164,22 @@ __global__ __launch_bounds__(256) void gemm_kernel(const float* A, const float* 
         if (m >= M) continue;
         const size_t o = (size_t)m * N + n;
         float v = acc[i][j][r];
-        if (split) {
+        if (split)
           part[(size_t)blockIdx.z * M * N + o] = v;
-          continue;
-        }
-        if (epi == kEpiGelu) v = gelu_erf(v);
-        else if (epi == kEpiResid) v += R[o];
-        C[o] = v;
+        else
+          C[o] = v;
       }
 }
 
 // One workgroup per row of a K-split projection (width d, a multiple of 64;
 // thread c takes columns c + 256 k): the splits' partial sums added in split
 // order (loaded eight splits at a time, indices clamped so all eight loads
-// are in flight together), the epilogue (GELU, or the residual R added), the
-// row x written; then the LayerNorm of x (mean, then the mean squared
-// deviation, each a fixed reduction over the workgroup): head == 0 writes
-// u = LN(x) with gain g, bias b; head != 0 takes LN_out and the output head,
-// scores[row] = sigmoid(w_out . LN_out(x)), and advances the trace's step
-// count.  Each thread re-reads only the columns it wrote.
+// are in flight together), the residual R added, the row x written; then
+// the LayerNorm of x (mean, then the mean squared deviation, each a fixed
+// reduction over the workgroup): head == 0 writes u = LN(x) with gain g,
+// bias b; head != 0 takes LN_out and the output head, scores[row] =
+// sigmoid(w_out . LN_out(x)), and advances the trace's step count.  Each
+// thread re-reads only the columns it wrote.
 __device__ inline float block_sum(float v, float* red) {
   v = wave_sum(v);
   __syncthreads();  // red[] is free
@@ -216,7 +213,7 @@ __device__ inline void ln_tail(float s, const float* x, size_t base, int d, cons
   }
 }
 
-__global__ __launch_bounds__(256) void reduce_ln_kernel(const float* part, int splits, int epi, const float* R,
+__global__ __launch_bounds__(256) void reduce_ln_kernel(const float* part, int splits, const float* R,
                                                         float* x, int d, const float* g, const float* b, float* u,
                                                         int head, SeqDev S, float* scores, int n) {
   __shared__ float red[4];
@@ -233,8 +230,7 @@ __global__ __launch_bounds__(256) void reduce_ln_kernel(const float* part, int s
       for (int e = 0; e < 8; ++e)
         if (z0 + e < splits) y += v[e];
     }
-    if (epi == kEpiGelu) y = gelu_erf(y);
-    else if (epi == kEpiResid) y += R[base + i];
+    y += R[base + i];
     x[base + i] = y;
     s += y;
   }
@@ -539,16 +535,16 @@ __global__ void seq_set_len_kernel(SeqDev S, const int32_t* ids, int n, int valu
 
 }  // namespace
 
-hipError_t seq_gemm(const float* A, const float* W, float* C, int M, int N, int K, int splits, int epi,
-                    const float* R, float* part, hipStream_t s) {
+hipError_t seq_gemm(const float* A, const float* W, float* C, int M, int N, int K, int splits, int epi, float* part,
+                    hipStream_t s) {
   const int ks = K / splits;
   // 64-row tiles when they alone give the GPU ~256 workgroups, else 32-row
   const bool wide = (long)(N / 64) * ((M + 63) / 64) * splits >= 256;
   const dim3 grid(N / 64, wide ? (M + 63) / 64 : (M + 31) / 32, splits);
   if (wide)
-    hipLaunchKernelGGL((gemm_kernel<64>), grid, dim3(256), 0, s, A, W, C, M, N, K, ks, epi, R, part);
+    hipLaunchKernelGGL((gemm_kernel<64>), grid, dim3(256), 0, s, A, W, C, M, N, K, ks, epi, part);
   else
-    hipLaunchKernelGGL((gemm_kernel<32>), grid, dim3(256), 0, s, A, W, C, M, N, K, ks, epi, R, part);
+    hipLaunchKernelGGL((gemm_kernel<32>), grid, dim3(256), 0, s, A, W, C, M, N, K, ks, epi, part);
   return hipGetLastError();
 }
 
@@ -566,9 +562,9 @@ hipError_t seq_reduce_in(const uint16_t* h, int dim, const float* part, int spli
   return hipGetLastError();
 }
 
-hipError_t seq_reduce_ln(const float* part, int splits, int epi, const float* R, float* x, int d, const float* g,
+hipError_t seq_reduce_ln(const float* part, int splits, const float* R, float* x, int d, const float* g,
                          const float* b, float* u, bool head, const SeqDev& S, float* scores, int n, hipStream_t s) {
-  hipLaunchKernelGGL(reduce_ln_kernel, dim3(n), dim3(256), 0, s, part, splits, epi, R, x, d, g, b, u, (int)head, S,
+  hipLaunchKernelGGL(reduce_ln_kernel, dim3(n), dim3(256), 0, s, part, splits, R, x, d, g, b, u, (int)head, S,
                      scores, n);
   return hipGetLastError();
 }
